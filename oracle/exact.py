@@ -1,0 +1,129 @@
+"""Brute-force rational MixFP4 quantizer for tiny inputs.
+
+TEST INFRASTRUCTURE (oracle); see ``oracle/__init__``.
+
+An independent restatement of Algorithm 1 with Python ``Fraction``s that shares
+no code with ``oracle.quant`` or ``oracle.formats``: it enumerates its own
+codebooks from the value equation (Sec. 2.1, eq. (2)), rounds by scanning every
+code for the nearest value of the *exact* rational quotient, and evaluates both
+candidate errors as exact rational sums of squares (Algorithm 1's MSE).  It is
+slow (about a millisecond per block) and serves as a pin on the vectorised
+oracle, not as a second implementation of the GPU path.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+
+def _value(e: int, m: int, we: int, wm: int) -> Fraction:
+    bias = (1 << (we - 1)) - 1
+    if e:
+        return Fraction(2) ** (e - bias) * Fraction((1 << wm) + m, 1 << wm)
+    return Fraction(2) ** (1 - bias) * Fraction(m, 1 << wm)
+
+
+# (code, magnitude) lists; E1M2 carries the x2 INT4 remap (App. B.2).
+E2M1 = [(p, _value(p >> 1, p & 1, 2, 1)) for p in range(8)]
+E1M2X2 = [(p, 2 * _value(p >> 2, p & 3, 1, 2)) for p in range(8)]
+E4M3 = [(c, _value(c >> 3, c & 7, 4, 3)) for c in range(127)]
+
+
+def nearest(q: Fraction, book) -> tuple[int, Fraction]:
+    """Scan ``book`` for the entry nearest to q >= 0; ties go to the even code;
+    beyond the largest entry the largest is taken (it is then the nearest)."""
+    best = None
+    for code, v in book:
+        d = abs(q - v)
+        if best is None or d < best[0] or (d == best[0] and code % 2 == 0 and best[1] % 2 == 1):
+            best = (d, code, v)
+    return best[1], best[2]
+
+
+def round_f32(q: Fraction) -> Fraction:
+    """IEEE-754 binary32 round-to-nearest-even of a rational (finite range,
+    gradual underflow).  Written from the definition: find the binade, scale to
+    a 24-bit integer significand, round half to even."""
+    if q == 0:
+        return Fraction(0)
+    sgn = -1 if q < 0 else 1
+    a = abs(q)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    while Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    e = max(e, -126)                       # subnormals share the minimum exponent
+    scaled = a / Fraction(2) ** (e - 23)   # significand in units of the last place
+    n = scaled.numerator // scaled.denominator
+    rem = scaled - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return sgn * Fraction(n) * Fraction(2) ** (e - 23)
+
+
+def bf16_value(bits: int) -> Fraction:
+    """Exact value of a finite bf16 bit pattern (1-8-7 layout)."""
+    s, e, m = bits >> 15, (bits >> 7) & 0xFF, bits & 0x7F
+    assert e != 0xFF
+    v = _value(e, m, 8, 7)
+    return -v if s else v
+
+
+def quantize_block(xb_bits, s32: Fraction):
+    """Algorithm 1 on one 16-element block of bf16 bit patterns with a given s32.
+    Returns (scale_byte, [nibbles], err_e2m1, err_e1m2)."""
+    X = [bf16_value(int(b)) for b in xb_bits]
+    x = [round_f32(v / s32) for v in X]                      # X_FP8 in fp32
+    bm = max(abs(v) for v in x)
+    results = {}
+    for name, div, book in (("F", 6, E2M1), ("I", 7, E1M2X2)):
+        cand = round_f32(bm / div)                           # fp32 argument of FP8_E4M3
+        scode, s8 = nearest(cand, E4M3)
+        codes, err = [], Fraction(0)
+        for v in x:
+            if s8 == 0:
+                c, qv = 0, Fraction(0)
+            else:
+                c, qv = nearest(abs(v) / s8, book)           # exact quotient
+            d = qv * s8
+            err += (abs(v) - d) ** 2
+            codes.append(c)
+        results[name] = (scode, codes, err)
+    ef, ei = results["F"][2], results["I"][2]
+    t = 0 if ef < ei else 1
+    scode, mags, _ = results["I" if t else "F"]
+    nibs = [((int(b) >> 15) << 3) | c for b, c in zip(xb_bits, mags)]
+    return (t << 7) | scode, nibs, ef, ei
+
+
+def tensor_scale(x_bits) -> Fraction:
+    amax = max((abs(bf16_value(int(b))) for b in x_bits), default=Fraction(0))
+    if amax == 0:
+        return Fraction(1)
+    return round_f32(amax / 2688)
+
+
+def quantize(x_bits_2d, s32=None):
+    """Brute-force Algorithm 1 on a small [rows, K] uint16 array.  Returns
+    (codes bytes [rows][K/2], scale bytes [rows][K/16], s32 Fraction)."""
+    rows = [list(map(int, r)) for r in x_bits_2d]
+    flat = [b for r in rows for b in r]
+    s = tensor_scale(flat) if s32 is None else Fraction(s32)
+    codes, scales = [], []
+    for r in rows:
+        crow, srow = [], []
+        for j in range(0, len(r), 16):
+            sb, nibs, _, _ = quantize_block(r[j:j + 16], s)
+            srow.append(sb)
+            crow.extend(nibs[i] | (nibs[i + 1] << 4) for i in range(0, 16, 2))
+        codes.append(crow)
+        scales.append(srow)
+    return codes, scales, s
+
+
+def decode_value(nibble: int, scale_byte: int) -> Fraction:
+    """Exact s8 * v(code, T) * sign for one element (App. B.2-B.3)."""
+    t = scale_byte >> 7
+    s8 = E4M3[scale_byte & 0x7F][1]
+    mag = (E1M2X2 if t else E2M1)[nibble & 7][1]
+    return (-1 if nibble & 8 else 1) * mag * s8

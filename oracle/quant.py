@@ -1,0 +1,181 @@
+"""Algorithm 1 (MixFP4 data type quantization) and its inverse, on the CPU.
+
+TEST INFRASTRUCTURE (oracle); see ``oracle/__init__``.
+
+Follows, in order:
+  Algorithm 1, tensor-scale step: s32 = max|X| / 2688 (2688 = 6*448 = 7*384).
+  Algorithm 1, FP8-domain step:   X_FP8 = X / s32.
+  Algorithm 1, E2M1 branch:       s8 = FP8_E4M3(block-max|X_FP8| / 6),
+                                  quantize to E2M1, dequantize, MSE.
+  Algorithm 1, E1M2 branch:       same with 7 and the E1M2 (x2, INT4) grid.
+  Algorithm 1, selection:         E2M1 if Err_E2M1 < Err_E1M2, else E1M2 and T = 1.
+  Sec. 3.2 / App. B.3:            T stored in bit 7 of the E4M3 block scale.
+  App. B.2:                       nibble = [s | p2 p1 p0].
+  App. B.1:                       blocks of V = 16 values along the reduction dim.
+
+Readings of passages the paper leaves open (all listed in the design notes):
+  * X_FP8 = fl32(X / s32) with IEEE fp32 division; s32 = fl32(amax / 2688),
+    or 1.0 when the tensor is all zero; a caller may supply s32 instead.
+  * FP8_E4M3 / FP4 rounding: nearest value, ties to even code, saturating.
+    The FP4 argument is the fp32 quotient fl32(|x| / s8); rounding that is the
+    same as rounding the exact quotient (checked by ``oracle.exact``).
+  * MSE compares the exact real sums of squared errors (the 1/16 cancels).
+  * The nibble's sign bit is the sign bit of X, also when the code is zero.
+  * Layout: element 2j in the low nibble of byte j; codes [rows, K/2],
+    scales [rows, K/16], both row-major.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from fractions import Fraction
+
+import numpy as np
+
+from . import formats as F
+
+BLOCK = 16
+TENSOR_DIVISOR = np.float32(2688.0)     # 6 * 448 = 7 * 384 (Algorithm 1)
+
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
+
+
+def tensor_scale(x_bits: np.ndarray) -> np.float32:
+    """Algorithm 1 tensor-scale step: fl32(max|X| / 2688), 1.0 for an all-zero X."""
+    x = bf16_to_f32(x_bits)
+    amax = np.float32(np.max(np.abs(x))) if x.size else np.float32(0)
+    if amax == 0:
+        return np.float32(1.0)
+    return np.float32(amax / TENSOR_DIVISOR)
+
+
+@dataclass
+class Quantized:
+    codes: np.ndarray      # uint8 [rows, K/2]
+    scales: np.ndarray     # uint8 [rows, K/16]
+    s32: np.float32
+    # diagnostics (not part of the format)
+    t: np.ndarray          # uint8 [rows, K/16] format bit
+    sf_code: np.ndarray    # E4M3 code of the E2M1 candidate scale
+    si_code: np.ndarray    # E4M3 code of the E1M2 candidate scale
+    delta: np.ndarray      # float64 Err_E2M1 - Err_E1M2 (sum form), exact
+
+
+def _exact_block_sums(terms: np.ndarray):
+    """Sum each row of exactly representable float64 ``terms``; also return a
+    mask of rows whose fp64 sum is provably exact.
+
+    A row is certified when all its nonzero terms are integer multiples of
+    2^u (u = lowest set bit over the row) and sum(|terms|) < 2^(u+53): every
+    partial sum is then an integer multiple of 2^u below 2^53 * 2^u, hence
+    representable, so no addition rounds."""
+    s = terms.sum(axis=-1)
+    nz = terms != 0
+    m, e = np.frexp(terms)
+    mi = np.abs(np.ldexp(m, 53)).astype(np.int64)
+    low = mi & (-mi)
+    lowexp = np.where(nz, e.astype(np.float64) - 53.0 + np.log2(np.maximum(low, 1).astype(np.float64)),
+                      np.inf)
+    u = lowexp.min(axis=-1)
+    total = np.abs(terms).sum(axis=-1) * (1.0 + 2.0 ** -40)
+    ok = np.isinf(u) | (total < np.ldexp(1.0, np.clip(u + 53, -1074, 1023).astype(np.int64)))
+    return s, ok
+
+
+def _fraction_sum(row) -> Fraction:
+    return sum((Fraction(float(t)) for t in row), Fraction(0))
+
+
+def quantize(x_bits: np.ndarray, s32=None) -> Quantized:
+    """Algorithm 1 on a bf16 tensor ``x_bits`` (uint16 [rows, K], K % 16 == 0).
+
+    ``s32`` None computes the tensor scale (Algorithm 1); otherwise the given
+    fp32 value is used as s32."""
+    x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    rows, k = x_bits.shape
+    assert k % BLOCK == 0
+    s32 = tensor_scale(x_bits) if s32 is None else np.float32(s32)
+    X = bf16_to_f32(x_bits)
+    x = (X / s32).astype(np.float32)                       # X_FP8, IEEE fp32 division
+    nb = k // BLOCK
+    xb = np.abs(x).reshape(rows, nb, BLOCK)
+    bm = xb.max(axis=-1)                                    # block-max |X_FP8|
+
+    def branch(divisor, grid):
+        cand = (bm / np.float32(divisor)).astype(np.float32)
+        code = F.e4m3_encode(cand.astype(np.float64))
+        s8 = F.e4m3_decode(code)                            # exact float64
+        s8_32 = s8.astype(np.float32)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            y = np.where(s8_32[..., None] > 0, xb / s8_32[..., None], np.float32(0)).astype(np.float32)
+        q = F.round_to_codebook(y.astype(np.float64), grid)
+        d = grid[q] * s8[..., None]                          # dequantized, exact in fp64
+        return code, s8, q, d
+
+    cf, sf, qf, df = branch(6, F.F_GRID)
+    ci, si, qi, di = branch(7, F.I_GRID)
+
+    # Err_E2M1 - Err_E1M2 = sum((x - Df)^2 - (x - Di)^2) = sum((Di - Df) * (2x - Df - Di)).
+    # Each term is exact in fp64; the block sum is certified exact or redone
+    # with rationals.
+    xd = xb.astype(np.float64)
+    terms = (di - df) * ((2.0 * xd - df) - di)
+    delta, ok = _exact_block_sums(terms.reshape(-1, BLOCK))
+    if not ok.all():
+        flat_terms = terms.reshape(-1, BLOCK)
+        for i in np.flatnonzero(~ok):
+            exact = _fraction_sum(flat_terms[i])
+            delta[i] = 0.0 if exact == 0 else (1.0 if exact > 0 else -1.0) * max(abs(float(exact)), 5e-324)
+    delta = delta.reshape(rows, nb)
+    t = (~(delta < 0)).astype(np.uint8)                    # E2M1 iff Err_E2M1 < Err_E1M2
+
+    mag = np.where(t[..., None] == 1, qi, qf).astype(np.uint8)
+    sign = (x_bits.reshape(rows, nb, BLOCK) >> 15).astype(np.uint8)
+    nib = (sign << 3) | mag
+    nib = nib.reshape(rows, k)
+    codes = (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+    scales = ((t << 7) | np.where(t == 1, ci, cf)).astype(np.uint8)
+    return Quantized(codes=codes, scales=scales, s32=s32, t=t,
+                     sf_code=cf.astype(np.uint8), si_code=ci.astype(np.uint8), delta=delta)
+
+
+def unpack_nibbles(codes: np.ndarray) -> np.ndarray:
+    """uint8 [rows, K/2] -> uint8 [rows, K] nibbles (element 2j = low nibble)."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    rows, half = codes.shape
+    nib = np.empty((rows, half * 2), dtype=np.uint8)
+    nib[:, 0::2] = codes & 0x0F
+    nib[:, 1::2] = codes >> 4
+    return nib
+
+
+def decode_unit(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """s8 * v(code, T) * sign as exact float64 (the per-element value before the
+    tensor scale).  T (scale bit 7) selects the E2M1 or INT4 magnitude; the
+    scale magnitude is bits 6:0 (App. B.3)."""
+    nib = unpack_nibbles(codes)
+    rows, k = nib.shape
+    scales = np.asarray(scales, dtype=np.uint8)
+    t = np.repeat((scales >> 7).astype(np.int64), BLOCK, axis=1)
+    s8 = np.repeat(F.e4m3_decode(scales & 0x7F), BLOCK, axis=1)
+    mag = (nib & 7).astype(np.int64)
+    v = np.where(t == 1, F.I_GRID[mag], F.F_GRID[mag])
+    sgn = np.where(nib & 8, -1.0, 1.0)
+    return sgn * v * s8
+
+
+def dequantize(codes, scales, s32=None) -> np.ndarray:
+    """fl32(s32 * (s8 * v)); s8 * v is exact, so this rounds once.  ``s32`` None
+    gives the FP8-domain values (scale 1.0)."""
+    unit = decode_unit(codes, scales)
+    s = 1.0 if s32 is None else float(np.float32(s32))
+    return (unit * s).astype(np.float32)
+
+
+def dequantize_exact(codes, scales, s32=None) -> np.ndarray:
+    """s32 * s8 * v in float64 without the final fp32 rounding (exact: at most
+    24 + 4 + 3 significant bits)."""
+    unit = decode_unit(codes, scales)
+    s = 1.0 if s32 is None else float(np.float32(s32))
+    return unit * s

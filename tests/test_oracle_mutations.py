@@ -1,0 +1,127 @@
+"""Planted mistakes: each test breaks the CPU oracle in one plausible way
+(monkeypatched, on the CPU only) and checks that the pins above catch it.
+This guards the pins themselves: a pin set that passes a broken oracle would
+not be evidence of anything."""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+from oracle import exact as E
+from oracle import formats as F
+from oracle import quant as Q
+from tests._golden import handworked_blocks
+from workloads import f32_to_bf16_bits
+
+
+def _pins_pass() -> bool:
+    """Hand-worked blocks plus brute-force agreement on a small mixed tensor."""
+    cases = handworked_blocks()
+    bits = f32_to_bf16_bits(np.stack([c["block"] for c in cases]))
+    q = Q.quantize(bits, s32=1.0)
+    for i, c in enumerate(cases):
+        if q.scales[i, 0] != c["scale"] or bytes(q.codes[i]) != c["codes"]:
+            return False
+    rng = np.random.default_rng(99)
+    x = rng.standard_t(3, (8, 64)).astype(np.float32)
+    x[0, :16] = -0.0
+    x[1, :16] = np.arange(16) * 0.25
+    x[2, :16] = rng.integers(-7, 8, 16)
+    bits = f32_to_bf16_bits(x)
+    q = Q.quantize(bits)
+    codes, scales, s = E.quantize(bits)
+    return (np.array_equal(q.codes, np.array(codes, np.uint8))
+            and np.array_equal(q.scales, np.array(scales, np.uint8))
+            and Fraction(float(q.s32)) == s)
+
+
+def test_unmutated_pins_pass():
+    assert _pins_pass()
+
+
+def test_catches_ties_to_lower_code(monkeypatch):
+    orig = F.round_to_codebook
+
+    def ties_down(y, values):
+        idx = orig(y, values)
+        y = np.asarray(y, np.float64)
+        lo = np.maximum(idx - 1, 0)
+        tie = (idx > 0) & (values[idx] - y == y - values[lo])
+        return np.where(tie, lo, idx)
+
+    monkeypatch.setattr(F, "round_to_codebook", ties_down)
+    assert not _pins_pass()
+
+
+def test_catches_selection_tie_to_e2m1(monkeypatch):
+    orig = Q.quantize
+
+    def mutated(x_bits, s32=None):
+        q = orig(x_bits, s32)
+        flip = (q.delta == 0)
+        q.scales = np.where(flip, q.sf_code, q.scales).astype(np.uint8)
+        return q
+
+    monkeypatch.setattr(Q, "quantize", mutated)
+    assert not _pins_pass()
+
+
+def test_catches_swapped_divisors(monkeypatch):
+    orig_encode = F.e4m3_encode
+    calls = {"n": 0}
+
+    def swapped(v):
+        # first call is the E2M1 branch (bm/6): feed it bm/7 instead, and vice versa
+        calls["n"] += 1
+        factor = 6.0 / 7.0 if calls["n"] % 2 == 1 else 7.0 / 6.0
+        return orig_encode(np.asarray(v, np.float64) * factor)
+
+    monkeypatch.setattr(F, "e4m3_encode", swapped)
+    assert not _pins_pass()
+
+
+def test_catches_nibble_order(monkeypatch):
+    orig = Q.quantize
+
+    def mutated(x_bits, s32=None):
+        q = orig(x_bits, s32)
+        q.codes = ((q.codes >> 4) | (q.codes << 4)).astype(np.uint8)
+        return q
+
+    monkeypatch.setattr(Q, "quantize", mutated)
+    assert not _pins_pass()
+
+
+def test_catches_missing_int4_remap(monkeypatch):
+    monkeypatch.setattr(F, "I_GRID", F.I_GRID / 2)
+    assert not _pins_pass()
+
+
+def test_catches_dropped_zero_sign(monkeypatch):
+    orig = Q.quantize
+
+    def mutated(x_bits, s32=None):
+        q = orig(x_bits, s32)
+        nib = Q.unpack_nibbles(q.codes)
+        nib = np.where((nib & 7) == 0, 0, nib).astype(np.uint8)
+        q.codes = (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+        return q
+
+    monkeypatch.setattr(Q, "quantize", mutated)
+    assert not _pins_pass()
+
+
+def test_catches_inverted_selection(monkeypatch):
+    orig = Q._exact_block_sums
+
+    def neg(terms):
+        s, ok = orig(terms)
+        return -s, ok
+
+    monkeypatch.setattr(Q, "_exact_block_sums", neg)
+    assert not _pins_pass()
+
+
+def test_catches_wrong_tensor_divisor(monkeypatch):
+    monkeypatch.setattr(Q, "TENSOR_DIVISOR", np.float32(2687.0))
+    assert not _pins_pass()
