@@ -1,0 +1,132 @@
+/*
+ * mixfp4.h - C ABI of the MixFP4 quantizer, dequantizer and block-scaled GEMM
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * MixFP4 (Sec. 3.2 of the paper) stores a tensor as
+ *   - 4-bit codes [s | p2 p1 p0] (App. B.2), two per byte, element 2j in the
+ *     low nibble of byte j; one row of K elements takes K/2 bytes;
+ *   - one scale byte per 16 consecutive elements along K (App. B.1, V = 16):
+ *     bits 6:0 are an unsigned E4M3 (OCP E4M3FN) magnitude, bit 7 is the
+ *     format type T (App. B.3): T = 0 -> the block's codes are E2M1
+ *     (magnitudes {0,.5,1,1.5,2,3,4,6}), T = 1 -> E1M2 read through the x2
+ *     INT4 remap (magnitudes {0,...,7}) (Sec. 3.1, App. B.2);
+ *   - one fp32 per-tensor scale s32 (Sec. 2.1, Algorithm 1).
+ * An element decodes to s32 * E4M3(scale & 0x7F) * v(code, T) * sign.
+ *
+ * General conventions for every entry point:
+ *   - Every pointer argument is DEVICE memory owned by the caller.  The
+ *     library never allocates, frees or synchronizes; it only enqueues
+ *     kernels on `stream` (a hipStream_t; NULL means the default stream).
+ *   - Arguments are checked on the host before anything is enqueued; on any
+ *     error the function returns a nonzero mixfp4_status and the stream is
+ *     left untouched.  A failed kernel launch returns MIXFP4_ERR_LAUNCH.
+ *     Faults inside kernels surface at the caller's next synchronization.
+ *   - Outputs must not alias inputs.  Calls are reentrant; calls that write
+ *     the same outputs from different streams race.
+ *   - Inputs must be finite (bf16 NaN / Inf are outside the contract).
+ *   - Matrices are row-major.  Scale rows are K/16 bytes, code rows K/2
+ *     bytes, both contiguous (no padding between rows).
+ */
+#ifndef MIXFP4_H
+#define MIXFP4_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MIXFP4_OK = 0,
+  MIXFP4_ERR_NULL = 1,    /* a required pointer is NULL                      */
+  MIXFP4_ERR_SHAPE = 2,   /* negative size, K % 16 != 0, ldx < K, ldx % 8    */
+  MIXFP4_ERR_ALIGN = 3,   /* a pointer misses its required alignment         */
+  MIXFP4_ERR_FLAGS = 4,   /* unknown flag bits                               */
+  MIXFP4_ERR_LAUNCH = 5   /* the HIP runtime rejected a kernel launch        */
+} mixfp4_status;
+
+/* Tensor-scale modes of mixfp4_quantize (flags argument). */
+#define MIXFP4_SCALE_COMPUTE 0u /* compute s32 = max|X| / 2688 on the device  */
+#define MIXFP4_SCALE_GIVEN 1u   /* read s32 from *tensor_scale                */
+
+/*
+ * mixfp4_quantize - Algorithm 1 ("MixFP4 data type quantization") on a bf16
+ * matrix X [rows, k] with row pitch ldx elements.
+ *
+ * For each row and each block of 16 consecutive elements along k it computes
+ * x = X / s32 in fp32 (the "FP8 domain"), the block maximum |x|, the two E4M3
+ * candidate scales E4M3(max/6) and E4M3(max/7), quantizes the block to the
+ * E2M1 grid and to the E1M2 (x2, INT4) grid, keeps E2M1 when its squared
+ * error is strictly smaller and E1M2 otherwise (ties pick E1M2), stores T in
+ * bit 7 of the scale byte and packs the codes (Sec. 3.2, App. B.3).  Rounding
+ * is to nearest with ties to the even code, saturating; a code's sign bit is
+ * the sign bit of X (also for a zero magnitude).  The result is bit-identical
+ * to the CPU oracle and deterministic.
+ *
+ *   x            bf16 bit patterns, rows x ldx, 16-byte aligned; only the
+ *                first k of each row are read.  ldx >= k, ldx % 8 == 0.
+ *   rows, k      rows >= 0, k >= 0, k % 16 == 0.  rows * k == 0 writes no
+ *                codes (and s32 = 1.0 in COMPUTE mode).
+ *   codes        out, rows * k/2 bytes, 16-byte aligned.
+ *   scales       out, rows * k/16 bytes, any alignment.
+ *   tensor_scale 1 float, 4-byte aligned.  COMPUTE: written with
+ *                fl32(max|X| / 2688), or 1.0f if X is all zero (Algorithm 1).
+ *                GIVEN: read; must be finite and > 0.
+ *   flags        MIXFP4_SCALE_COMPUTE or MIXFP4_SCALE_GIVEN.
+ */
+int mixfp4_quantize(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
+                    uint8_t *codes, uint8_t *scales, float *tensor_scale,
+                    unsigned flags, void *stream);
+
+/*
+ * mixfp4_dequantize - decode MixFP4 back to fp32 (App. B.2-B.3):
+ *   out[r, i] = fl32(s32 * (E4M3(scale & 0x7F) * v(code, T))) * sign,
+ * where the inner product is exact, so each output is rounded once.
+ *
+ *   codes, scales  as written by mixfp4_quantize for a [rows, k] matrix
+ *                  (codes 16-byte aligned).
+ *   tensor_scale   1 float (4-byte aligned), or NULL for 1.0 (the output is
+ *                  then in Algorithm 1's FP8 domain).
+ *   rows, k        rows >= 0, k >= 0, k % 16 == 0.
+ *   out            out, rows * k floats, contiguous, 16-byte aligned.
+ */
+int mixfp4_dequantize(const uint8_t *codes, const uint8_t *scales,
+                      const float *tensor_scale, int64_t rows, int64_t k,
+                      float *out, void *stream);
+
+/*
+ * mixfp4_gemm - C[m, n] = sum_k A[m, k] * W[n, k] for two MixFP4 operands
+ * (C = A W^T, both quantized along the reduction dimension K, App. B.1).
+ * Each element is decoded through the unified E2M2 value set (Sec. 3.3,
+ * App. B.5) to an exact bf16 value E4M3 * v, the products accumulate in fp32
+ * on the matrix cores, and the epilogue multiplies by s32_A * s32_W.
+ * Accuracy: |C - C_exact| <= 1e-5 * sum_k |A_hat * W_hat| + 1e-6, where
+ * A_hat, W_hat are the exactly dequantized operands.
+ *
+ *   a_codes [m, k/2], a_scales [m, k/16], a_tensor_scale (NULL = 1.0)
+ *   w_codes [n, k/2], w_scales [n, k/16], w_tensor_scale (NULL = 1.0)
+ *   m, n, k        >= 0, k % 16 == 0; k == 0 writes zeros.
+ *   c              out, m * n floats, row-major, 4-byte aligned.
+ *   Code pointers 16-byte aligned; scale pointers any alignment.
+ */
+int mixfp4_gemm(const uint8_t *a_codes, const uint8_t *a_scales,
+                const float *a_tensor_scale, const uint8_t *w_codes,
+                const uint8_t *w_scales, const float *w_tensor_scale,
+                int64_t m, int64_t n, int64_t k, float *c, void *stream);
+
+/* Human-readable name of a mixfp4_status value (static storage). */
+const char *mixfp4_status_string(int status);
+
+/* HIP error string of the last MIXFP4_ERR_LAUNCH on the calling thread. */
+const char *mixfp4_last_launch_error(void);
+
+/* ABI version of this header (major * 100 + minor). */
+int mixfp4_abi_version(void);
+
+#define MIXFP4_ABI_VERSION 100
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MIXFP4_H */

@@ -1,0 +1,101 @@
+"""MixFP4 on MI355X: Python binding of libmixfp4.so.
+
+The binding only marshals arguments: torch supplies device memory and the
+current HIP stream, every step of the quantizer, dequantizer and GEMM runs in
+the library's HIP kernels.  There is no CPU fallback: if the library is
+missing or fails to load, importing the low-level handle raises.
+
+Functions (same names as the C ABI in include/mixfp4.h):
+  mixfp4_quantize(x, tensor_scale=None, out=None) -> (codes, scales, s32)
+  mixfp4_dequantize(codes, scales, tensor_scale=None) -> fp32 tensor
+  mixfp4_gemm(a, w) -> C = A W^T (fp32), a/w are (codes, scales, s32) triples
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+from ._lib import LIB_PATH, MixFP4Error, lib
+
+__all__ = ["mixfp4_quantize", "mixfp4_dequantize", "mixfp4_gemm", "MixFP4Error",
+           "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN"]
+
+SCALE_COMPUTE = 0
+SCALE_GIVEN = 1
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def _check(status: int):
+    if status != 0:
+        msg = lib.mixfp4_status_string(status).decode()
+        if status == 5:
+            msg += ": " + lib.mixfp4_last_launch_error().decode()
+        raise MixFP4Error(status, msg)
+
+
+def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
+                    codes: torch.Tensor | None = None, scales: torch.Tensor | None = None,
+                    scale_out: torch.Tensor | None = None):
+    """Quantize a bf16 [rows, k] CUDA tensor (Algorithm 1).
+
+    ``tensor_scale`` None computes s32 = max|X| / 2688 on the device (into
+    ``scale_out`` if given); a 1-element fp32 tensor is used as the given s32.
+    Returns (codes uint8 [rows, k/2], scales uint8 [rows, k/16], s32 fp32 [1])."""
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_cuda:
+        raise ValueError("x must be a 2-D bfloat16 CUDA tensor")
+    if x.stride(1) != 1:
+        raise ValueError("x must have unit stride along K")
+    rows, k = x.shape
+    dev = x.device
+    if codes is None:
+        codes = torch.empty((rows, k // 2), dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty((rows, k // 16), dtype=torch.uint8, device=dev)
+    if tensor_scale is None:
+        ts = scale_out if scale_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
+        flags = SCALE_COMPUTE
+    else:
+        ts = tensor_scale
+        flags = SCALE_GIVEN
+    st = lib.mixfp4_quantize(_ptr(x), rows, k, x.stride(0) if rows > 0 else k, _ptr(codes),
+                             _ptr(scales), _ptr(ts), flags, _stream(dev))
+    _check(st)
+    return codes, scales, ts
+
+
+def mixfp4_dequantize(codes: torch.Tensor, scales: torch.Tensor,
+                      tensor_scale: torch.Tensor | None = None) -> torch.Tensor:
+    """Decode MixFP4 to fp32 [rows, k]; ``tensor_scale`` None decodes in the
+    FP8 domain (s32 = 1)."""
+    rows, half = codes.shape
+    k = half * 2
+    out = torch.empty((rows, k), dtype=torch.float32, device=codes.device)
+    st = lib.mixfp4_dequantize(_ptr(codes), _ptr(scales), _ptr(tensor_scale), rows, k,
+                               _ptr(out), _stream(codes.device))
+    _check(st)
+    return out
+
+
+def mixfp4_gemm(a, w, out: torch.Tensor | None = None) -> torch.Tensor:
+    """C = A W^T for MixFP4 operands given as (codes, scales, s32) triples
+    (s32 may be None for 1.0).  Returns fp32 [m, n]."""
+    ac, asc, ats = a
+    wc, wsc, wts = w
+    m, n, k = ac.shape[0], wc.shape[0], ac.shape[1] * 2
+    if wc.shape[1] * 2 != k:
+        raise ValueError("A and W disagree on K")
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=ac.device)
+    st = lib.mixfp4_gemm(_ptr(ac), _ptr(asc), _ptr(ats), _ptr(wc), _ptr(wsc), _ptr(wts),
+                         m, n, k, _ptr(out), _stream(ac.device))
+    _check(st)
+    return out

@@ -1,0 +1,46 @@
+"""ctypes handle on libmixfp4.so with the C ABI's argument types.
+
+Loading fails loudly: there is no pure-Python or CPU implementation of the
+path behind this handle.  torch must be imported first so that the library
+binds to the HIP runtime torch already loaded (same soname).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # noqa: F401  (loads the HIP runtime the library binds to)
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmixfp4.so")
+
+SYMBOLS = ("mixfp4_quantize", "mixfp4_dequantize", "mixfp4_gemm", "mixfp4_status_string",
+           "mixfp4_last_launch_error", "mixfp4_abi_version")
+
+
+class MixFP4Error(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(msg)
+        self.status = status
+
+
+def load(path: str = LIB_PATH) -> ctypes.CDLL:
+    if not os.path.exists(path):
+        raise ImportError(f"{path} not found: build it with `python -m paper_2605_31035_amd.build`")
+    h = ctypes.CDLL(path)
+    vp, i64, u32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint, ctypes.c_int
+    h.mixfp4_quantize.argtypes = [vp, i64, i64, i64, vp, vp, vp, u32, vp]
+    h.mixfp4_quantize.restype = i32
+    h.mixfp4_dequantize.argtypes = [vp, vp, vp, i64, i64, vp, vp]
+    h.mixfp4_dequantize.restype = i32
+    h.mixfp4_gemm.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, vp, vp]
+    h.mixfp4_gemm.restype = i32
+    h.mixfp4_status_string.argtypes = [i32]
+    h.mixfp4_status_string.restype = ctypes.c_char_p
+    h.mixfp4_last_launch_error.argtypes = []
+    h.mixfp4_last_launch_error.restype = ctypes.c_char_p
+    h.mixfp4_abi_version.argtypes = []
+    h.mixfp4_abi_version.restype = i32
+    return h
+
+
+lib = load()

@@ -1,0 +1,96 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/mixfp4.h declares, and rejects bad arguments on the host before
+anything reaches a GPU (no kernel is launched by these calls)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mixfp4.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mixfp4_\w+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2605_31035_amd import _lib
+    return _lib.lib
+
+
+def test_exports_every_declared_symbol(lib):
+    names = _declared()
+    assert {"mixfp4_quantize", "mixfp4_dequantize", "mixfp4_gemm"} <= set(names)
+    for name in names:
+        assert hasattr(lib, name), name
+    from paper_2605_31035_amd import _lib
+    assert set(_lib.SYMBOLS) == set(names)
+
+
+def test_abi_version(lib):
+    v = re.search(r"#define MIXFP4_ABI_VERSION (\d+)", open(HEADER).read()).group(1)
+    assert lib.mixfp4_abi_version() == int(v)
+
+
+def test_status_strings(lib):
+    for st, key in [(0, b"OK"), (1, b"NULL"), (2, b"SHAPE"), (3, b"ALIGN"), (4, b"FLAGS"), (5, b"LAUNCH")]:
+        assert key in lib.mixfp4_status_string(st)
+    assert b"unknown" in lib.mixfp4_status_string(99)
+
+
+P = ctypes.c_void_p
+A16 = P(0x10000)          # a fake, 16-byte aligned address: never dereferenced
+A4 = P(0x10004)
+
+
+def q(lib, x=A16, rows=4, k=32, ldx=32, codes=A16, scales=A16, ts=A16, flags=0):
+    return lib.mixfp4_quantize(x, rows, k, ldx, codes, scales, ts, flags, None)
+
+
+def test_quantize_rejects(lib):
+    assert q(lib, flags=7) == 4
+    assert q(lib, k=24) == 2
+    assert q(lib, k=-16) == 2
+    assert q(lib, rows=-1) == 2
+    assert q(lib, ldx=16) == 2            # ldx < k
+    assert q(lib, ldx=36) == 2            # ldx % 8
+    assert q(lib, ts=P(0)) == 1
+    assert q(lib, x=P(0)) == 1
+    assert q(lib, codes=P(0)) == 1
+    assert q(lib, scales=P(0)) == 1
+    assert q(lib, x=P(0x10008)) == 3
+    assert q(lib, codes=P(0x10008)) == 3
+    assert q(lib, ts=P(0x10002)) == 3
+
+
+def test_dequantize_rejects(lib):
+    f = lib.mixfp4_dequantize
+    assert f(A16, A16, None, 2, 20, A16, None) == 2
+    assert f(A16, A16, None, -2, 32, A16, None) == 2
+    assert f(P(0), A16, None, 2, 32, A16, None) == 1
+    assert f(A16, A16, None, 2, 32, P(0), None) == 1
+    assert f(P(0x10008), A16, None, 2, 32, A16, None) == 3
+    assert f(A16, A16, None, 2, 32, A4, None) == 3
+    assert f(A16, A16, P(0x10001), 2, 32, A16, None) == 3
+    assert f(P(0), P(0), None, 0, 32, P(0), None) == 0      # empty: nothing to do
+
+
+def test_gemm_rejects(lib):
+    f = lib.mixfp4_gemm
+    args = lambda **kw: [kw.get(n, d) for n, d in [
+        ("ac", A16), ("asc", A16), ("ats", None), ("wc", A16), ("wsc", A16), ("wts", None),
+        ("m", 8), ("n", 8), ("k", 32), ("c", A16), ("s", None)]]
+    assert f(*args(k=40)) == 2
+    assert f(*args(m=-1)) == 2
+    assert f(*args(c=P(0))) == 1
+    assert f(*args(ac=P(0))) == 1
+    assert f(*args(wsc=P(0))) == 1
+    assert f(*args(ac=P(0x10008))) == 3
+    assert f(*args(c=P(0x10002))) == 3
+    assert f(*args(ats=P(0x10002))) == 3
+    assert f(*args(m=0, ac=P(0), c=P(0))) == 0                # empty output: no-op

@@ -1,0 +1,114 @@
+"""GPU parity of mixfp4_gemm against the oracle's fp64 GEMM of the exactly
+dequantized operands: |C - C_ref| <= 1e-5 * sum|a*w| + 1e-6 element-wise."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import gemm as G
+from oracle import quant as Q
+from tests._golden import handworked_gemm
+from tests._gpu import dev_f32, dev_u8, gpu_quantize, host, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _gemm_dev(qa, qw):
+    import paper_2605_31035_amd as M
+    a = (dev_u8(qa.codes), dev_u8(qa.scales), dev_f32(qa.s32))
+    w = (dev_u8(qw.codes), dev_u8(qw.scales), dev_f32(qw.s32))
+    c = M.mixfp4_gemm(a, w)
+    torch.cuda.synchronize()
+    return host(c)
+
+
+def _check(c, qa, qw, rows=None, cols=None):
+    if rows is not None:
+        qa = _subset(qa, rows)
+        qw = _subset(qw, cols)
+        c = c[np.ix_(rows, cols)]
+    a_hat, w_hat = G.operands(qa, qw)
+    c_ref, bound = G.gemm(a_hat, w_hat)
+    ok, worst = G.within_tolerance(c, c_ref, bound)
+    assert ok.all(), f"{(~ok).sum()} elements out of tolerance, worst ratio {worst}"
+    return worst
+
+
+def _subset(q, rows):
+    return Q.Quantized(codes=q.codes[rows], scales=q.scales[rows], s32=q.s32, t=None,
+                       sf_code=None, si_code=None, delta=None)
+
+
+def test_handworked_dot():
+    g = handworked_gemm()
+    bits = W.f32_to_bf16_bits(np.array([g["a"], g["w"]], np.float32))
+    qa, qw = Q.quantize(bits[:1], s32=1.0), Q.quantize(bits[1:], s32=1.0)
+    c = _gemm_dev(qa, qw)
+    assert c[0, 0] == g["c"][0]
+
+
+def test_integer_operands_exact():
+    rng = np.random.default_rng(12)
+    a = rng.integers(-7, 8, (70, 96)).astype(np.float32)
+    w = rng.integers(-7, 8, (45, 96)).astype(np.float32)
+    a.reshape(-1, 16)[:, 0] = 7
+    w.reshape(-1, 16)[:, 0] = 7
+    qa = Q.quantize(W.f32_to_bf16_bits(a), s32=1.0)
+    qw = Q.quantize(W.f32_to_bf16_bits(w), s32=1.0)
+    c = _gemm_dev(qa, qw)
+    np.testing.assert_array_equal(c, (a.astype(np.int64) @ w.astype(np.int64).T).astype(np.float32))
+
+
+@pytest.mark.parametrize("m,n,k", [(1, 1, 16), (130, 77, 48), (257, 129, 80), (16, 300, 4096),
+                                   (128, 128, 32), (33, 1000, 272), (512, 256, 1024)])
+def test_ragged_shapes(m, n, k):
+    a = W.adversarial(m + k, m, k)
+    w = W.adversarial(n + 3 * k, n, k)
+    qa, qw = Q.quantize(a), Q.quantize(w)
+    log(f"gemm ragged m={m} n={n} k={k}")
+    _check(_gemm_dev(qa, qw), qa, qw)
+
+
+def test_k_zero_writes_zeros():
+    import paper_2605_31035_amd as M
+    e = torch.empty((4, 0), dtype=torch.uint8, device="cuda")
+    w = torch.empty((3, 0), dtype=torch.uint8, device="cuda")
+    out = torch.full((4, 3), 7.0, device="cuda")
+    M.mixfp4_gemm((e, e, None), (w, w, None), out=out)
+    assert torch.all(out == 0)
+
+
+def test_tiny_workload_end_to_end():
+    import paper_2605_31035_amd as M
+    wl = W.tiny()
+    ga = gpu_quantize(wl.tensors["A"])
+    gw = gpu_quantize(wl.tensors["W"])
+    c = host(M.mixfp4_gemm(ga, gw))
+    qa, qw = Q.quantize(wl.tensors["A"]), Q.quantize(wl.tensors["W"])
+    np.testing.assert_array_equal(host(ga[0]), qa.codes)
+    np.testing.assert_array_equal(host(gw[0]), qw.codes)
+    log(f"tiny worst ratio {_check(c, qa, qw):.3g}")
+
+
+@pytest.mark.parametrize("name", ["prefill_7b", "rotated", "decode", "large"])
+def test_workload_full_size(name):
+    """Full-size GEMMs of each workload from GPU-quantized operands (whose
+    bit-exactness is checked in test_gpu_quantize); C checked on a sampled
+    grid of rows x columns against the oracle."""
+    import paper_2605_31035_amd as M
+    log(f"generate {name}")
+    wl = W.get(name) if name != "large" else W.get(name, tensors=("A", "W"))
+    rng = np.random.default_rng(6)
+    dq = {}
+    for tname, bits in wl.tensors.items():
+        dq[tname] = gpu_quantize(bits)
+    for a_name, w_name in wl.gemms:
+        a_bits, w_bits = wl.tensors[a_name], wl.tensors[w_name]
+        log(f"{name}: gemm {a_name}{a_bits.shape} x {w_name}{w_bits.shape}^T")
+        c = host(M.mixfp4_gemm(dq[a_name], dq[w_name]))
+        rows = np.unique(np.concatenate([[0, a_bits.shape[0] - 1], rng.integers(0, a_bits.shape[0], 48)]))
+        cols = np.unique(np.concatenate([[0, w_bits.shape[0] - 1], rng.integers(0, w_bits.shape[0], 48)]))
+        qa = Q.quantize(a_bits[rows], s32=Q.tensor_scale(a_bits))
+        qw = Q.quantize(w_bits[cols], s32=Q.tensor_scale(w_bits))
+        worst = _check(c[np.ix_(rows, cols)], qa, qw)
+        log(f"{name} {a_name}x{w_name} ok, worst ratio {worst:.3g}")

@@ -1,0 +1,119 @@
+"""GPU parity of mixfp4_quantize / mixfp4_dequantize against the CPU oracle:
+codes, scale bytes and s32 bit-exact, dequantized values bit-exact."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from oracle import quant as Q
+from tests._golden import handworked_blocks
+from tests._gpu import dev_f32, dev_u8, gpu_quantize, host, log
+
+pytestmark = pytest.mark.gpu
+
+
+def _assert_same(bits, s32=None, ldx_pad=0, label=""):
+    log(f"quantize {label} shape={bits.shape} s32={s32} pad={ldx_pad}")
+    codes, scales, s = gpu_quantize(bits, s32, ldx_pad)
+    ref = Q.quantize(bits, s32=s32)
+    assert host(s)[0] == ref.s32, (host(s)[0], ref.s32)
+    np.testing.assert_array_equal(host(scales), ref.scales)
+    np.testing.assert_array_equal(host(codes), ref.codes)
+    return codes, scales, s, ref
+
+
+def test_handworked_blocks():
+    cases = handworked_blocks()
+    bits = W.f32_to_bf16_bits(np.stack([c["block"] for c in cases]))
+    codes, scales, _, _ = _assert_same(bits, s32=1.0, label="handworked")
+    for i, c in enumerate(cases):
+        assert host(scales)[i, 0] == c["scale"]
+        assert bytes(host(codes)[i]) == c["codes"]
+
+
+def test_tiny_workload_and_dequant():
+    import paper_2605_31035_amd as M
+    wl = W.tiny()
+    for name, bits in wl.tensors.items():
+        codes, scales, s, ref = _assert_same(bits, label=f"tiny.{name}")
+        d = host(M.mixfp4_dequantize(codes, scales, s))
+        np.testing.assert_array_equal(d, Q.dequantize(ref.codes, ref.scales, ref.s32))
+        d1 = host(M.mixfp4_dequantize(codes, scales, None))
+        np.testing.assert_array_equal(d1, Q.dequantize(ref.codes, ref.scales, None))
+
+
+@pytest.mark.parametrize("rows,k,seed", [(1, 16, 0), (3, 48, 1), (257, 80, 2), (64, 4096, 3), (1000, 272, 4)])
+def test_adversarial(rows, k, seed):
+    bits = W.adversarial(seed, rows, k)
+    _assert_same(bits, label="adversarial")
+    _assert_same(bits, s32=np.float32(0.37), label="adversarial/given")
+
+
+def test_strided_rows():
+    bits = W.adversarial(9, 33, 64)
+    _assert_same(bits, ldx_pad=8, label="ldx=k+8")
+    _assert_same(bits, ldx_pad=64, s32=1.5, label="ldx=k+64 given")
+
+
+def test_near_midpoints():
+    from oracle import formats as F
+    rows = []
+    for s8 in F.E4M3_VALUES[1:126:3]:
+        for grid, top in ((F.F_GRID, 6.0), (F.I_GRID, 7.0)):
+            mids = (grid[:-1] + grid[1:]) / 2
+            blk = np.zeros(16, np.float32)
+            vals = ([top * s8] + list(mids * s8) + list(grid[1:] * s8))[:16]
+            blk[:len(vals)] = np.array(vals, np.float32)
+            rows.append(blk)
+            rows.append(-blk)
+    bits = W.f32_to_bf16_bits(np.stack(rows))
+    for b in (bits, np.where(bits & 0x7FFF, bits + 1, bits).astype(np.uint16)):
+        for s in (1.0, 1 + 2 ** -23, 1 - 2 ** -24, 1 + 5 * 2 ** -23, 0.75 - 2 ** -25):
+            _assert_same(b, s32=np.float32(s), label="near-midpoint")
+
+
+def test_empty_inputs():
+    import paper_2605_31035_amd as M
+    x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    codes, scales, s = M.mixfp4_quantize(x)
+    torch.cuda.synchronize()
+    assert codes.shape == (0, 32) and host(s)[0] == 1.0
+    x = torch.zeros((5, 64), dtype=torch.bfloat16, device="cuda")
+    codes, scales, s = M.mixfp4_quantize(x)
+    assert host(s)[0] == 1.0 and np.all(host(scales) == 0x80) and np.all(host(codes) == 0)
+
+
+def test_deterministic():
+    bits = W.adversarial(21, 512, 1024)
+    a = gpu_quantize(bits)
+    b = gpu_quantize(bits)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def _sampled_rows(rng, rows, n=192):
+    return np.unique(np.concatenate([[0, rows - 1], rng.integers(0, rows, n)]))
+
+
+@pytest.mark.parametrize("name,tensors", [
+    ("prefill_7b", ("A", "W1", "W2")), ("rotated", ("A", "W")), ("decode", ("A", "W")),
+    ("large", ("A", "W")), ("large", ("Q",))])
+def test_workload_full_size(name, tensors):
+    """Full-size tensors of each workload quantized on the GPU in the bench's
+    launch configuration; s32 checked exactly, codes and scales on sampled rows
+    (the oracle quantizes those rows with the full-tensor s32)."""
+    log(f"generate {name} {tensors}")
+    wl = W.get(name, tensors=tensors)
+    rng = np.random.default_rng(5)
+    for tname in tensors:
+        bits = wl.tensors[tname]
+        log(f"{name}.{tname} shape={bits.shape}")
+        codes, scales, s = gpu_quantize(bits)
+        s_ref = Q.tensor_scale(bits)
+        assert host(s)[0] == s_ref
+        rows = _sampled_rows(rng, bits.shape[0])
+        ref = Q.quantize(bits[rows], s32=s_ref)
+        idx = torch.from_numpy(rows).to("cuda")
+        np.testing.assert_array_equal(host(scales.index_select(0, idx)), ref.scales)
+        np.testing.assert_array_equal(host(codes.index_select(0, idx)), ref.codes)
+        log(f"{name}.{tname} ok; E1M2 share {ref.t.mean():.3f}")
