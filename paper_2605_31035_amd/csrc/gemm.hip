@@ -1,22 +1,35 @@
 // MixFP4 block-scaled GEMM for gfx950: C[m, n] = s32_A s32_W sum_k a[m,k] w[n,k].
 //
-// Sec. 3.3 / App. B.5 decode both micro-formats into one value set (E2M2):
-// E2M1 magnitudes gain a zero mantissa bit, E1M2 magnitudes go through a
-// small table, T (scale bit 7) selects the path.  Here that unified value v
-// is multiplied by the block's E4M3 scale s8 on the fly: s8 has at most 4
-// significant bits and v at most 3, so a = s8 * v has at most 7 and lies in
-// [2^-10, 3136] -- it is exact in bf16.  The bf16 operands feed
-// v_mfma_f32_32x32x16_bf16 with fp32 accumulation (the accumulation format
-// the paper keeps, Sec. 3.3); the per-tensor fp32 scales are applied once in
-// the epilogue.  App. B.1's factored form (scale product per block) is not
-// needed because the per-element decode is exact.
+// Numerics.  Sec. 3.3 / App. B.5 decode both micro-formats into one value
+// set (E2M2): E2M1 magnitudes gain a zero mantissa bit, E1M2 magnitudes go
+// through a small table, T (scale bit 7) selects the path.  Here the unified
+// value v is multiplied by the block's E4M3 scale s8 during decode: s8 has at
+// most 4 significant bits and v at most 3, so a = s8 * v has at most 7 and lies
+// in [2^-10, 3136] -- exact in bf16.  The bf16 operands feed
+// v_mfma_f32_32x32x16_bf16 with fp32 accumulation (the paper keeps FP16/FP32
+// accumulation unchanged, Sec. 3.3); the two fp32 tensor scales are applied
+// once in the epilogue.  App. B.1's factored per-block scale is not needed
+// because the per-element decode is exact.
 //
-// Tiling: a 256-thread workgroup owns a 128 x 128 tile of C; its four waves
-// each own 64 x 64 (2 x 2 MFMA tiles of 32 x 32).  The K loop steps over
-// two 16-element scale blocks at a time: every thread decodes one block of A
-// and one block of W into LDS (each element decoded once per workgroup),
-// then the waves run their MFMAs from LDS.  Rows beyond m / n and blocks
-// beyond k decode as zeros; stores are masked.
+// Decode.  For each of the 256 possible scale bytes a 16-byte table holds the
+// low and high bytes of the bf16 values s8 * v(m, T) for the 8 magnitudes m.
+// A code dword (8 nibbles) decodes with v_perm_b32 byte lookups: magnitudes
+// of the even and odd elements select low / high bytes, the nibble sign bit is
+// OR-ed into the high byte, and two more perms pair the bytes into bf16.  The
+// decoded 8 values are kept in the order [e0 e2 e4 e6 e1 e3 e5 e7]; A and W use
+// the same order, and a dot product does not depend on the order of k.
+//
+// Tiling.  A workgroup of 256 threads (2 x 2 waves) owns a BM x BN tile of C;
+// each wave owns (BM/2) x (BN/2) as 32 x 32 MFMA tiles.  The K loop steps 64
+// (four 16-element scale blocks).  Per step every thread loads the packed
+// codes + scale bytes of (BM+BN)/256 rows one step ahead into registers,
+// decodes the previous step's rows into the idle half of a double-buffered
+// LDS tile while the waves run MFMAs from the other half, so every element
+// is decoded once per workgroup and one barrier separates the steps.
+// LDS layout per buffer: [slice s (16 K)][half h (8 K)][row of A|W][16 B];
+// the 64 lanes of a fragment read and the threads of a decode write both hit
+// consecutive 16-byte words.  Rows beyond m / n and blocks beyond k decode as
+// zeros; stores are masked.
 #include "formats.h"
 #include "internal.h"
 
@@ -26,116 +39,220 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kThreads = 256;
-constexpr int kTileM = 128;
-constexpr int kTileN = 128;
-constexpr int kStepK = 32;                 // two scale blocks per K step
-constexpr int kLdsPitch = kStepK + 8;      // bf16 elements per LDS row (80 bytes)
+constexpr int kStepBlocks = 4;               // scale blocks per K step (64 elements)
 
-// Decode one 16-element block (8 code bytes + scale byte) to 16 bf16 values,
-// packed two per dword (element 2j in the low half).
-__device__ __forceinline__ void decode_block(uint2 c, uint32_t sb, uint32_t out[8]) {
+// Table of bf16 bytes for every scale byte: {lo bytes m=0..3, lo 4..7, hi 0..3, hi 4..7}.
+__device__ __forceinline__ uint4 make_table_entry(uint32_t sb) {
   const bool t1 = (sb & 0x80u) != 0;
   const float s8 = e4m3_value(sb & 0x7Fu);
+  uint32_t lo[2] = {0, 0}, hi[2] = {0, 0};
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const uint32_t byte = ((j < 4 ? c.x : c.y) >> (8 * (j & 3))) & 0xFFu;
-    const uint32_t n0 = byte & 0xFu, n1 = byte >> 4;
-    const float v0 = t1 ? (float)(n0 & 7u) : e2m1_value(n0 & 7u);
-    const float v1 = t1 ? (float)(n1 & 7u) : e2m1_value(n1 & 7u);
-    const uint32_t b0 = (__float_as_uint(s8 * v0) >> 16) | ((n0 & 8u) << 12);
-    const uint32_t b1 = (__float_as_uint(s8 * v1) >> 16) | ((n1 & 8u) << 12);
-    out[j] = b0 | (b1 << 16);
+  for (uint32_t m = 0; m < 8; ++m) {
+    const float v = t1 ? (float)m : e2m1_value(m);
+    const uint32_t b = __float_as_uint(s8 * v) >> 16;     // exact bf16
+    lo[m >> 2] |= (b & 0xFFu) << (8 * (m & 3));
+    hi[m >> 2] |= (b >> 8) << (8 * (m & 3));
+  }
+  return make_uint4(lo[0], lo[1], hi[0], hi[1]);
+}
+
+// Decode one code dword (8 nibbles, element 2j in the low nibble of byte j)
+// with the table of its block into 8 bf16 in the order [e0 e2 e4 e6 e1 e3 e5 e7].
+__device__ __forceinline__ uint4 decode8(uint32_t c, uint4 tab) {
+  const uint32_t me = c & 0x07070707u;
+  const uint32_t mo = (c >> 4) & 0x07070707u;
+  const uint32_t le = __builtin_amdgcn_perm(tab.y, tab.x, me);
+  const uint32_t lo = __builtin_amdgcn_perm(tab.y, tab.x, mo);
+  uint32_t he = __builtin_amdgcn_perm(tab.w, tab.z, me);
+  uint32_t ho = __builtin_amdgcn_perm(tab.w, tab.z, mo);
+  he |= (c << 4) & 0x80808080u;                 // sign of even elements
+  ho |= c & 0x80808080u;                        // sign of odd elements
+  uint4 r;
+  r.x = __builtin_amdgcn_perm(he, le, 0x05010400u);   // e0 e2
+  r.y = __builtin_amdgcn_perm(he, le, 0x07030602u);   // e4 e6
+  r.z = __builtin_amdgcn_perm(ho, lo, 0x05010400u);   // e1 e3
+  r.w = __builtin_amdgcn_perm(ho, lo, 0x07030602u);   // e5 e7
+  return r;
+}
+
+template <int BM, int BN, int WM, int WN>
+struct Tile {
+  static constexpr int kThreads = 64 * WM * WN;
+  static constexpr int kRowsAll = BM + BN;                 // A rows then W rows
+  static constexpr int kRowsPerThread = kRowsAll / kThreads;
+  static constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
+  static constexpr int kTM = kWaveM / 32, kTN = kWaveN / 32;
+  // uint4 words per (slice, half) plane and per buffer
+  static constexpr int kPlane = kRowsAll;
+  static constexpr int kBuf = kStepBlocks * 2 * kPlane;
+  static_assert(kRowsAll % kThreads == 0, "rows must split evenly over threads");
+  static_assert(kTM >= 1 && kTN >= 1, "wave tile must hold whole 32x32 MFMA tiles");
+  static_assert(kThreads >= 256, "the scale table is built by the first 256 threads");
+};
+
+// Packed inputs of one row for one K step: 4 code qwords (4 blocks) + 4 scale bytes.
+struct RowPack {
+  uint2 c[kStepBlocks];
+  uint32_t s;   // scale bytes, block b in byte b
+};
+
+// Fast path (k % 64 == 0, word-aligned scales): rows are clamped into range
+// and the step index into [0, steps), so loads never branch and never leave
+// the operands; data of clamped rows only reaches masked-out outputs, data of
+// clamped steps is never decoded into a buffer that is read.
+__device__ __forceinline__ void load_row_fast(RowPack& p, const uint8_t* __restrict__ crow,
+                                              const uint8_t* __restrict__ srow, int64_t kb0) {
+  const uint4 lo = *reinterpret_cast<const uint4*>(crow + kb0 * 8);
+  const uint4 hi = *reinterpret_cast<const uint4*>(crow + kb0 * 8 + 16);
+  p.c[0] = make_uint2(lo.x, lo.y);
+  p.c[1] = make_uint2(lo.z, lo.w);
+  p.c[2] = make_uint2(hi.x, hi.y);
+  p.c[3] = make_uint2(hi.z, hi.w);
+  p.s = *reinterpret_cast<const uint32_t*>(srow + kb0);
+}
+
+// General path: blocks beyond k and rows beyond m / n load as zeros.
+__device__ __forceinline__ void load_row_masked(RowPack& p, const uint8_t* __restrict__ crow,
+                                                const uint8_t* __restrict__ srow, bool row_ok,
+                                                int64_t kb0, int64_t kb_total) {
+  p.s = 0u;
+#pragma unroll
+  for (int b = 0; b < kStepBlocks; ++b) {
+    const bool ok = row_ok && (kb0 + b) < kb_total;
+    p.c[b] = ok ? *reinterpret_cast<const uint2*>(crow + (kb0 + b) * 8) : make_uint2(0u, 0u);
+    p.s |= (ok ? (uint32_t)srow[kb0 + b] : 0u) << (8 * b);
   }
 }
 
-__device__ __forceinline__ bf16x8 lds_frag(const uint16_t* p) {
-  const uint4 v = *reinterpret_cast<const uint4*>(p);
-  return __builtin_bit_cast(bf16x8, v);
-}
-
-__global__ __launch_bounds__(kThreads) void gemm_kernel(
+template <int BM, int BN, int WM, int WN, bool kFast>
+__global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c) {
-  __shared__ __attribute__((aligned(16))) uint16_t sa[kTileM * kLdsPitch];
-  __shared__ __attribute__((aligned(16))) uint16_t sw[kTileN * kLdsPitch];
+  using T = Tile<BM, BN, WM, WN>;
+  constexpr int R = T::kRowsPerThread;
+  __shared__ uint4 table[256];
+  // Two separate buffers (not one indexed array) so the compiler can see that
+  // the decode stores of one step never alias the fragment loads of the other
+  // and may interleave them with the MFMAs.
+  __shared__ uint4 lds0[T::kBuf];
+  __shared__ uint4 lds1[T::kBuf];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int64_t m0 = (int64_t)blockIdx.y * kTileM;
-  const int64_t n0 = (int64_t)blockIdx.x * kTileN;
-  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 64;
+  const int64_t m0 = (int64_t)blockIdx.y * BM;
+  const int64_t n0 = (int64_t)blockIdx.x * BN;
+  const int wm = (wave / WN) * T::kWaveM, wn = (wave % WN) * T::kWaveN;
   const int64_t kb_total = k / kBlock;
   const int64_t code_pitch = k / 2;
+  const int64_t steps = (kb_total + kStepBlocks - 1) / kStepBlocks;
 
-  // decode assignment: row tid/2 of the tile, block tid%2 of the K step
-  const int drow = tid >> 1, dblk = tid & 1;
-  const int64_t arow = m0 + drow, wrow = n0 + drow;
+  if (tid < 256) table[tid] = make_table_entry((uint32_t)tid);
 
-  f32x16 acc[2][2];
+  // rows this thread decodes: g = tid + threads * r over [A rows | W rows]
+  const uint8_t* rc[R];
+  const uint8_t* rs[R];
+  bool rok[R];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  for (int64_t kb = 0; kb < kb_total; kb += 2) {
-    const int64_t blk = kb + dblk;
-    uint32_t da[8], dw[8];
-    if (arow < m && blk < kb_total) {
-      const uint2 cc = *reinterpret_cast<const uint2*>(a_codes + arow * code_pitch + blk * 8);
-      decode_block(cc, a_scales[arow * kb_total + blk], da);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) da[q] = 0u;
-    }
-    if (wrow < n && blk < kb_total) {
-      const uint2 cc = *reinterpret_cast<const uint2*>(w_codes + wrow * code_pitch + blk * 8);
-      decode_block(cc, w_scales[wrow * kb_total + blk], dw);
-    } else {
-#pragma unroll
-      for (int q = 0; q < 8; ++q) dw[q] = 0u;
-    }
-    uint4* pa = reinterpret_cast<uint4*>(sa + drow * kLdsPitch + dblk * 16);
-    uint4* pw = reinterpret_cast<uint4*>(sw + drow * kLdsPitch + dblk * 16);
-    pa[0] = make_uint4(da[0], da[1], da[2], da[3]);
-    pa[1] = make_uint4(da[4], da[5], da[6], da[7]);
-    pw[0] = make_uint4(dw[0], dw[1], dw[2], dw[3]);
-    pw[1] = make_uint4(dw[4], dw[5], dw[6], dw[7]);
-    __syncthreads();
-
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int koff = kk * 16 + (lane >> 5) * 8;
-      bf16x8 fa[2], fw[2];
-#pragma unroll
-      for (int i = 0; i < 2; ++i) fa[i] = lds_frag(sa + (wm + i * 32 + (lane & 31)) * kLdsPitch + koff);
-#pragma unroll
-      for (int j = 0; j < 2; ++j) fw[j] = lds_frag(sw + (wn + j * 32 + (lane & 31)) * kLdsPitch + koff);
-#pragma unroll
-      for (int i = 0; i < 2; ++i)
-#pragma unroll
-        for (int j = 0; j < 2; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fw[j], acc[i][j], 0, 0, 0);
-    }
-    __syncthreads();
+  for (int r = 0; r < R; ++r) {
+    const int g = tid + T::kThreads * r;
+    const bool is_a = g < BM;
+    int64_t row = is_a ? m0 + g : n0 + (g - BM);
+    const int64_t lim = is_a ? m : n;
+    rok[r] = row < lim;
+    if (kFast && !rok[r]) row = lim - 1;
+    rc[r] = (is_a ? a_codes : w_codes) + row * code_pitch;
+    rs[r] = (is_a ? a_scales : w_scales) + row * kb_total;
   }
 
-  const float s = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
-  // 32 x 32 accumulator layout: lane holds column lane%32; register r holds
-  // row 8*(r/4) + 4*(lane/32) + r%4.
+  auto load_step = [&](RowPack (&p)[R], int64_t step) {
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+    for (int r = 0; r < R; ++r) {
+      if (kFast) {
+        const int64_t st = step < steps ? step : steps - 1;
+        load_row_fast(p[r], rc[r], rs[r], st * kStepBlocks);
+      } else {
+        load_row_masked(p[r], rc[r], rs[r], rok[r], step * kStepBlocks, kb_total);
+      }
+    }
+  };
+  auto decode_block = [&](const RowPack (&p)[R], uint4* wr, int b) {
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      const int64_t col = n0 + wn + j * 32 + (lane & 31);
+    for (int r = 0; r < R; ++r) {
+      const int g = tid + T::kThreads * r;
+      const uint4 tab = table[(p[r].s >> (8 * b)) & 0xFFu];
+      uint4* dst = wr + (b * 2) * T::kPlane + g;
+      dst[0] = decode8(p[r].c[b].x, tab);
+      dst[T::kPlane] = decode8(p[r].c[b].y, tab);
+    }
+  };
+
+  f32x16 acc[T::kTM][T::kTN];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        if (row < m && col < n) c[row * n + col] = acc[i][j][r] * s;
+  for (int i = 0; i < T::kTM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::kTN; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+
+  const int half = lane >> 5, lrow = lane & 31;
+  // One K step: MFMAs over `rd`, interleaved with decoding `p` (the next
+  // step) into `wr`; `pn` receives the step after that.
+  auto body = [&](const uint4* rd, uint4* wr, const RowPack (&p)[R], RowPack (&pn)[R],
+                  int64_t s, bool decode) {
+    if (decode) load_step(pn, s + 2);
+    // keep the prefetch at the top of the step so its latency hides under the MFMAs
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int sl = 0; sl < kStepBlocks; ++sl) {
+      const uint4* plane = rd + (sl * 2 + half) * T::kPlane;
+      bf16x8 fa[T::kTM], fw[T::kTN];
+#pragma unroll
+      for (int i = 0; i < T::kTM; ++i) fa[i] = __builtin_bit_cast(bf16x8, plane[wm + i * 32 + lrow]);
+#pragma unroll
+      for (int j = 0; j < T::kTN; ++j) fw[j] = __builtin_bit_cast(bf16x8, plane[BM + wn + j * 32 + lrow]);
+#pragma unroll
+      for (int i = 0; i < T::kTM; ++i)
+#pragma unroll
+        for (int j = 0; j < T::kTN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fw[j], acc[i][j], 0, 0, 0);
+      if (decode) decode_block(p, wr, sl);
+    }
+  };
+
+  RowPack pa[R], pb[R];
+  load_step(pa, 0);
+  __syncthreads();   // table ready
+#pragma unroll
+  for (int b = 0; b < kStepBlocks; ++b) decode_block(pa, lds0, b);
+  load_step(pa, 1);
+
+  // Step s reads buffer s%2 and decodes step s+1 into the other one; one
+  // barrier per step orders "decoded" before "read" and "read" before
+  // "overwritten".  On the fast path the last step decodes clamped data into
+  // a buffer that is never read again.
+  for (int64_t s = 0; s < steps; s += 2) {
+    __syncthreads();
+    body(lds0, lds1, pa, pb, s, kFast || s + 1 < steps);
+    if (s + 1 < steps) {
+      __syncthreads();
+      body(lds1, lds0, pb, pa, s + 1, kFast || s + 2 < steps);
+    }
+  }
+
+  const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
+  // 32 x 32 accumulator layout: lane holds column lane%32; register q holds
+  // row 8*(q/4) + 4*(lane/32) + q%4.
+#pragma unroll
+  for (int i = 0; i < T::kTM; ++i)
+#pragma unroll
+    for (int j = 0; j < T::kTN; ++j) {
+      const int64_t col = n0 + wn + j * 32 + lrow;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int64_t row = m0 + wm + i * 32 + 8 * (q >> 2) + 4 * half + (q & 3);
+        if (row < m && col < n) c[row * n + col] = acc[i][j][q] * scale;
       }
     }
 }
@@ -143,6 +260,23 @@ __global__ __launch_bounds__(kThreads) void gemm_kernel(
 __global__ void fill_zero(float* c, int64_t count) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) c[i] = 0.0f;
+}
+
+template <int BM, int BN, int WM, int WN>
+hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
+                       const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
+                       int64_t m, int64_t n, int64_t k, float* c, hipStream_t stream) {
+  dim3 grid((unsigned)((n + BN - 1) / BN), (unsigned)((m + BM - 1) / BM));
+  constexpr int threads = 64 * WM * WN;
+  const bool fast = k % 64 == 0 && ((reinterpret_cast<uintptr_t>(a_scales) |
+                                     reinterpret_cast<uintptr_t>(w_scales)) & 3u) == 0;
+  if (fast)
+    gemm_kernel<BM, BN, WM, WN, true><<<grid, threads, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
+  else
+    gemm_kernel<BM, BN, WM, WN, false><<<grid, threads, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -157,10 +291,17 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     fill_zero<<<(int)g, 256, 0, stream>>>(c, m * n);
     return hipGetLastError();
   }
-  dim3 grid((unsigned)((n + kTileN - 1) / kTileN), (unsigned)((m + kTileM - 1) / kTileM));
-  gemm_kernel<<<grid, kThreads, 0, stream>>>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m,
-                                             n, k, c);
-  return hipGetLastError();
+  // Tile choice: 256 x 256 halves LDS traffic per MFMA but needs enough tiles
+  // to fill the 256 compute units; fall back to 128 x 128 otherwise.
+  const int64_t tiles256 = ((m + 255) / 256) * ((n + 255) / 256);
+  const int64_t tiles128 = ((m + 127) / 128) * ((n + 127) / 128);
+  const double t256 = (double)((tiles256 + 255) / 256) * 4.0;          // 4x the work per tile
+  const double t128 = (double)((tiles128 + 255) / 256) * 1.0 / 0.6;    // lower MFMA efficiency
+  if (t256 <= t128)
+    return launch_tile<256, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
+                                       c, stream);
+  return launch_tile<128, 128, 2, 2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
+                                     c, stream);
 }
 
 }  // namespace mixfp4
