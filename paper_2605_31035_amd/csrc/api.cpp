@@ -52,8 +52,9 @@ int mixfp4_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uin
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();   // drop stale errors so a launch failure is ours
   if (flags == MIXFP4_SCALE_COMPUTE) {
-    const int st = launch_status(mixfp4::launch_tensor_scale(x, empty ? 0 : rows, k, ldx,
-                                                             tensor_scale, s));
+    const int st = launch_status(mixfp4::launch_tensor_scale(
+        x, empty ? 0 : rows, k, ldx, empty ? nullptr : scales,
+        empty ? 0 : rows * (k / mixfp4::kBlock), tensor_scale, s));
     if (st != MIXFP4_OK) return st;
   }
   if (empty) return MIXFP4_OK;

@@ -25,14 +25,14 @@ __device__ __forceinline__ float e4m3_value(uint32_t c) {
 }
 
 // Round v >= 0 (finite fp32) to the nearest E4M3 value, ties to the even
-// code, saturating at 448; returns the 7-bit magnitude code.
+// code, saturating at 448; returns the 7-bit magnitude code.  Branch-free.
 __device__ __forceinline__ uint32_t e4m3_code(float v) {
-  if (!(v < 448.0f)) return 0x7Eu;
-  if (v < 0x1p-6f) return (uint32_t)rintf(v * 512.0f);   // m * 2^-9, m in 0..8
   uint32_t b = __float_as_uint(v);
-  b += 0x7FFFFu + ((b >> 20) & 1u);                     // RNE to 3 mantissa bits
-  const uint32_t code = (b >> 20) - (120u << 3);         // rebias exponent 127 -> 7
-  return code < 0x7Eu ? code : 0x7Eu;
+  b += 0x7FFFFu + ((b >> 20) & 1u);                      // RNE to 3 mantissa bits
+  const uint32_t normal = (b >> 20) - (120u << 3);        // rebias exponent 127 -> 7
+  const uint32_t sub = (uint32_t)rintf(v * 512.0f);       // m * 2^-9, m in 0..8
+  const uint32_t c = v < 0x1p-6f ? sub : normal;
+  return (v < 448.0f && c < 0x7Eu) ? c : 0x7Eu;
 }
 
 // E2M1 magnitude of a 3-bit code (App. B.2: e = p2p1, m = p0, bias 1).

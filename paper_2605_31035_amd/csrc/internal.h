@@ -10,9 +10,12 @@ namespace mixfp4 {
 constexpr int kBlock = 16;
 
 // Launchers: shapes are validated by the ABI layer before these are called.
+// Tensor scale s32 = max|X| / 2688 (1.0 for all-zero X) into *tensor_scale.
+// `scratch` (may be NULL) is device memory of `scratch_bytes` that the call
+// may overwrite before the quantize kernel writes it (the scale-byte output).
 hipError_t launch_tensor_scale(const uint16_t* x, int64_t rows, int64_t k,
-                               int64_t ldx, float* tensor_scale,
-                               hipStream_t stream);
+                               int64_t ldx, uint8_t* scratch, int64_t scratch_bytes,
+                               float* tensor_scale, hipStream_t stream);
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k,
                            int64_t ldx, uint8_t* codes, uint8_t* scales,
                            const float* tensor_scale, hipStream_t stream);
