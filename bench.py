@@ -40,53 +40,92 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def cpu_baseline(wl, budget_s: float = 12.0) -> dict:
-    """Time the CPU oracle on a bounded sample of the step and scale it to the
-    full step: quantize sampled rows of every operand (row chunks in a process
-    pool, one process per core), fp64 GEMM of sampled rows of A against sampled
-    rows of W1 (multithreaded BLAS)."""
+def _oracle_quantize_rows(args):
+    from oracle import quant as Q
+    bits, s32 = args
+    q = Q.quantize(bits, s32)
+    return q.codes, q.scales
+
+
+def cpu_baseline(wl, budget_s: float = 10.0, max_reps: int = 8) -> dict:
+    """The CPU oracle on the same step: quantize A, W1, W2 (row chunks in a
+    process pool, one process per core; the tensor scale is the oracle's own
+    max over the full tensor) and both GEMMs as the oracle defines them (fp64
+    matmul of exactly dequantized operands plus the bound matmul, multithreaded
+    BLAS).  Whole steps repeat until `budget_s` has elapsed."""
     from concurrent.futures import ProcessPoolExecutor
 
     from oracle import gemm as G
     from oracle import quant as Q
 
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
-    rng = np.random.default_rng(0)
-    sample = {}
-    total_elems = 0
-    for name, bits in wl.tensors.items():
-        rows = np.sort(rng.choice(bits.shape[0], min(bits.shape[0], 96 * cores // 8 * 8), replace=False))
-        sample[name] = (bits[rows], Q.tensor_scale(bits))
-        total_elems += bits.size
-    t0 = time.perf_counter()
-    with ProcessPoolExecutor(cores) as ex:
-        futs = {}
-        for name, (b, s) in sample.items():
-            chunks = np.array_split(b, cores)
-            futs[name] = [ex.submit(Q.quantize, c, s) for c in chunks]
-        quant = {}
-        for name, fs in futs.items():
-            parts = [f.result() for f in fs]
-            quant[name] = Q.Quantized(codes=np.concatenate([p.codes for p in parts]),
-                                      scales=np.concatenate([p.scales for p in parts]),
-                                      s32=parts[0].s32, t=None, sf_code=None, si_code=None,
-                                      delta=None)
-    t_q = time.perf_counter() - t0
-    q_elems = sum(b.size for b, _ in sample.values())
-    a_hat, w_hat = G.operands(quant["A"], quant["W1"])
-    t0 = time.perf_counter()
-    G.gemm(a_hat, w_hat)
-    t_g = time.perf_counter() - t0
-    g_flops = 2.0 * a_hat.shape[0] * w_hat.shape[0] * a_hat.shape[1]
     step_flops = sum(2.0 * wl.tensors[a].shape[0] * wl.tensors[w].shape[0] * wl.tensors[a].shape[1]
                      for a, w in wl.gemms)
-    t_full = t_q / q_elems * total_elems + t_g / g_flops * step_flops
+    times = []
+    with ProcessPoolExecutor(cores) as ex:
+        while len(times) < max_reps and sum(times) < budget_s:
+            t0 = time.perf_counter()
+            quant = {}
+            for name, bits in wl.tensors.items():
+                s32 = Q.tensor_scale(bits)
+                parts = list(ex.map(_oracle_quantize_rows,
+                                    [(c, s32) for c in np.array_split(bits, 4 * cores)]))
+                quant[name] = Q.Quantized(codes=np.concatenate([p[0] for p in parts]),
+                                          scales=np.concatenate([p[1] for p in parts]),
+                                          s32=s32, t=None, sf_code=None, si_code=None, delta=None)
+            for a, w in wl.gemms:
+                G.gemm(*G.operands(quant[a], quant[w]))
+            times.append(time.perf_counter() - t0)
+    t = float(np.mean(times))
     return {
-        "value": step_flops / t_full / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-        "sample": (f"oracle quantize of {q_elems} sampled elements ({t_q:.2f} s, {cores} processes) "
-                   f"+ fp64 GEMM {a_hat.shape[0]}x{w_hat.shape[0]}x{a_hat.shape[1]} "
-                   f"({t_g:.2f} s, BLAS threads); scaled to the full step "
-                   f"({total_elems} elements, {step_flops / 1e9:.1f} GFLOP): {t_full:.1f} s/step"),
+        "value": step_flops / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+        "sample": (f"{len(times)} full step(s) of the same workload: oracle quantize of all three "
+                   f"tensors ({cores} processes) + oracle fp64 GEMMs with their bound matmuls "
+                   f"(BLAS threads); {t:.2f} s per step"),
+    }
+
+
+def measure_decode(M, torch, dev, iters: int = 50) -> dict:
+    """Decode-shape step (seed 3): online tensor scale + quantize of A[16,8192],
+    then C = A W^T [16, 28672] against W[28672,8192] quantized once before
+    timing.  HBM-bound: algorithmic bytes = W codes + W scales + A (bf16 in,
+    codes + scales) + C."""
+    import workloads as W
+    wl = W.decode()
+    xa = torch.from_numpy(wl.tensors["A"].view(np.int16)).to(dev).view(torch.bfloat16)
+    xw = torch.from_numpy(wl.tensors["W"].view(np.int16)).to(dev).view(torch.bfloat16)
+    qw = M.mixfp4_quantize(xw)
+    del xw
+    r, k = xa.shape
+    qa = (torch.empty((r, k // 2), dtype=torch.uint8, device=dev),
+          torch.empty((r, k // 16), dtype=torch.uint8, device=dev),
+          torch.empty(1, dtype=torch.float32, device=dev))
+    out = torch.empty((r, qw[0].shape[0]), dtype=torch.float32, device=dev)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(iters)]
+    for i in range(5 + iters):
+        e = ev[i - 5] if i >= 5 else None
+        if e:
+            e[0].record()
+        M.mixfp4_quantize(xa, None, qa[0], qa[1], scale_out=qa[2])
+        if e:
+            e[1].record()
+        M.mixfp4_gemm(qa, qw, out=out)
+        if e:
+            e[2].record()
+    torch.cuda.synchronize()
+    q_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    g_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    n = qw[0].shape[0]
+    gemm_bytes = n * k / 2 + n * k / 16 + r * k / 2 + r * k / 16 + r * n * 4
+    return {
+        "workload": "decode: A[16,8192] N(0,1) with 4 outlier channels x30 quantized online; "
+                    "W[28672,8192] N(0,0.02) with 0.5% outliers, quantized before timing",
+        "gemm_us": round(g_ms * 1e3, 2), "quantize_a_us": round(q_ms * 1e3, 2),
+        "gemm_bound": "hbm", "gemm_bytes": gemm_bytes,
+        "gemm_GBps": round(gemm_bytes / (g_ms * 1e-3) / 1e9, 1),
+        "gemm_hbm_frac": round(gemm_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "gemm_TFLOPs": round(2.0 * r * n * k / (g_ms * 1e-3) / 1e12, 2),
+        "step_us": round((q_ms + g_ms) * 1e3, 2),
     }
 
 
@@ -96,6 +135,11 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-decode", action="store_true",
+                    help="skip the extra decode-shape (m = 16) measurement")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="first run one elementwise copy of 512 MiB (read + write of known "
+                         "size) so hardware byte counters can be scaled")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU only: the MixFP4 path here runs on a single MI355X "
@@ -124,6 +168,11 @@ def main():
                 torch.empty(1, dtype=torch.float32, device=dev))
     c = {(a, w): torch.empty((x[a].shape[0], x[w].shape[0]), dtype=torch.float32, device=dev)
          for a, w in wl.gemms}
+    if args.calibrate_copy:
+        src = torch.ones(128 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.mul(src, 1.0, out=dst)
+        del src, dst
     torch.cuda.synchronize()
 
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
@@ -181,6 +230,7 @@ def main():
                      "note": "algorithmic 2.5625 B/element; the tensor-scale (amax) read "
                              "pass is inside the timed quantize region but not in the bytes"},
         "gemm_ms_per_step": round(g_ms, 4),
+        "decode_shape": None if args.no_decode else measure_decode(M, torch, dev),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

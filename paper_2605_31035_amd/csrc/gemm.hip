@@ -257,6 +257,121 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Decode-shape GEMM (m <= 16): HBM-bound, W is read once.
+//
+// A workgroup of 8 waves owns 128 columns of C (16 per wave) and all of K.
+// Each lane owns one W row (column n of C) and one quarter g of every
+// 128-element K step: it loads 16 code bytes (two scale blocks) and 2 scale
+// bytes, decodes its four code dwords straight into the B operands of four
+// v_mfma_f32_16x16x32_bf16, and never shares them.  The K slot (g, j) of
+// MFMA i holds element 32g + 8i + j of the step -- any order works as long as
+// A uses the same one.  A (at most 16 rows) is decoded once per workgroup, 512
+// K at a time, into a double-buffered LDS chunk laid out so that the A operand
+// of MFMA i is 64 consecutive 16-byte words.  W loads run two steps ahead.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kSkinnyRows = 16;
+constexpr int kSkinnyWaves = 8;
+constexpr int kSkinnyCols = 16 * kSkinnyWaves;     // columns of C per workgroup
+constexpr int kSkinnyChunk = 512;                  // K per A chunk (4 wave steps)
+
+struct WPack {
+  uint4 c;       // 32 codes (two scale blocks)
+  uint32_t s;    // their two scale bytes in the low 16 bits
+};
+
+__global__ __launch_bounds__(64 * kSkinnyWaves, 1) void gemm_skinny_kernel(
+    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+    const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
+    const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
+    int64_t n, int64_t k, float* __restrict__ c) {
+  __shared__ uint4 table[256];
+  // one A chunk: 4 sub-chunks x [MFMA i (4)][quarter g (4)][row (16)] 16-byte words
+  constexpr int kAWords = (kSkinnyChunk / 128) * 4 * 4 * kSkinnyRows;   // 1024 (16 KB)
+  __shared__ uint4 abuf0[kAWords];
+  __shared__ uint4 abuf1[kAWords];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int nn = lane & 15, g = lane >> 4;
+  const int64_t code_pitch = k / 2, scale_pitch = k / kBlock;
+  const int64_t steps = k / 128;                    // wave steps
+  const int64_t chunks = k / kSkinnyChunk;
+
+  if (tid < 256) table[tid] = make_table_entry((uint32_t)tid);
+
+  // this lane's W row (clamped rows only feed masked-out columns)
+  const int64_t col = (int64_t)blockIdx.x * kSkinnyCols + wave * 16 + nn;
+  const int64_t wrow = col < n ? col : n - 1;
+  const uint8_t* wc = w_codes + wrow * code_pitch + 16 * g;
+  const uint8_t* ws = w_scales + wrow * scale_pitch + 2 * g;
+  auto load_w = [&](WPack& p, int64_t step) {
+    const int64_t st = step < steps ? step : steps - 1;
+    p.c = *reinterpret_cast<const uint4*>(wc + 64 * st);
+    p.s = *reinterpret_cast<const uint16_t*>(ws + 8 * st);
+  };
+
+  // A decode: thread t owns row t/32 and block t%32 of every 512-wide chunk
+  const int ra = tid >> 5, ablk = tid & 31;
+  const int64_t arow = ra < m ? ra : m - 1;
+  const uint8_t* ac = a_codes + arow * code_pitch + 8 * ablk;
+  const uint8_t* as = a_scales + arow * scale_pitch + ablk;
+  // element offset 16*ablk within the chunk -> sub-chunk h, quarter gq, MFMA index iq
+  const int ko = 16 * ablk, h = ko >> 7, gq = (ko & 127) >> 5, iq = (ko & 31) >> 3;
+  const int adst = h * 256 + (iq * 4 + gq) * 16 + ra;
+  auto decode_a = [&](uint4* buf, int64_t chunk) {
+    const int64_t ch = chunk < chunks ? chunk : chunks - 1;
+    const uint2 cc = *reinterpret_cast<const uint2*>(ac + ch * (kSkinnyChunk / 2));
+    const uint4 tab = table[as[ch * (kSkinnyChunk / kBlock)]];
+    buf[adst] = decode8(cc.x, tab);
+    buf[adst + 64] = decode8(cc.y, tab);          // next 8 elements: MFMA index iq + 1
+  };
+
+  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  auto wave_step = [&](const uint4* abuf, int sub, const WPack& p) {
+    const uint4 tlo = table[p.s & 0xFFu], thi = table[(p.s >> 8) & 0xFFu];
+    const uint32_t cw[4] = {p.c.x, p.c.y, p.c.z, p.c.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const bf16x8 fb = __builtin_bit_cast(bf16x8, decode8(cw[i], i < 2 ? tlo : thi));
+      const bf16x8 fa = __builtin_bit_cast(bf16x8, abuf[sub * 256 + i * 64 + lane]);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fb, acc, 0, 0, 0);
+    }
+  };
+
+  WPack p0, p1, p2, p3;
+  load_w(p0, 0);
+  load_w(p1, 1);
+  __syncthreads();   // table ready
+  decode_a(abuf0, 0);
+  for (int64_t ch = 0; ch < chunks; ++ch) {
+    uint4* cur = (ch & 1) ? abuf1 : abuf0;
+    uint4* nxt = (ch & 1) ? abuf0 : abuf1;
+    __syncthreads();   // chunk `ch` of A decoded; the other buffer is free
+    decode_a(nxt, ch + 1);
+    const int64_t s0 = ch * 4;
+    load_w(p2, s0 + 2);
+    wave_step(cur, 0, p0);
+    load_w(p3, s0 + 3);
+    wave_step(cur, 1, p1);
+    load_w(p0, s0 + 4);
+    wave_step(cur, 2, p2);
+    load_w(p1, s0 + 5);
+    wave_step(cur, 3, p3);
+  }
+
+  const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
+  // 16 x 16 accumulator layout: lane holds column lane%16, register r holds row 4*(lane/16) + r
+  if (col < n) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = 4 * g + r;
+      if (row < m) c[row * n + col] = acc[r] * scale;
+    }
+  }
+}
+
 __global__ void fill_zero(float* c, int64_t count) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) c[i] = 0.0f;
@@ -289,6 +404,12 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     int64_t g = (m * n + 255) / 256;
     if (g > 65536) g = 65536;
     fill_zero<<<(int)g, 256, 0, stream>>>(c, m * n);
+    return hipGetLastError();
+  }
+  if (m <= kSkinnyRows && k % kSkinnyChunk == 0 &&
+      ((reinterpret_cast<uintptr_t>(w_scales) | reinterpret_cast<uintptr_t>(a_scales)) & 1u) == 0) {
+    gemm_skinny_kernel<<<(unsigned)((n + kSkinnyCols - 1) / kSkinnyCols), 64 * kSkinnyWaves, 0,
+                         stream>>>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
     return hipGetLastError();
   }
   // Tile choice: 256 x 256 halves LDS traffic per MFMA but needs enough tiles

@@ -69,6 +69,17 @@ def test_ragged_shapes(m, n, k):
     _check(_gemm_dev(qa, qw), qa, qw)
 
 
+@pytest.mark.parametrize("m,n,k", [(1, 1, 512), (5, 127, 1024), (16, 129, 512), (9, 1000, 2048),
+                                   (16, 256, 8192), (3, 300, 1536)])
+def test_decode_shapes(m, n, k):
+    """m <= 16 with k % 512 == 0 takes the decode-shape kernel."""
+    a = W.adversarial(7 * m + k, m, k)
+    w = W.adversarial(11 * n + k, n, k)
+    qa, qw = Q.quantize(a), Q.quantize(w)
+    log(f"gemm decode-shape m={m} n={n} k={k}")
+    _check(_gemm_dev(qa, qw), qa, qw)
+
+
 def test_k_zero_writes_zeros():
     import paper_2605_31035_amd as M
     e = torch.empty((4, 0), dtype=torch.uint8, device="cuda")
