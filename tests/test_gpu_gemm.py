@@ -80,6 +80,21 @@ def test_decode_shapes(m, n, k):
     _check(_gemm_dev(qa, qw), qa, qw)
 
 
+@pytest.mark.parametrize("m,n,k", [(4100, 4100, 512), (4100, 4100, 560)])
+def test_split_tail_tiles(m, n, k):
+    """More 256x256 tiles than CUs with a small last wave: the tail tiles run
+    as two K halves accumulated atomically (fast and masked-K paths, ragged
+    edges).  Checked in full, and twice for bit-identical results."""
+    a = W.adversarial(m + 5, m, k)
+    w = W.adversarial(n + 9, n, k)
+    qa, qw = Q.quantize(a), Q.quantize(w)
+    log(f"gemm split tail m={m} n={n} k={k}")
+    c1 = _gemm_dev(qa, qw)
+    c2 = _gemm_dev(qa, qw)
+    assert np.array_equal(c1, c2)
+    _check(c1, qa, qw)
+
+
 def test_k_zero_writes_zeros():
     import paper_2605_31035_amd as M
     e = torch.empty((4, 0), dtype=torch.uint8, device="cuda")
