@@ -160,16 +160,12 @@ __device__ __forceinline__ int64_t grouped_tile(int64_t i, int64_t ntm, int64_t 
   return (first + local % rows) * ntn + local / rows;
 }
 
-// Work items (after xcd_item): item < nfull is tile grouped_tile(item) over
-// all K; the items after it are the remaining tiles of that order in two K
-// halves each, accumulated with fp32 atomics into a zeroed C (two addends
-// onto zero sum identically in either order, so results stay deterministic).
 template <int BM, int BN, int WM, int WN, bool kFast, bool kSchedule>
 __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
-    int64_t n, int64_t k, float* __restrict__ c, int64_t ntn, int64_t nfull) {
+    int64_t n, int64_t k, float* __restrict__ c) {
   using T = Tile<BM, BN, WM, WN>;
   constexpr int R = T::kRowsPerThread;
   __shared__ uint4 table[256];
@@ -184,14 +180,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
   const int64_t kb_total = k / kBlock;
   const int64_t code_pitch = k / 2;
   const int64_t steps = (kb_total + kStepBlocks - 1) / kStepBlocks;
-  const int64_t ntm = (m + BM - 1) / BM;
-  // full tiles and split halves are each spread evenly over the XCDs
-  const int64_t b = blockIdx.x;
-  const bool split = b >= nfull;
-  const int64_t item = split ? nfull + xcd_item(b - nfull, gridDim.x - nfull) : xcd_item(b, nfull);
-  const int64_t tile = grouped_tile(split ? nfull + ((item - nfull) >> 1) : item, ntm, ntn);
-  const int64_t s_begin = split && ((item - nfull) & 1) ? steps / 2 : 0;
-  const int64_t s_end = split && !((item - nfull) & 1) ? steps / 2 : steps;
+  const int64_t ntm = (m + BM - 1) / BM, ntn = (n + BN - 1) / BN;
+  const int64_t tile = grouped_tile(xcd_item(blockIdx.x, gridDim.x), ntm, ntn);
+  const int64_t s_begin = 0, s_end = steps;
   const int64_t m0 = (tile / ntn) * BM;
   const int64_t n0 = (tile % ntn) * BN;
   const int wm = (wave / WN) * T::kWaveM, wn = (wave % WN) * T::kWaveN;
@@ -322,10 +313,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int64_t row = m0 + wm + i * 32 + 8 * (q >> 2) + 4 * half + (q & 3);
-        if (row < m && col < n) {
-          if (split) unsafeAtomicAdd(c + row * n + col, acc[i][j][q] * scale);
-          else c[row * n + col] = acc[i][j][q] * scale;
-        }
+        if (row < m && col < n) c[row * n + col] = acc[i][j][q] * scale;
       }
     }
 }
@@ -450,76 +438,20 @@ __global__ void fill_zero(float* c, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride) c[i] = 0.0f;
 }
 
-// Zero the C region of tiles [first, first + count) of the grouped tile
-// order, ahead of their atomic accumulation.  A workgroup
-// of 256 threads clears 16 rows of one tile, 4 floats per store when the row
-// pitch allows 16-byte stores.
-template <int BM, int BN>
-__global__ __launch_bounds__(256) void zero_tiles(float* __restrict__ c, int64_t m, int64_t n,
-                                                  int64_t ntn, int64_t first) {
-  static_assert(BN % 4 == 0 && (16 * BN / 4) % 256 == 0, "tile width");
-  constexpr int kGroups = BM / 16;
-  const int64_t tile = grouped_tile(first + blockIdx.x / kGroups, (m + BM - 1) / BM, ntn);
-  const int64_t r0 = (tile / ntn) * BM + (blockIdx.x % kGroups) * 16;
-  const int64_t n0 = (tile % ntn) * BN;
-  const bool vec = (n & 3) == 0 && (reinterpret_cast<uintptr_t>(c) & 15u) == 0;
-  for (int idx = threadIdx.x; idx < 16 * BN / 4; idx += 256) {
-    const int64_t row = r0 + idx / (BN / 4);
-    const int64_t col = n0 + 4 * (idx % (BN / 4));
-    if (row >= m) continue;
-    float* p = c + row * n + col;
-    if (vec && col + 4 <= n) {
-      *reinterpret_cast<float4*>(p) = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    } else {
-      for (int q = 0; q < 4; ++q)
-        if (col + q < n) p[q] = 0.0f;
-    }
-  }
-}
-
-// Splitting the last partial wave of tiles into K halves (atomic epilogue)
-// helps only when tiles are dealt without XCD locality; with the grouped,
-// XCD-contiguous order it measured slower (the atomic burst costs more than
-// the idle CUs), so it is off.  The path stays covered by the tests through
-// the kernel's split items when enabled.
-constexpr bool kSplitTail = false;
-
-int cu_count() {
-  static int cached[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (!cached[dev]) {
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0)
-      v = 256;
-    cached[dev] = v;
-  }
-  return cached[dev];
-}
-
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
                        const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
                        int64_t m, int64_t n, int64_t k, float* c, hipStream_t stream) {
-  const int64_t ntm = (m + BM - 1) / BM, ntn = (n + BN - 1) / BN, tiles = ntm * ntn;
+  const unsigned tiles = (unsigned)(((m + BM - 1) / BM) * ((n + BN - 1) / BN));
   constexpr int threads = 64 * WM * WN;
-  // One workgroup per CU: when the last wave of tiles would leave more than
-  // half of the CUs idle, its tiles run as two K halves each instead.
-  const int64_t cus = cu_count();
-  const int64_t tail = tiles > cus ? tiles % cus : 0;
-  const int64_t steps = (k / kBlock + kStepBlocks - 1) / kStepBlocks;
-  const bool split = kSplitTail && BM * BN >= 256 * 256 && tail > 0 && 2 * tail <= cus && steps >= 4;
-  const int64_t nfull = split ? tiles - tail : tiles;
-  const int64_t items = split ? nfull + 2 * tail : tiles;
-  if (split) zero_tiles<BM, BN><<<(unsigned)(tail * (BM / 16)), 256, 0, stream>>>(c, m, n, ntn, nfull);
   const bool fast = k % 64 == 0 && ((reinterpret_cast<uintptr_t>(a_scales) |
                                      reinterpret_cast<uintptr_t>(w_scales)) & 3u) == 0;
   if (fast)
-    gemm_kernel<BM, BN, WM, WN, true, false><<<(unsigned)items, threads, 0, stream>>>(
-        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, ntn, nfull);
+    gemm_kernel<BM, BN, WM, WN, true, false><<<tiles, threads, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
   else
-    gemm_kernel<BM, BN, WM, WN, false, false><<<(unsigned)items, threads, 0, stream>>>(
-        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, ntn, nfull);
+    gemm_kernel<BM, BN, WM, WN, false, false><<<tiles, threads, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
   return hipGetLastError();
 }
 

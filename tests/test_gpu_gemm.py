@@ -81,14 +81,14 @@ def test_decode_shapes(m, n, k):
 
 
 @pytest.mark.parametrize("m,n,k", [(4100, 4100, 512), (4100, 4100, 560)])
-def test_split_tail_tiles(m, n, k):
-    """More 256x256 tiles than CUs with a small last wave: the tail tiles run
-    as two K halves accumulated atomically (fast and masked-K paths, ragged
-    edges).  Checked in full, and twice for bit-identical results."""
+def test_many_tiles_ragged(m, n, k):
+    """More 256x256 tiles than CUs (several waves of workgroups through the
+    XCD-grouped tile order), ragged edges, fast and masked-K paths.  Checked
+    in full, and twice for bit-identical results."""
     a = W.adversarial(m + 5, m, k)
     w = W.adversarial(n + 9, n, k)
     qa, qw = Q.quantize(a), Q.quantize(w)
-    log(f"gemm split tail m={m} n={n} k={k}")
+    log(f"gemm many tiles m={m} n={n} k={k}")
     c1 = _gemm_dev(qa, qw)
     c2 = _gemm_dev(qa, qw)
     assert np.array_equal(c1, c2)
