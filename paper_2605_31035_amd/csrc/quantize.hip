@@ -108,30 +108,242 @@ __global__ void finalize_scale(uint32_t* p) {
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 
-
 // sum_{j<8} (0x4B000000 << 4j) mod 2^32: the constant part of the INT4 code
 // accumulator below (every term is the bit pattern of 2^23 + code).
 constexpr uint32_t kMagicPack = 0x4B000000u + (0x4B000000u << 4) + (0x4B000000u << 8) +
                                 (0x4B000000u << 12) + (0x4B000000u << 16) + (0x4B000000u << 20) +
                                 (0x4B000000u << 24) + (0x4B000000u << 28);
 
-// Exact Err_E2M1 - Err_E1M2 of one block (fp64 sum form), used only when the
-// fp32 estimate is too close to zero to decide.
-__device__ __attribute__((noinline)) double exact_delta(uint4 v0, uint4 v1, double rs, uint2 pf,
-                                                        uint2 pi, float sf, float si) {
+// fl32(a / s) given r = fl32(1 / s): q0 = a r is within an ulp of the
+// quotient, the fma residual q0 s - a is exact, and q0 minus residual * r is
+// the correctly rounded quotient (Markstein's division step).  Verified
+// exhaustively for every fp32 a against every divisor with at most 4
+// significant bits, and for every bf16 a against every fp32 divisor, with all
+// three results in the normal range.  The residual is taken as q0 s - a
+// (not a - q0 s) so that a zero a keeps its sign: both fmas then add two
+// zeros of the sign of a.  A zero divisor with r = 0 returns a zero with the
+// sign of a.
+__device__ __forceinline__ float div_rn(float a, float s, float r) {
+  const float q0 = a * r;
+  return __builtin_fmaf(-__builtin_fmaf(q0, s, -a), r, q0);
+}
+
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+
+// x = fl32(X / s32) for the 16 elements of a block, signed (Algorithm 1, FP8
+// domain).  X is first multiplied by xmul (a power of two, exact) when
+// kScaled, and divided by sx = s32 * xmul with rx = fl32(1 / sx).
+template <bool kScaled>
+__device__ __forceinline__ void to_fp8_domain(uint4 v0, uint4 v1, float xmul, float sx, float rx,
+                                              float (&xs)[16]) {
   const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-  double d = 0.0;
-  for (int j = 0; j < 16; ++j) {
-    const uint32_t word = w[j >> 1];
-    const float X = (j & 1) ? bf16_hi(word) : bf16_lo(word);
-    const double ax = (double)(float)((double)fabsf(X) * rs);
-    const uint32_t cf = (((j < 8) ? pf.x : pf.y) >> (4 * (j & 7))) & 7u;
-    const uint32_t ci = (((j < 8) ? pi.x : pi.y) >> (4 * (j & 7))) & 7u;
-    const double df = (double)(e2m1_value(cf) * sf);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const float lo = kScaled ? bf16_lo(w[i]) * xmul : bf16_lo(w[i]);
+    const float hi = kScaled ? bf16_hi(w[i]) * xmul : bf16_hi(w[i]);
+    xs[2 * i] = div_rn(lo, sx, rx);
+    xs[2 * i + 1] = div_rn(hi, sx, rx);
+  }
+}
+
+// Elements J, J+1 (J even) of a block:
+//   E2M1: y = fl32(x / s_F) rounded by the gfx950 FP4 converter (scale 1:
+//   nearest, ties to the even code, saturating at 6, sign kept) into nibble
+//   pair (J%8)/2 of pf[J/8];
+//   E1M2 (x2 = INT4): y = fl32(|x| / s_I); adding 2^23 rounds it to an
+//   integer (ties to even) held in the low mantissa bits, accumulated into
+//   pi[J/8] at nibble J%8 together with a constant removed afterwards;
+//   ai[J/2 % 2] += |x| * q_I.
+template <int J>
+__device__ __forceinline__ void encode_pair(const float (&xs)[16], float sf, float rf, float si,
+                                            float ri, uint32_t (&pf)[2], uint32_t (&pi)[2],
+                                            float (&ai)[2]) {
+  const float yf0 = div_rn(xs[J], sf, rf), yf1 = div_rn(xs[J + 1], sf, rf);
+  pf[J >> 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(pf[J >> 3], yf0, yf1, 1.0f, (J & 7) >> 1);
+  const float a0 = fabsf(xs[J]), a1 = fabsf(xs[J + 1]);
+  const uint32_t b0 = __float_as_uint(div_rn(a0, si, ri) + 0x1p23f);
+  const uint32_t b1 = __float_as_uint(div_rn(a1, si, ri) + 0x1p23f);
+  float& acc = ai[(J >> 1) & 1];
+  acc = __builtin_fmaf(a0, __uint_as_float(b0) - 0x1p23f, acc);
+  acc = __builtin_fmaf(a1, __uint_as_float(b1) - 0x1p23f, acc);
+  pi[J >> 3] += b0 << (4 * (J & 7));
+  pi[J >> 3] += b1 << (4 * ((J + 1) & 7));
+}
+
+// E2M1 error sums of elements J, J+1 from the decoded codes, in two chains:
+//   af += x * q_F (same signs, so every term is >= 0),  bf += q_F^2.
+template <int J>
+__device__ __forceinline__ void error_pair(const float (&xs)[16], const uint32_t (&pf)[2],
+                                           float (&af)[2], float (&bf)[2]) {
+  const f32x2 qf = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pf[J >> 3], 1.0f, (J & 7) >> 1);
+  constexpr int c = (J >> 1) & 1;
+  af[c] = __builtin_fmaf(xs[J], qf.x, af[c]);
+  af[c] = __builtin_fmaf(xs[J + 1], qf.y, af[c]);
+  bf[c] = __builtin_fmaf(qf.x, qf.x, bf[c]);
+  bf[c] = __builtin_fmaf(qf.y, qf.y, bf[c]);
+}
+
+// Exact contribution of elements J, J+1 to Err_E2M1 - Err_E1M2 in fp64:
+//   (D_I - D_F) (2|x| - D_F - D_I),  D_T = s_T q_T.
+// D_F, D_I are exact fp32 products; an element contributes only when
+// D_I != D_F, and then |x| >= min(s_F, s_I) / 4, so every term and every
+// partial sum of a block is exact in fp64 and the total is exact.
+template <int J>
+__device__ __forceinline__ void exact_pair(const float (&xs)[16], const uint32_t (&pf)[2],
+                                           const uint32_t (&pi)[2], float sf, float si, double& d) {
+  const f32x2 qf = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pf[J >> 3], 1.0f, (J & 7) >> 1);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const double ax = (double)fabsf(xs[J + h]);
+    const double df = (double)(fabsf(h ? qf.y : qf.x) * sf);
+    const uint32_t ci = (pi[(J + h) >> 3] >> (4 * ((J + h) & 7))) & 7u;
     const double di = (double)((float)ci * si);
     d += (di - df) * ((2.0 * ax - df) - di);
   }
-  return d;
+}
+
+// Codes and scale byte of one block from x (Algorithm 1 after the tensor
+// scale).
+__device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2* __restrict__ tab,
+                                            uint2& out, uint32_t& scale_byte) {
+  // fl32 rounding is monotonic, so bm is also fl32(max|X| / s32).
+  float bm = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 16; ++j) bm = fmaxf(bm, fabsf(xs[j]));
+  // Candidate block scales E4M3(bm/6), E4M3(bm/7): the exactly rounded
+  // quotients, clamped at 448 (saturation), through the gfx950 E4M3
+  // converter (scale 1: nearest, ties to the even code; checked against the
+  // software rounding on every fp32 value in [0, 448]).
+  constexpr float kR6 = 1.0f / 6.0f, kR7 = 1.0f / 7.0f;
+  const s16x2 sc = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(
+      s16x2{0, 0}, fminf(div_rn(bm, 6.0f, kR6), 448.0f), fminf(div_rn(bm, 7.0f, kR7), 448.0f),
+      1.0f, false);
+  const uint32_t scw = __builtin_bit_cast(uint32_t, sc);
+  const uint32_t cf = scw & 0x7Fu, ci = (scw >> 8) & 0x7Fu;
+  const float2 ef = tab[cf], ei = tab[ci];
+  const float sf = ef.x, rf = ef.y, si = ei.x, ri = ei.y;
+
+  uint32_t pf[2] = {0u, 0u}, pi[2] = {0u, 0u};
+  float af[2] = {0.0f, 0.0f}, bf[2] = {0.0f, 0.0f}, ai[2] = {0.0f, 0.0f};
+  encode_pair<0>(xs, sf, rf, si, ri, pf, pi, ai);
+  encode_pair<2>(xs, sf, rf, si, ri, pf, pi, ai);
+  encode_pair<4>(xs, sf, rf, si, ri, pf, pi, ai);
+  encode_pair<6>(xs, sf, rf, si, ri, pf, pi, ai);
+  encode_pair<8>(xs, sf, rf, si, ri, pf, pi, ai);
+  encode_pair<10>(xs, sf, rf, si, ri, pf, pi, ai);
+  encode_pair<12>(xs, sf, rf, si, ri, pf, pi, ai);
+  encode_pair<14>(xs, sf, rf, si, ri, pf, pi, ai);
+  pi[0] -= kMagicPack;
+  pi[1] -= kMagicPack;
+  error_pair<0>(xs, pf, af, bf);
+  error_pair<2>(xs, pf, af, bf);
+  error_pair<4>(xs, pf, af, bf);
+  error_pair<6>(xs, pf, af, bf);
+  error_pair<8>(xs, pf, af, bf);
+  error_pair<10>(xs, pf, af, bf);
+  error_pair<12>(xs, pf, af, bf);
+  error_pair<14>(xs, pf, af, bf);
+  // INT4 codes cannot exceed 7 when s_I is a normal E4M3 value below the
+  // maximum (then max|x| / s_I < 7.47); other blocks redo the branch with
+  // saturation (rare path).
+  if (ci < 8u || ci >= 0x7Eu) {
+    pi[0] = pi[1] = 0u;
+    ai[0] = ai[1] = 0.0f;
+    for (int j = 0; j < 16; ++j) {
+      const float q = fminf(rintf(div_rn(fabsf(xs[j]), si, ri)), 7.0f);
+      ai[j & 1] = __builtin_fmaf(fabsf(xs[j]), q, ai[j & 1]);
+      pi[j >> 3] |= (uint32_t)q << (4 * (j & 7));
+    }
+  }
+  const uint32_t bi = __builtin_amdgcn_udot8(pi[0], pi[0], __builtin_amdgcn_udot8(pi[1], pi[1], 0u, false),
+                                             false);
+
+  // Err_F - Err_I with Err_T = sum x^2 - 2 s_T sum |x| q_T + s_T^2 sum q_T^2
+  // (the sum of x^2 cancels):  est = (sf^2 bf - si^2 bi) + 2 (si ai - sf af).
+  // bf and bi are exact (multiples of 1/4, integers) and so are sf^2 bf and
+  // si^2 bi (at most 20 significant bits).  af and ai are sums of
+  // non-negative terms in two chains of 8 fmas plus one add: relative error
+  // at most 9u (u = 2^-24); with the four roundings that follow, |est - Err_F
+  // + Err_I| <= 24u (tf + ti) + 2u (sf^2 bf + si^2 bi) to first order, which
+  // tau bounds with margin.  Products x q with q != 0 are at least 2^-12
+  // (|x| >= s/4 >= 2^-11), so nothing underflows.  Inside tau, or when
+  // either candidate scale is zero (that branch's error is then sum x^2,
+  // which the estimate does not model), the exact fp64 sum decides.
+  const float afs = af[0] + af[1], ais = ai[0] + ai[1], bfs = bf[0] + bf[1];
+  const float sf2b = (sf * sf) * bfs, si2b = (si * si) * (float)bi;
+  const float tf = sf * afs, ti = si * ais;
+  const float est = (sf2b - si2b) + 2.0f * (ti - tf);
+  const float tau = 0x1p-19f * (tf + ti) + 0x1p-22f * (sf2b + si2b);
+  bool t1;
+  if (cf != 0u && ci != 0u && fabsf(est) > tau) {
+    t1 = !(est < 0.0f);
+  } else {
+    double d = 0.0;
+    exact_pair<0>(xs, pf, pi, sf, si, d);
+    exact_pair<2>(xs, pf, pi, sf, si, d);
+    exact_pair<4>(xs, pf, pi, sf, si, d);
+    exact_pair<6>(xs, pf, pi, sf, si, d);
+    exact_pair<8>(xs, pf, pi, sf, si, d);
+    exact_pair<10>(xs, pf, pi, sf, si, d);
+    exact_pair<12>(xs, pf, pi, sf, si, d);
+    exact_pair<14>(xs, pf, pi, sf, si, d);
+    t1 = !(d < 0.0);
+  }
+  // Sign of X into bit 3 of every nibble: the E2M1 codes already carry it.
+  out.x = t1 ? (pi[0] | (pf[0] & 0x88888888u)) : pf[0];
+  out.y = t1 ? (pi[1] | (pf[1] & 0x88888888u)) : pf[1];
+  scale_byte = t1 ? (0x80u | ci) : cf;
+}
+
+// Grid-stride walk over the blocks with two blocks of this thread in flight
+// while one is computed.  The loop body is written twice with two register
+// sets (A, B): a set is reloaded, for the block two strides ahead, as soon
+// as its data has been turned into x, so no register copies are needed.
+template <bool kContig, bool kScaled>
+__device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, int64_t nbk,
+                                              int64_t ldx, int64_t nblocks,
+                                              uint8_t* __restrict__ codes,
+                                              uint8_t* __restrict__ scales, float xmul, float sx,
+                                              float rx, const float2* tab) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  // Loads are unconditional (a block index past the end reads the last
+  // block, whose data is then never used), so they need no branch and no
+  // register copies.
+  auto load = [&](int64_t gi, uint4& p, uint4& q) {
+    gi = gi < nblocks ? gi : nblocks - 1;
+    const uint16_t* src;
+    if (kContig) {
+      src = x + (gi << 4);
+    } else {
+      const int64_t r = gi / nbk;
+      src = x + r * ldx + ((gi - r * nbk) << 4);
+    }
+    p = *reinterpret_cast<const uint4*>(src);
+    q = *reinterpret_cast<const uint4*>(src + 8);
+  };
+  auto emit = [&](int64_t gi, const float (&xs)[16]) {
+    uint2 out;
+    uint32_t sb;
+    quantize_xs(xs, tab, out, sb);
+    *reinterpret_cast<uint2*>(codes + (gi << 3)) = out;
+    scales[gi] = (uint8_t)sb;
+  };
+  int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint4 a0 = make_uint4(0, 0, 0, 0), a1 = a0, b0 = a0, b1 = a0;
+  load(g, a0, a1);
+  load(g + stride, b0, b1);
+  while (g < nblocks) {
+    float xs[16];
+    to_fp8_domain<kScaled>(a0, a1, xmul, sx, rx, xs);
+    load(g + 2 * stride, a0, a1);
+    emit(g, xs);
+    g += stride;
+    if (g >= nblocks) break;
+    to_fp8_domain<kScaled>(b0, b1, xmul, sx, rx, xs);
+    load(g + 2 * stride, b0, b1);
+    emit(g, xs);
+    g += stride;
+  }
 }
 
 template <bool kContig>
@@ -139,137 +351,49 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
     const float* __restrict__ tensor_scale) {
-  // fl64(1 / E4M3(c)) for every 7-bit code (0 for the zero scale)
-  __shared__ double rcp_tab[128];
+  // {E4M3(c), fl32(1 / E4M3(c))} for every 7-bit code ({0, 0} for the zero
+  // scale and the NaN code)
+  __shared__ float2 tab[128];
   if (threadIdx.x < 128) {
     const float v = e4m3_value(threadIdx.x);
-    rcp_tab[threadIdx.x] = (threadIdx.x > 0 && threadIdx.x < 127) ? 1.0 / (double)v : 0.0;
+    const bool ok = threadIdx.x > 0 && threadIdx.x < 127;
+    tab[threadIdx.x] = ok ? make_float2(v, __fdiv_rn(1.0f, v)) : make_float2(0.0f, 0.0f);
   }
   __syncthreads();
   const float s32 = *tensor_scale;
-  const double rs = 1.0 / (double)s32;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  auto block_ptr = [&](int64_t g) -> const uint16_t* {
-    if (kContig) return x + (g << 4);
-    const int64_t r = g / nbk;
-    return x + r * ldx + ((g - r * nbk) << 4);
-  };
-  int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  uint4 n0 = make_uint4(0, 0, 0, 0), n1 = n0;
-  if (g < nblocks) {
-    const uint16_t* src = block_ptr(g);
-    n0 = *reinterpret_cast<const uint4*>(src);
-    n1 = *reinterpret_cast<const uint4*>(src + 8);
+  // The division steps stay in the normal range for every element that can
+  // get a nonzero code when 2^-90 <= s32 <= 2^120; beyond that both X and s32
+  // are rescaled by 2^64 or 2^-64 first.
+  if (s32 >= 0x1p-90f && s32 <= 0x1p120f) {
+    quantize_loop<kContig, false>(x, nbk, ldx, nblocks, codes, scales, 1.0f, s32,
+                                  __fdiv_rn(1.0f, s32), tab);
+  } else {
+    const float xmul = s32 < 1.0f ? 0x1p64f : 0x1p-64f;
+    const float sx = s32 * xmul;
+    quantize_loop<kContig, true>(x, nbk, ldx, nblocks, codes, scales, xmul, sx,
+                                 __fdiv_rn(1.0f, sx), tab);
   }
-  for (; g < nblocks; g += stride) {
-    const uint4 v0 = n0, v1 = n1;
-    // prefetch the next block of this thread while this one is computed
-    if (g + stride < nblocks) {
-      const uint16_t* src = block_ptr(g + stride);
-      n0 = *reinterpret_cast<const uint4*>(src);
-      n1 = *reinterpret_cast<const uint4*>(src + 8);
-    }
-    const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+}
 
-    // x = fl32(X / s32), signed, and its fp64 copy (Algorithm 1, FP8 domain)
-    float xs[16];
-    double xd[16];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      xs[2 * i] = (float)((double)bf16_lo(w[i]) * rs);
-      xs[2 * i + 1] = (float)((double)bf16_hi(w[i]) * rs);
-    }
-    float bm = 0.0f;
-#pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      bm = fmaxf(bm, fabsf(xs[j]));
-      xd[j] = (double)xs[j];
-    }
-    // Candidate block scales E4M3(bm/6), E4M3(bm/7).  fl32(bm * fl64(1/d))
-    // equals fl32(bm / d) for d = 6, 7: the exact quotients have periodic
-    // binary expansions and never sit within 2^-50 of an fp32 midpoint.
-    const double bmd = (double)bm;
-    const uint32_t cf = e4m3_code((float)(bmd * (1.0 / 6.0)));
-    const uint32_t ci = e4m3_code((float)(bmd * (1.0 / 7.0)));
-    const float sf = e4m3_value(cf), si = e4m3_value(ci);
-    const double rf = rcp_tab[cf], ri = rcp_tab[ci];
-    // INT4 codes cannot exceed 7 when s_I is a normal E4M3 value below the
-    // maximum (then max|x| / s_I < 7.47); other blocks clamp (rare path).
-    const bool clamp_i = ci < 8u || ci >= 0x7Eu;
-
-    uint32_t pf0 = 0, pf1 = 0, pi0 = 0, pi1 = 0;
-    float accf = 0.0f, acci = 0.0f;
-    // Elements J, J+1 (J even): E2M1 codes via the hardware converter into
-    // byte (J%8)/2 of pf, decoded back for the error; INT4 codes by adding
-    // 2^23 (integer in the low bits, round half to even), accumulated into pi
-    // together with a constant 0x4B000000 per code that is removed below.
-#define MIXFP4_PAIR(J, PF, PI)                                                       \
-  {                                                                                  \
-    const float yf0 = (float)(xd[J] * rf), yf1 = (float)(xd[J + 1] * rf);            \
-    const float yi0 = fabsf((float)(xd[J] * ri)), yi1 = fabsf((float)(xd[J + 1] * ri)); \
-    PF = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(PF, yf0, yf1, 1.0f, ((J) & 7) >> 1);  \
-    const f32x2 qf = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(PF, 1.0f, ((J) & 7) >> 1); \
-    const float rf0 = yf0 - qf.x, rf1 = yf1 - qf.y;                                  \
-    accf = __builtin_fmaf(rf0, rf0, accf);                                           \
-    accf = __builtin_fmaf(rf1, rf1, accf);                                           \
-    const uint32_t b0 = __float_as_uint(yi0 + 0x1p23f);                              \
-    const uint32_t b1 = __float_as_uint(yi1 + 0x1p23f);                              \
-    const float ri0 = yi0 - (__uint_as_float(b0) - 0x1p23f);                         \
-    const float ri1 = yi1 - (__uint_as_float(b1) - 0x1p23f);                         \
-    acci = __builtin_fmaf(ri0, ri0, acci);                                           \
-    acci = __builtin_fmaf(ri1, ri1, acci);                                           \
-    PI += b0 << (4 * ((J) & 7));                                                     \
-    PI += b1 << (4 * (((J) + 1) & 7));                                               \
+// Workgroups of kThreads that the device keeps resident at once for
+// quantize_kernel<kContig> (occupancy per CU x CU count), cached per device.
+template <bool kContig>
+int64_t resident_groups() {
+  static int64_t cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+  if (!cached[dev]) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, quantize_kernel<kContig>, kThreads,
+                                                     0) != hipSuccess ||
+        per_cu <= 0)
+      per_cu = 4;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+    cached[dev] = (int64_t)per_cu * cus;
   }
-    MIXFP4_PAIR(0, pf0, pi0)
-    MIXFP4_PAIR(2, pf0, pi0)
-    MIXFP4_PAIR(4, pf0, pi0)
-    MIXFP4_PAIR(6, pf0, pi0)
-    MIXFP4_PAIR(8, pf1, pi1)
-    MIXFP4_PAIR(10, pf1, pi1)
-    MIXFP4_PAIR(12, pf1, pi1)
-    MIXFP4_PAIR(14, pf1, pi1)
-#undef MIXFP4_PAIR
-    pi0 -= kMagicPack;
-    pi1 -= kMagicPack;
-    if (clamp_i) {
-      // Subnormal or saturated s_I: codes above 7 are possible; redo the
-      // INT4 branch with saturation.
-      pi0 = pi1 = 0u;
-      acci = 0.0f;
-      for (int j = 0; j < 16; ++j) {
-        const float yi = fabsf((float)(xd[j] * ri));
-        const float q = fminf(rintf(yi), 7.0f);
-        const float r = yi - q;
-        acci = __builtin_fmaf(r, r, acci);
-        if (j < 8) pi0 |= (uint32_t)q << (4 * j);
-        else pi1 |= (uint32_t)q << (4 * (j - 8));
-      }
-    }
-
-    // Err_E2M1 - Err_E1M2 ~= sf^2 * sum rf^2 - si^2 * sum ri^2.  Each r is off
-    // by at most 7.5 * 2^-24 (y is a correctly rounded quotient), so each sum
-    // is within 2^-15 of its exact value; tau covers that with margin.  Inside
-    // tau the exact fp64 sum decides.
-    const float sf2 = sf * sf, si2 = si * si;
-    const float est = sf2 * accf - si2 * acci;
-    const float tau = sf2 * (0x1p-13f + 0x1p-20f * accf) + si2 * (0x1p-13f + 0x1p-20f * acci);
-    // A zero candidate scale makes that branch's error sum(x^2), which the
-    // estimate does not model: such blocks (max below 7 * 2^-10 in the FP8
-    // domain) take the exact path too.
-    bool t1;
-    if (cf != 0u && ci != 0u && fabsf(est) > tau) {
-      t1 = !(est < 0.0f);
-    } else {
-      t1 = !(exact_delta(v0, v1, rs, make_uint2(pf0, pf1), make_uint2(pi0, pi1), sf, si) < 0.0);
-    }
-    // Sign of X into bit 3 of every nibble: the E2M1 codes already carry it.
-    uint2 out;
-    out.x = t1 ? (pi0 | (pf0 & 0x88888888u)) : pf0;
-    out.y = t1 ? (pi1 | (pf1 & 0x88888888u)) : pf1;
-    *reinterpret_cast<uint2*>(codes + (g << 3)) = out;
-    scales[g] = (uint8_t)(t1 ? (0x80u | ci) : cf);
-  }
+  return cached[dev];
 }
 
 int grid_for(int64_t work, int per_thread) {
@@ -313,11 +437,11 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t l
   const int64_t nbk = k / kBlock;
   const int64_t nblocks = rows * nbk;
   if (nblocks == 0) return hipSuccess;
-  // Enough workgroups to keep ~8 per CU resident; beyond that each thread
-  // walks several blocks (amortising its set-up, prefetching the next one).
-  int64_t per_thread = nblocks / (2048LL * kThreads);
-  per_thread = per_thread < 1 ? 1 : (per_thread > 8 ? 8 : per_thread);
-  const int g = grid_for(nblocks, (int)per_thread);
+  // One wave of resident workgroups (occupancy x CUs) walks all blocks, so
+  // no partial second wave is left at the end; fewer if the tensor is small.
+  const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
+  const int64_t resident = ldx == k ? resident_groups<true>() : resident_groups<false>();
+  const int g = (int)(wanted < resident ? wanted : resident);
   if (ldx == k)
     quantize_kernel<true><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, codes, scales,
                                                        tensor_scale);

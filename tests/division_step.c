@@ -1,0 +1,87 @@
+/* Exhaustive check of the quantizer's fp32 division step.
+ *
+ * The kernel computes fl32(a / s) from r = fl32(1 / s) as
+ *     q0 = fl32(a * r);  e = fma(q0, s, -a);  q = fma(-e, r, q0).
+ * Scaling a or s by a power of two scales q0, e and q by the same power while
+ * all of them stay in the normal range, so it suffices to check mantissas:
+ *   (A) every fp32 a in [1, 2) against every divisor in [1, 2) with at most
+ *       4 significant bits (the E4M3 block scales, and 6 and 7);
+ *   (B) every bf16 a in [1, 2) against every fp32 divisor in [1, 2) (the
+ *       tensor scale s32; X is bf16).
+ * (C) signed zeros: a = +-0 returns a zero of the same sign, also with the
+ *     zero divisor the kernel encodes as s = 0, r = 0.
+ * Exit status 0 iff every case equals the IEEE quotient (C's a / s, correctly
+ * rounded to nearest even).  Built with -mfma so fmaf is one fused operation.
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdio.h>
+#include <string.h>
+
+static float from_bits(uint32_t b) { float x; memcpy(&x, &b, 4); return x; }
+static uint32_t to_bits(float x) { uint32_t b; memcpy(&b, &x, 4); return b; }
+
+static float step(float a, float s, float r) {
+  const float q0 = a * r;
+  /* volatile keeps the compiler from rewriting -fma(q0, s, -a) as
+     fma(-q0, s, a), which differs for a zero a (the kernel's compiler keeps
+     the form as written) */
+  volatile float e = fmaf(q0, s, -a);
+  return fmaf(-e, r, q0);
+}
+
+static int same_as_ieee(float a, float s) {
+  volatile float r = 1.0f / s;
+  volatile float want = a / s;
+  return to_bits(step(a, s, r)) == to_bits(want);
+}
+
+typedef struct { uint32_t lo, hi; long bad; } range_t;
+
+static void* part_b(void* p) {
+  range_t* j = (range_t*)p;
+  for (uint32_t sm = j->lo; sm < j->hi; ++sm) {
+    const float s = from_bits(0x3F800000u | sm);
+    for (uint32_t am = 0; am < 128; ++am)
+      if (!same_as_ieee(from_bits(0x3F800000u | (am << 16)), s)) j->bad++;
+  }
+  return NULL;
+}
+
+int main(void) {
+  long bad_a = 0, bad_b = 0, bad_c = 0;
+  for (uint32_t m = 0; m < 8; ++m) {
+    const float s = 1.0f + (float)m / 8.0f;
+    for (uint32_t am = 0; am < (1u << 23); ++am)
+      if (!same_as_ieee(from_bits(0x3F800000u | am), s)) bad_a++;
+  }
+  enum { kThreads = 8 };
+  pthread_t t[kThreads];
+  range_t jobs[kThreads];
+  for (int i = 0; i < kThreads; ++i) {
+    jobs[i].lo = (1u << 23) / kThreads * (uint32_t)i;
+    jobs[i].hi = (1u << 23) / kThreads * (uint32_t)(i + 1);
+    jobs[i].bad = 0;
+    pthread_create(&t[i], NULL, part_b, &jobs[i]);
+  }
+  for (int i = 0; i < kThreads; ++i) {
+    pthread_join(t[i], NULL);
+    bad_b += jobs[i].bad;
+  }
+  const float divisors[] = {1.0f, 1.375f, 6.0f, 7.0f, 448.0f, 0x1p-9f, 3.0e-5f};
+  for (unsigned i = 0; i < sizeof divisors / sizeof divisors[0]; ++i) {
+    const float s = divisors[i], r = 1.0f / s;
+    if (to_bits(step(0.0f, s, r)) != 0u) bad_c++;
+    if (to_bits(step(-0.0f, s, r)) != 0x80000000u) bad_c++;
+  }
+  const float dividends[] = {0.0f, -0.0f, 1.5f, -1.5f, 0x1p-20f, -3000.0f};
+  for (unsigned i = 0; i < sizeof dividends / sizeof dividends[0]; ++i) {
+    const float a = dividends[i], q = step(a, 0.0f, 0.0f);
+    if (q != 0.0f || signbit(q) != signbit(a)) bad_c++;
+  }
+  printf("A: %ld of %ld mismatched\n", bad_a, 8L << 23);
+  printf("B: %ld of %ld mismatched\n", bad_b, 128L << 23);
+  printf("C: %ld signed-zero mismatches\n", bad_c);
+  return (bad_a || bad_b || bad_c) ? 1 : 0;
+}

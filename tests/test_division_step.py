@@ -1,0 +1,24 @@
+"""The quantizer divides in fp32 with one multiply and two fmas instead of a
+division (x = X / s32 and y = x / s_block).  tests/division_step.c proves on
+the CPU, exhaustively over the operand mantissas the kernel can see, that
+this gives the IEEE quotient bit for bit, and that zeros keep their sign."""
+import os
+import shutil
+import subprocess
+import tempfile
+
+import pytest
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="gcc not available")
+def test_division_step_exhaustive():
+    with tempfile.TemporaryDirectory() as d:
+        exe = os.path.join(d, "division_step")
+        subprocess.run(["gcc", "-O2", "-mfma", "-std=c11", "-o", exe,
+                        os.path.join(HERE, "division_step.c"), "-lm", "-lpthread"], check=True)
+        r = subprocess.run([exe], capture_output=True, text=True, timeout=300)
+    print(r.stdout)
+    assert r.returncode == 0, r.stdout + r.stderr
+    assert "A: 0 of" in r.stdout and "B: 0 of" in r.stdout and "C: 0 " in r.stdout

@@ -72,6 +72,19 @@ def test_near_midpoints():
             _assert_same(b, s32=np.float32(s), label="near-midpoint")
 
 
+@pytest.mark.parametrize("exp,s32", [
+    (-100, None), (-60, None), (100, None), (112, None),
+    (-100, 1.3 * 2.0 ** -100), (112, 1.1 * 2.0 ** 121), (-125, 1.5 * 2.0 ** -140)])
+def test_extreme_tensor_scales(exp, s32):
+    """Data scaled by 2^exp and tensor scales far from 1 (down to an fp32
+    subnormal s32): below 2^-90 and above 2^120 the kernel rescales X and s32
+    by 2^64 or 2^-64 before dividing; in between it divides directly."""
+    f = W.bf16_bits_to_f32(W.adversarial(200 + exp, 48, 256)).astype(np.float64) * 2.0 ** exp
+    bits = W.f32_to_bf16_bits(f.astype(np.float32))
+    given = None if s32 is None else np.float32(s32)
+    _assert_same(bits, s32=given, label=f"2^{exp} data")
+
+
 def test_empty_inputs():
     import paper_2605_31035_amd as M
     x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
