@@ -5,73 +5,87 @@
 // through a small table, T (scale bit 7) selects the path.  Here the unified
 // value v is multiplied by the block's E4M3 scale s8 during decode: s8 has at
 // most 4 significant bits and v at most 3, so a = s8 * v has at most 7 and lies
-// in [2^-10, 3136] -- exact in bf16.  The bf16 operands feed
-// v_mfma_f32_32x32x16_bf16 with fp32 accumulation (the paper keeps FP16/FP32
-// accumulation unchanged, Sec. 3.3); the two fp32 tensor scales are applied
-// once in the epilogue.  App. B.1's factored per-block scale is not needed
-// because the per-element decode is exact.
+// in [2^-10, 3136] -- exact in fp16 (normal range, 11-bit significand).  The
+// fp16 operands feed v_mfma_f32_32x32x16_f16 (the bf16 rate) with fp32
+// accumulation (the paper keeps FP16/FP32 accumulation unchanged, Sec. 3.3);
+// the two fp32 tensor scales are applied once in the epilogue.  App. B.1's
+// factored per-block scale is not needed because the per-element decode is
+// exact.
 //
-// Decode.  For each of the 256 possible scale bytes a 16-byte table holds the
-// low and high bytes of the bf16 values s8 * v(m, T) for the 8 magnitudes m.
-// A code dword (8 nibbles) decodes with v_perm_b32 byte lookups: magnitudes
-// of the even and odd elements select low / high bytes, the nibble sign bit is
-// OR-ed into the high byte, and two more perms pair the bytes into bf16.  The
-// decoded 8 values are kept in the order [e0 e2 e4 e6 e1 e3 e5 e7]; A and W use
-// the same order, and a dot product does not depend on the order of k.
+// Decode.  Every unscaled unified value (E2M1 {0,.5,1,1.5,2,3,4,6}, E1M2 x2 =
+// INT4 {0..7}) has a zero low byte in fp16, so the 8 magnitudes of a codebook
+// are one 8-byte constant of high bytes.  A code dword (8 nibbles) decodes
+// with v_perm_b32 byte lookups into that constant (picked by T), the nibble
+// sign bit is OR-ed in, two more perms place the bytes as fp16 pairs, and
+// v_pk_mul_f16 multiplies by s8 (E4M3 -> fp32 by the hardware converter,
+// then to an fp16 pair).  No lookup depends on the scale byte, so decoding
+// reads nothing from LDS.  The decoded 8 values are kept in the order
+// [e0 e2 e4 e6 e1 e3 e5 e7]; A and W use the same order, and a dot product
+// does not depend on the order of k.
 //
-// Tiling.  A workgroup of 256 threads (2 x 2 waves) owns a BM x BN tile of C;
-// each wave owns (BM/2) x (BN/2) as 32 x 32 MFMA tiles.  The K loop steps 64
+// Tiling.  A workgroup of 64 * WM * WN threads owns a BM x BN tile of C; each
+// wave owns (BM/WM) x (BN/WN) as 32 x 32 MFMA tiles.  The K loop steps 64
 // (four 16-element scale blocks).  Per step every thread loads the packed
-// codes + scale bytes of (BM+BN)/256 rows one step ahead into registers,
-// decodes the previous step's rows into the idle half of a double-buffered
-// LDS tile while the waves run MFMAs from the other half, so every element
-// is decoded once per workgroup and one barrier separates the steps.
-// LDS layout per buffer: [slice s (16 K)][half h (8 K)][row of A|W][16 B];
-// the 64 lanes of a fragment read and the threads of a decode write both hit
-// consecutive 16-byte words.  Rows beyond m / n and blocks beyond k decode as
-// zeros; stores are masked.
+// codes + scale bytes of (BM+BN)/threads rows two steps ahead into
+// registers, decodes the next step's rows into the idle half of a
+// double-buffered LDS tile while the waves run MFMAs from the other half, so
+// every element is decoded once per workgroup and one barrier separates the
+// steps.  LDS layout per buffer: [slice s (16 K)][half h (8 K)][row of A|W]
+// [16 B]; the 64 lanes of a fragment read and the threads of a decode write
+// both hit consecutive 16-byte words.  Rows beyond m / n and blocks beyond k
+// decode as zeros; stores are masked.
 #include "formats.h"
 #include "internal.h"
 
 namespace mixfp4 {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kStepBlocks = 4;               // scale blocks per K step (64 elements)
 
-// Table of bf16 bytes for every scale byte: {lo bytes m=0..3, lo 4..7, hi 0..3, hi 4..7}.
-__device__ __forceinline__ uint4 make_table_entry(uint32_t sb) {
+// High bytes of the fp16 values of magnitudes 0..7 (bytes 0-3 in the low
+// dword): E2M1 {0, .5, 1, 1.5, 2, 3, 4, 6} and E1M2 x2 = INT4 {0, ..., 7}.
+constexpr uint32_t kE2M1Lo = 0x3E3C3800u, kE2M1Hi = 0x46444240u;
+constexpr uint32_t kInt4Lo = 0x42403C00u, kInt4Hi = 0x47464544u;
+
+// Decoding constants of one block from its scale byte: the codebook's high
+// bytes (by T = bit 7) and s8 = E4M3(bits 6:0) as an fp16 pair.  E4M3 ->
+// fp32 is exact (hardware converter) and so is fp32 -> fp16 (4 significant
+// bits, 2^-9 .. 448), whatever the rounding mode of the packing conversion.
+struct BlockDec {
+  uint32_t lo, hi;
+  f16x2 s8;
+};
+__device__ __forceinline__ BlockDec block_dec(uint32_t sb) {
+  BlockDec d;
   const bool t1 = (sb & 0x80u) != 0;
-  const float s8 = e4m3_value(sb & 0x7Fu);
-  uint32_t lo[2] = {0, 0}, hi[2] = {0, 0};
-#pragma unroll
-  for (uint32_t m = 0; m < 8; ++m) {
-    const float v = t1 ? (float)m : e2m1_value(m);
-    const uint32_t b = __float_as_uint(s8 * v) >> 16;     // exact bf16
-    lo[m >> 2] |= (b & 0xFFu) << (8 * (m & 3));
-    hi[m >> 2] |= (b >> 8) << (8 * (m & 3));
-  }
-  return make_uint4(lo[0], lo[1], hi[0], hi[1]);
+  d.lo = t1 ? kInt4Lo : kE2M1Lo;
+  d.hi = t1 ? kInt4Hi : kE2M1Hi;
+  const float s8 = __builtin_amdgcn_cvt_f32_fp8((int)(sb & 0x7Fu), 0);
+  d.s8 = __builtin_bit_cast(f16x2, __builtin_amdgcn_cvt_pkrtz(s8, s8));
+  return d;
+}
+
+__device__ __forceinline__ uint32_t scale_pair(uint32_t v, f16x2 s8) {
+  return __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, v) * s8);
 }
 
 // Decode one code dword (8 nibbles, element 2j in the low nibble of byte j)
-// with the table of its block into 8 bf16 in the order [e0 e2 e4 e6 e1 e3 e5 e7].
-__device__ __forceinline__ uint4 decode8(uint32_t c, uint4 tab) {
+// of a block into 8 fp16 s8 * v in the order [e0 e2 e4 e6 e1 e3 e5 e7].
+__device__ __forceinline__ uint4 decode8(uint32_t c, const BlockDec& d) {
   const uint32_t me = c & 0x07070707u;
   const uint32_t mo = (c >> 4) & 0x07070707u;
-  const uint32_t le = __builtin_amdgcn_perm(tab.y, tab.x, me);
-  const uint32_t lo = __builtin_amdgcn_perm(tab.y, tab.x, mo);
-  uint32_t he = __builtin_amdgcn_perm(tab.w, tab.z, me);
-  uint32_t ho = __builtin_amdgcn_perm(tab.w, tab.z, mo);
-  he |= (c << 4) & 0x80808080u;                 // sign of even elements
-  ho |= c & 0x80808080u;                        // sign of odd elements
+  const uint32_t he = __builtin_amdgcn_perm(d.hi, d.lo, me) | ((c << 4) & 0x80808080u);
+  const uint32_t ho = __builtin_amdgcn_perm(d.hi, d.lo, mo) | (c & 0x80808080u);
+  // selector byte 0x0C yields a zero byte: fp16 pairs {0, hi_a, 0, hi_b}
   uint4 r;
-  r.x = __builtin_amdgcn_perm(he, le, 0x05010400u);   // e0 e2
-  r.y = __builtin_amdgcn_perm(he, le, 0x07030602u);   // e4 e6
-  r.z = __builtin_amdgcn_perm(ho, lo, 0x05010400u);   // e1 e3
-  r.w = __builtin_amdgcn_perm(ho, lo, 0x07030602u);   // e5 e7
+  r.x = scale_pair(__builtin_amdgcn_perm(he, he, 0x010C000Cu), d.s8);   // e0 e2
+  r.y = scale_pair(__builtin_amdgcn_perm(he, he, 0x030C020Cu), d.s8);   // e4 e6
+  r.z = scale_pair(__builtin_amdgcn_perm(ho, ho, 0x010C000Cu), d.s8);   // e1 e3
+  r.w = scale_pair(__builtin_amdgcn_perm(ho, ho, 0x030C020Cu), d.s8);   // e5 e7
   return r;
 }
 
@@ -79,15 +93,14 @@ template <int BM, int BN, int WM, int WN>
 struct Tile {
   static constexpr int kThreads = 64 * WM * WN;
   static constexpr int kRowsAll = BM + BN;                 // A rows then W rows
-  static constexpr int kRowsPerThread = kRowsAll / kThreads;
+  static constexpr int kRowsPerThread = (kRowsAll + kThreads - 1) / kThreads;
+  static constexpr bool kEven = kRowsAll % kThreads == 0;  // every thread decodes R rows
   static constexpr int kWaveM = BM / WM, kWaveN = BN / WN;
   static constexpr int kTM = kWaveM / 32, kTN = kWaveN / 32;
   // uint4 words per (slice, half) plane and per buffer
   static constexpr int kPlane = kRowsAll;
   static constexpr int kBuf = kStepBlocks * 2 * kPlane;
-  static_assert(kRowsAll % kThreads == 0, "rows must split evenly over threads");
   static_assert(kTM >= 1 && kTN >= 1, "wave tile must hold whole 32x32 MFMA tiles");
-  static_assert(kThreads >= 256, "the scale table is built by the first 256 threads");
 };
 
 // Packed inputs of one row for one K step: 4 code qwords (4 blocks) + 4 scale bytes.
@@ -168,7 +181,6 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
     int64_t n, int64_t k, float* __restrict__ c) {
   using T = Tile<BM, BN, WM, WN>;
   constexpr int R = T::kRowsPerThread;
-  __shared__ uint4 table[256];
   // Two separate buffers (not one indexed array) so the compiler can see that
   // the decode stores of one step never alias the fragment loads of the other
   // and may interleave them with the MFMAs.
@@ -187,20 +199,22 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
   const int64_t n0 = (tile % ntn) * BN;
   const int wm = (wave / WN) * T::kWaveM, wn = (wave % WN) * T::kWaveN;
 
-  if (tid < 256) table[tid] = make_table_entry((uint32_t)tid);
-
   // rows this thread decodes: g = tid + threads * r over [A rows | W rows]
   const uint8_t* rc[R];
   const uint8_t* rs[R];
   bool rok[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    const int g = tid + T::kThreads * r;
+    // threads past the last row of an uneven split load row 0 of A (never
+    // decoded) so that their loads stay in bounds
+    const int g0 = tid + T::kThreads * r;
+    const bool in_tile = T::kEven || g0 < T::kRowsAll;
+    const int g = in_tile ? g0 : 0;
     const bool is_a = g < BM;
     int64_t row = is_a ? m0 + g : n0 + (g - BM);
     const int64_t lim = is_a ? m : n;
-    rok[r] = row < lim;
-    if (kFast && !rok[r]) row = lim - 1;
+    rok[r] = in_tile && row < lim;
+    if (kFast && row >= lim) row = lim - 1;
     rc[r] = (is_a ? a_codes : w_codes) + row * code_pitch;
     rs[r] = (is_a ? a_scales : w_scales) + row * kb_total;
   }
@@ -220,10 +234,11 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int g = tid + T::kThreads * r;
-      const uint4 tab = table[(p[r].s >> (8 * b)) & 0xFFu];
+      if (!T::kEven && g >= T::kRowsAll) continue;
+      const BlockDec d = block_dec((p[r].s >> (8 * b)) & 0xFFu);
       uint4* dst = wr + (b * 2) * T::kPlane + g;
-      dst[0] = decode8(p[r].c[b].x, tab);
-      dst[T::kPlane] = decode8(p[r].c[b].y, tab);
+      dst[0] = decode8(p[r].c[b].x, d);
+      dst[T::kPlane] = decode8(p[r].c[b].y, d);
     }
   };
 
@@ -243,15 +258,15 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
     if (decode) load_step(pn, s + 2);
     // keep the prefetch at the top of the step so its latency hides under the MFMAs
     __builtin_amdgcn_sched_barrier(0);
-    bf16x8 fa[2][T::kTM], fw[2][T::kTN];
+    f16x8 fa[2][T::kTM], fw[2][T::kTN];
     auto load_frags = [&](int buf, int sl) {
       const uint4* plane = rd + (sl * 2 + half) * T::kPlane;
 #pragma unroll
       for (int i = 0; i < T::kTM; ++i)
-        fa[buf][i] = __builtin_bit_cast(bf16x8, plane[wm + i * 32 + lrow]);
+        fa[buf][i] = __builtin_bit_cast(f16x8, plane[wm + i * 32 + lrow]);
 #pragma unroll
       for (int j = 0; j < T::kTN; ++j)
-        fw[buf][j] = __builtin_bit_cast(bf16x8, plane[BM + wn + j * 32 + lrow]);
+        fw[buf][j] = __builtin_bit_cast(f16x8, plane[BM + wn + j * 32 + lrow]);
     };
     load_frags(0, 0);
 #pragma unroll
@@ -262,13 +277,12 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
       for (int i = 0; i < T::kTM; ++i)
 #pragma unroll
         for (int j = 0; j < T::kTN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[cb][i], fw[cb][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[cb][i], fw[cb][j], acc[i][j], 0, 0, 0);
       if (decode) decode_block(p, wr, sl);
     }
     if constexpr (kSchedule) {
-      // Per slice: the next slice's fragment loads (and the decode table
-      // read), then every MFMA followed by a few decode VALU ops, then the
-      // decoded stores.
+      // Per slice: the next slice's fragment loads, then every MFMA followed
+      // by a few decode VALU ops, then the decoded stores.
       sched_slice<T::kTM + T::kTN + R, T::kTM * T::kTN, 2 * R>();
       sched_slice<T::kTM + T::kTN + R, T::kTM * T::kTN, 2 * R>();
       sched_slice<T::kTM + T::kTN + R, T::kTM * T::kTN, 2 * R>();
@@ -278,7 +292,6 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 
   RowPack pa[R], pb[R];
   load_step(pa, s_begin);
-  __syncthreads();   // table ready
 #pragma unroll
   for (int b = 0; b < kStepBlocks; ++b) decode_block(pa, lds0, b);
   load_step(pa, s_begin + 1);
@@ -325,7 +338,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // Each lane owns one W row (column n of C) and one quarter g of every
 // 128-element K step: it loads 16 code bytes (two scale blocks) and 2 scale
 // bytes, decodes its four code dwords straight into the B operands of four
-// v_mfma_f32_16x16x32_bf16, and never shares them.  The K slot (g, j) of
+// v_mfma_f32_16x16x32_f16, and never shares them.  The K slot (g, j) of
 // MFMA i holds element 32g + 8i + j of the step -- any order works as long as
 // A uses the same one.  A (at most 16 rows) is decoded once per workgroup, 512
 // K at a time, into a double-buffered LDS chunk laid out so that the A operand
@@ -347,7 +360,6 @@ __global__ __launch_bounds__(64 * kSkinnyWaves, 1) void gemm_skinny_kernel(
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c) {
-  __shared__ uint4 table[256];
   // one A chunk: 4 sub-chunks x [MFMA i (4)][quarter g (4)][row (16)] 16-byte words
   constexpr int kAWords = (kSkinnyChunk / 128) * 4 * 4 * kSkinnyRows;   // 1024 (16 KB)
   __shared__ uint4 abuf0[kAWords];
@@ -359,8 +371,6 @@ __global__ __launch_bounds__(64 * kSkinnyWaves, 1) void gemm_skinny_kernel(
   const int64_t code_pitch = k / 2, scale_pitch = k / kBlock;
   const int64_t steps = k / 128;                    // wave steps
   const int64_t chunks = k / kSkinnyChunk;
-
-  if (tid < 256) table[tid] = make_table_entry((uint32_t)tid);
 
   // this lane's W row (clamped rows only feed masked-out columns)
   const int64_t col = (int64_t)blockIdx.x * kSkinnyCols + wave * 16 + nn;
@@ -384,27 +394,26 @@ __global__ __launch_bounds__(64 * kSkinnyWaves, 1) void gemm_skinny_kernel(
   auto decode_a = [&](uint4* buf, int64_t chunk) {
     const int64_t ch = chunk < chunks ? chunk : chunks - 1;
     const uint2 cc = *reinterpret_cast<const uint2*>(ac + ch * (kSkinnyChunk / 2));
-    const uint4 tab = table[as[ch * (kSkinnyChunk / kBlock)]];
-    buf[adst] = decode8(cc.x, tab);
-    buf[adst + 64] = decode8(cc.y, tab);          // next 8 elements: MFMA index iq + 1
+    const BlockDec d = block_dec(as[ch * (kSkinnyChunk / kBlock)]);
+    buf[adst] = decode8(cc.x, d);
+    buf[adst + 64] = decode8(cc.y, d);            // next 8 elements: MFMA index iq + 1
   };
 
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
   auto wave_step = [&](const uint4* abuf, int sub, const WPack& p) {
-    const uint4 tlo = table[p.s & 0xFFu], thi = table[(p.s >> 8) & 0xFFu];
+    const BlockDec d0 = block_dec(p.s & 0xFFu), d1 = block_dec((p.s >> 8) & 0xFFu);
     const uint32_t cw[4] = {p.c.x, p.c.y, p.c.z, p.c.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const bf16x8 fb = __builtin_bit_cast(bf16x8, decode8(cw[i], i < 2 ? tlo : thi));
-      const bf16x8 fa = __builtin_bit_cast(bf16x8, abuf[sub * 256 + i * 64 + lane]);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa, fb, acc, 0, 0, 0);
+      const f16x8 fb = __builtin_bit_cast(f16x8, decode8(cw[i], i < 2 ? d0 : d1));
+      const f16x8 fa = __builtin_bit_cast(f16x8, abuf[sub * 256 + i * 64 + lane]);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa, fb, acc, 0, 0, 0);
     }
   };
 
   WPack p0, p1, p2, p3;
   load_w(p0, 0);
   load_w(p1, 1);
-  __syncthreads();   // table ready
   decode_a(abuf0, 0);
   for (int64_t ch = 0; ch < chunks; ++ch) {
     uint4* cur = (ch & 1) ? abuf1 : abuf0;

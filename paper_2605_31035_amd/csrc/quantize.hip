@@ -295,10 +295,10 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
   scale_byte = t1 ? (0x80u | ci) : cf;
 }
 
-// Grid-stride walk over the blocks with two blocks of this thread in flight
-// while one is computed.  The loop body is written twice with two register
-// sets (A, B): a set is reloaded, for the block two strides ahead, as soon
-// as its data has been turned into x, so no register copies are needed.
+// Grid-stride walk over the blocks.  The next block of this thread is
+// loaded as soon as the current one has been turned into x, so its load
+// overlaps this block's arithmetic (measured: a second block in flight, or
+// more waves per SIMD, gains nothing; the kernel is bound by VALU issue).
 template <bool kContig, bool kScaled>
 __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, int64_t nbk,
                                               int64_t ldx, int64_t nblocks,
@@ -321,28 +321,18 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
     p = *reinterpret_cast<const uint4*>(src);
     q = *reinterpret_cast<const uint4*>(src + 8);
   };
-  auto emit = [&](int64_t gi, const float (&xs)[16]) {
+  int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  uint4 a0, a1;
+  load(g, a0, a1);
+  for (; g < nblocks; g += stride) {
+    float xs[16];
+    to_fp8_domain<kScaled>(a0, a1, xmul, sx, rx, xs);
+    load(g + stride, a0, a1);
     uint2 out;
     uint32_t sb;
     quantize_xs(xs, tab, out, sb);
-    *reinterpret_cast<uint2*>(codes + (gi << 3)) = out;
-    scales[gi] = (uint8_t)sb;
-  };
-  int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  uint4 a0 = make_uint4(0, 0, 0, 0), a1 = a0, b0 = a0, b1 = a0;
-  load(g, a0, a1);
-  load(g + stride, b0, b1);
-  while (g < nblocks) {
-    float xs[16];
-    to_fp8_domain<kScaled>(a0, a1, xmul, sx, rx, xs);
-    load(g + 2 * stride, a0, a1);
-    emit(g, xs);
-    g += stride;
-    if (g >= nblocks) break;
-    to_fp8_domain<kScaled>(b0, b1, xmul, sx, rx, xs);
-    load(g + 2 * stride, b0, b1);
-    emit(g, xs);
-    g += stride;
+    *reinterpret_cast<uint2*>(codes + (g << 3)) = out;
+    scales[g] = (uint8_t)sb;
   }
 }
 
