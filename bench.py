@@ -1,18 +1,27 @@
 #!/usr/bin/env python3
 """Throughput of the MixFP4 hot path on one MI355X.
 
-One step = one pass of the whole path over the 7B-class prefill workload
-(seed 1): compute the tensor scale of and quantize A [2048, 4096] (Student-t
-nu=4 with 8 outlier channels x50), W1 [11008, 4096] and W2 [4096, 4096]
-(N(0, 0.02)), then C1 = A W1^T and C2 = A W2^T in fp32 on the matrix cores.
-Inputs are resident in HBM before timing starts.
+One step = one pass of the prefill path over the 7B-class workload (seed 1):
+compute the tensor scale of and quantize the activations A [2048, 4096]
+(Student-t nu=4 with 8 outlier channels x50), then C1 = A W1^T [2048, 11008]
+and C2 = A W2^T [2048, 4096] in fp32 on the matrix cores.  The weights W1
+[11008, 4096] and W2 [4096, 4096] (N(0, 0.02)) are quantized once before
+timing, as weights are quantized offline.  Inputs are resident in HBM before
+timing starts.
 
 Prints ONE JSON line:
-  value       GEMM FLOPs of the step / step time (TFLOP/s; the quantizer time is
-              inside the step time)
-  roofline    the GEMM kernel (dominant) against the dense bf16 MFMA peak,
-              timed with HIP events on the library's stream
-  quantize    the quantizer against HBM (algorithmic 2.5625 B / element)
+  value         GEMM FLOPs of the step / step time (TFLOP/s; the activation
+                quantizer is inside the step time)
+  roofline      the dominant kernel, the GEMM C1 = A W1^T, against the dense
+                bf16 MFMA peak: its FLOPs per launch over its mean launch time,
+                timed with HIP events on the stream it runs on
+  gemm2         the same for C2 = A W2^T
+  quantize      the quantizer kernel on the standalone 2^28-element tensor
+                (seed 4 block mixture) against HBM, with the tensor scale given
+                (algorithmic 2.5625 B / element), plus the end-to-end time with
+                the tensor scale computed on the device
+  quantize_step the activation quantizer inside the step
+  decode_shape  the memory-bound m = 16 GEMM (seed 3) against HBM
   cpu_baseline  the CPU oracle on a bounded sample of the same step
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 """
@@ -35,6 +44,26 @@ PEAK_HBM_GBPS = 8000.0             # MI355X HBM3E
 QUANT_BYTES_PER_ELEM = 2 + 0.5 + 1 / 16   # read bf16, write codes + scales
 AMAX_BYTES_PER_ELEM = 2                   # the tensor-scale pass re-reads X
 
+# HBM traffic of one launch of the dominant GEMM kernel (C1 = A W1^T, 256x256
+# tiles), from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then
+# WRITE_SIZE, KiB per dispatch; summary and commands in profiles/), scaled by
+# what the same counters read for a 512 MiB elementwise copy: FETCH x 2.0,
+# WRITE x 1.0.  Valid only for the GEMM source it was measured on (first 16
+# hex digits of its SHA-256); reported as null otherwise.
+GEMM1_TRAFFIC = {"gemm_src_sha256_16": "ac921d68e3ae719a",
+                 "fetch_kib": 46818.8, "write_kib": 88064.0,
+                 "fetch_scale": 2.0, "write_scale": 1.0}
+
+
+def gemm1_traffic_bytes():
+    import hashlib
+    with open(os.path.join(ROOT, "paper_2605_31035_amd", "csrc", "gemm.hip"), "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()[:16]
+    t = GEMM1_TRAFFIC
+    if sha != t["gemm_src_sha256_16"]:
+        return None
+    return round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024)
+
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
@@ -48,11 +77,12 @@ def _oracle_quantize_rows(args):
 
 
 def cpu_baseline(wl, budget_s: float = 10.0, max_reps: int = 8) -> dict:
-    """The CPU oracle on the same step: quantize A, W1, W2 (row chunks in a
-    process pool, one process per core; the tensor scale is the oracle's own
-    max over the full tensor) and both GEMMs as the oracle defines them (fp64
-    matmul of exactly dequantized operands plus the bound matmul, multithreaded
-    BLAS).  Whole steps repeat until `budget_s` has elapsed."""
+    """The CPU oracle on the same step: quantize A (row chunks in a process
+    pool, one process per core; the tensor scale is the oracle's own max over
+    the full tensor) and both GEMMs as the oracle defines them (fp64 matmul of
+    exactly dequantized operands plus the bound matmul, multithreaded BLAS).
+    The weights are quantized by the oracle once, outside the timed sample, as
+    in the GPU step.  Whole steps repeat until `budget_s` has elapsed."""
     from concurrent.futures import ProcessPoolExecutor
 
     from oracle import gemm as G
@@ -61,27 +91,79 @@ def cpu_baseline(wl, budget_s: float = 10.0, max_reps: int = 8) -> dict:
     cores = max(1, min(16, len(os.sched_getaffinity(0))))
     step_flops = sum(2.0 * wl.tensors[a].shape[0] * wl.tensors[w].shape[0] * wl.tensors[a].shape[1]
                      for a, w in wl.gemms)
+
+    def quantize(ex, bits):
+        s32 = Q.tensor_scale(bits)
+        parts = list(ex.map(_oracle_quantize_rows,
+                            [(c, s32) for c in np.array_split(bits, 4 * cores)]))
+        return Q.Quantized(codes=np.concatenate([p[0] for p in parts]),
+                           scales=np.concatenate([p[1] for p in parts]),
+                           s32=s32, t=None, sf_code=None, si_code=None, delta=None)
+
     times = []
     with ProcessPoolExecutor(cores) as ex:
+        weights = {w: quantize(ex, wl.tensors[w]) for _, w in wl.gemms}
         while len(times) < max_reps and sum(times) < budget_s:
             t0 = time.perf_counter()
-            quant = {}
-            for name, bits in wl.tensors.items():
-                s32 = Q.tensor_scale(bits)
-                parts = list(ex.map(_oracle_quantize_rows,
-                                    [(c, s32) for c in np.array_split(bits, 4 * cores)]))
-                quant[name] = Q.Quantized(codes=np.concatenate([p[0] for p in parts]),
-                                          scales=np.concatenate([p[1] for p in parts]),
-                                          s32=s32, t=None, sf_code=None, si_code=None, delta=None)
-            for a, w in wl.gemms:
-                G.gemm(*G.operands(quant[a], quant[w]))
+            qa = quantize(ex, wl.tensors["A"])
+            for _, w in wl.gemms:
+                G.gemm(*G.operands(qa, weights[w]))
             times.append(time.perf_counter() - t0)
     t = float(np.mean(times))
     return {
         "value": step_flops / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-        "sample": (f"{len(times)} full step(s) of the same workload: oracle quantize of all three "
-                   f"tensors ({cores} processes) + oracle fp64 GEMMs with their bound matmuls "
-                   f"(BLAS threads); {t:.2f} s per step"),
+        "sample": (f"{len(times)} full step(s) of the same workload: oracle quantize of A "
+                   f"({cores} processes) + oracle fp64 GEMMs C1, C2 with their bound matmuls "
+                   f"(BLAS threads), weights quantized by the oracle beforehand; "
+                   f"{t:.2f} s per step"),
+    }
+
+
+def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
+    """Quantize-only throughput on the standalone tensor Q [16384, 16384]
+    (2^28 elements, seed 4 block mixture).  The kernel alone: tensor scale
+    given (computed once beforehand on the device); end to end: tensor scale
+    computed on the device in the same call (one extra read of Q)."""
+    import workloads as W
+    log("generating the 2^28-element quantize-only tensor (seed 4)")
+    bits = W.large(tensors=("Q",)).tensors["Q"]
+    xq = torch.from_numpy(bits.view(np.int16)).to(dev).view(torch.bfloat16)
+    del bits
+    r, k = xq.shape
+    codes = torch.empty((r, k // 2), dtype=torch.uint8, device=dev)
+    scales = torch.empty((r, k // 16), dtype=torch.uint8, device=dev)
+    s32 = torch.empty(1, dtype=torch.float32, device=dev)
+    M.mixfp4_quantize(xq, None, codes, scales, scale_out=s32)     # s32 for the given mode
+
+    def timed(given: bool) -> float:
+        for _ in range(3):
+            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32)
+        torch.cuda.synchronize()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)]
+        e[0].record()
+        for i in range(iters):
+            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32)
+            e[i + 1].record()
+        torch.cuda.synchronize()
+        return float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(iters)]))
+
+    ms_given = timed(True)
+    ms_compute = timed(False)
+    n = xq.numel()
+    del xq, codes, scales
+    torch.cuda.empty_cache()
+    gbps = n * QUANT_BYTES_PER_ELEM / (ms_given * 1e-3) / 1e9
+    return {
+        "workload": "quantize-only Q[16384,16384] bf16 (2^28 elements), seed 4 block mixture: "
+                    "90% of 16-blocks N(0,0.1), 10% Laplace(0,1) with one x40 spike",
+        "bound": "hbm", "kernel": "quantize_kernel (tensor scale given)",
+        "achieved": round(gbps, 1), "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+        "frac": round(gbps / PEAK_HBM_GBPS, 4), "us": round(ms_given * 1e3, 2),
+        "bytes_per_elem": QUANT_BYTES_PER_ELEM,
+        "compute_mode_us": round(ms_compute * 1e3, 2),
+        "compute_mode_GBps": round(n * QUANT_BYTES_PER_ELEM / (ms_compute * 1e-3) / 1e9, 1),
+        "compute_mode_note": "tensor scale computed on the device (amax pass + quantize); "
+                             "GB/s counts the same 2.5625 B/element",
     }
 
 
@@ -137,6 +219,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the extra decode-shape (m = 16) measurement")
+    ap.add_argument("--no-quantize-only", action="store_true",
+                    help="skip the quantize-only measurement on the 2^28-element tensor")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one elementwise copy of 512 MiB (read + write of known "
                          "size) so hardware byte counters can be scaled")
@@ -160,14 +244,15 @@ def main():
     torch.cuda.set_device(dev)
     x = {n: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
          for n, b in wl.tensors.items()}
-    q = {}
-    for n, t in x.items():
-        r, k = t.shape
-        q[n] = (torch.empty((r, k // 2), dtype=torch.uint8, device=dev),
-                torch.empty((r, k // 16), dtype=torch.uint8, device=dev),
-                torch.empty(1, dtype=torch.float32, device=dev))
-    c = {(a, w): torch.empty((x[a].shape[0], x[w].shape[0]), dtype=torch.float32, device=dev)
-         for a, w in wl.gemms}
+    (g1a, g1w), (g2a, g2w) = wl.gemms
+    # weights: quantized once, before timing
+    qw = {w: M.mixfp4_quantize(x[w]) for _, w in wl.gemms}
+    ra, ka = x["A"].shape
+    qa = (torch.empty((ra, ka // 2), dtype=torch.uint8, device=dev),
+          torch.empty((ra, ka // 16), dtype=torch.uint8, device=dev),
+          torch.empty(1, dtype=torch.float32, device=dev))
+    c1 = torch.empty((ra, x[g1w].shape[0]), dtype=torch.float32, device=dev)
+    c2 = torch.empty((ra, x[g2w].shape[0]), dtype=torch.float32, device=dev)
     if args.calibrate_copy:
         src = torch.ones(128 << 20, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
@@ -177,22 +262,23 @@ def main():
 
     ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
 
-    def step(record=None):
-        if record is not None:
-            record["q0"].record()
-        for n in x:
-            M.mixfp4_quantize(x[n], None, q[n][0], q[n][1], scale_out=q[n][2])
-        if record is not None:
-            record["q1"].record()
-        for a, w in wl.gemms:
-            M.mixfp4_gemm(q[a], q[w], out=c[(a, w)])
-        if record is not None:
-            record["g1"].record()
+    def step(e=None):
+        if e is not None:
+            e[0].record()
+        M.mixfp4_quantize(x["A"], None, qa[0], qa[1], scale_out=qa[2])
+        if e is not None:
+            e[1].record()
+        M.mixfp4_gemm(qa, qw[g1w], out=c1)
+        if e is not None:
+            e[2].record()
+        M.mixfp4_gemm(qa, qw[g2w], out=c2)
+        if e is not None:
+            e[3].record()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    marks = [{"q0": ev(), "q1": ev(), "g1": ev()} for _ in range(args.steps)]
+    marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -200,36 +286,42 @@ def main():
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
-    q_ms = float(np.mean([m["q0"].elapsed_time(m["q1"]) for m in marks]))
-    g_ms = float(np.mean([m["q1"].elapsed_time(m["g1"]) for m in marks]))
+    span = lambda a, b: float(np.mean([m[a].elapsed_time(m[b]) for m in marks]))  # noqa: E731
+    q_ms, g1_ms, g2_ms = span(0, 1), span(1, 2), span(2, 3)
 
-    gemm_flops = sum(2.0 * x[a].shape[0] * x[w].shape[0] * x[a].shape[1] for a, w in wl.gemms)
-    elems = sum(t.numel() for t in x.values())
-    q_bytes = elems * QUANT_BYTES_PER_ELEM
-    gemm_tflops = gemm_flops / (g_ms * 1e-3) / 1e12
-    q_gbps = q_bytes / (q_ms * 1e-3) / 1e9
+    fl1 = 2.0 * ra * x[g1w].shape[0] * ka
+    fl2 = 2.0 * ra * x[g2w].shape[0] * ka
+    tf1 = fl1 / (g1_ms * 1e-3) / 1e12
+    tf2 = fl2 / (g2_ms * 1e-3) / 1e12
+    qa_gbps = ra * ka * QUANT_BYTES_PER_ELEM / (q_ms * 1e-3) / 1e9
     out = {
         "metric": METRIC,
-        "value": round(gemm_flops / (ms_step * 1e-3) / 1e12, 3),
+        "value": round((fl1 + fl2) / (ms_step * 1e-3) / 1e12, 3),
         "unit": "TFLOP/s",
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "prefill_7b: quantize A[2048,4096] (Student-t nu=4, 8 outlier "
-                               "channels x50), W1[11008,4096], W2[4096,4096] (N(0,0.02)) with "
-                               "device-computed tensor scales, then C1=A W1^T, C2=A W2^T fp32",
-                   "seed": 1, "gemm_flops_per_step": gemm_flops,
-                   "quantized_elements_per_step": elems},
-        "roofline": {"bound": "mfma", "kernel": "gemm", "achieved": round(gemm_tflops, 2),
-                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(gemm_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
-        "quantize": {"bound": "hbm", "achieved": round(q_gbps, 1), "peak": PEAK_HBM_GBPS,
-                     "unit": "GB/s", "frac": round(q_gbps / PEAK_HBM_GBPS, 4),
-                     "ms_per_step": round(q_ms, 4),
-                     "note": "algorithmic 2.5625 B/element; the tensor-scale (amax) read "
-                             "pass is inside the timed quantize region but not in the bytes"},
-        "gemm_ms_per_step": round(g_ms, 4),
+                               "channels x50, tensor scale computed on the device), then "
+                               "C1=A W1^T [2048,11008] and C2=A W2^T [2048,4096] fp32; "
+                               "W1[11008,4096], W2[4096,4096] N(0,0.02) quantized before timing",
+                   "seed": 1, "gemm_flops_per_step": fl1 + fl2,
+                   "quantized_elements_per_step": ra * ka},
+        "roofline": {"bound": "mfma", "kernel": "gemm_kernel 256x256 tiles (C1 = A W1^T)",
+                     "achieved": round(tf1, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(tf1 / PEAK_BF16_TFLOPS, 4), "traffic": gemm1_traffic_bytes(),
+                     "algorithmic_bytes": ra * ka * QUANT_BYTES_PER_ELEM - ra * ka * 2
+                     + x[g1w].shape[0] * ka * (QUANT_BYTES_PER_ELEM - 2) + 4.0 * ra * x[g1w].shape[0],
+                     "flops_per_launch": fl1, "us_per_launch": round(g1_ms * 1e3, 2)},
+        "gemm2": {"kernel": "gemm_kernel 128x256 tiles (C2 = A W2^T)",
+                  "achieved": round(tf2, 2), "unit": "TFLOP/s",
+                  "frac": round(tf2 / PEAK_BF16_TFLOPS, 4), "us_per_launch": round(g2_ms * 1e3, 2)},
+        "quantize_step": {"what": "A[2048,4096] with the tensor scale computed on the device "
+                                  "(amax pass + reduction + quantize kernel)",
+                          "us": round(q_ms * 1e3, 2), "GBps": round(qa_gbps, 1),
+                          "bytes_per_elem": QUANT_BYTES_PER_ELEM},
+        "quantize": None if args.no_quantize_only else measure_quantize(M, torch, dev),
         "decode_shape": None if args.no_decode else measure_decode(M, torch, dev),
         "cpu_baseline": cpu,
     }

@@ -482,14 +482,19 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
                          stream>>>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
     return hipGetLastError();
   }
-  // Tile choice: 256 x 256 halves LDS traffic per MFMA but needs enough tiles
-  // to fill the 256 compute units; fall back to 128 x 128 otherwise.
+  // Tile choice (measured on MI355X): 256 x 256 with 8 waves is the most
+  // efficient tile per compute unit (least LDS traffic and decode work per
+  // MFMA), so it is used whenever it fills at least one round of the 256
+  // compute units; the clock headroom of a partly idle last round makes up for
+  // much of its imbalance.  Below that, 128 x 256 (same wave tiles, half the
+  // rows) if it fills most of a round, else 128 x 128.
   const int64_t tiles256 = ((m + 255) / 256) * ((n + 255) / 256);
-  const int64_t tiles128 = ((m + 127) / 128) * ((n + 127) / 128);
-  const double t256 = (double)((tiles256 + 255) / 256) * 4.0;          // 4x the work per tile
-  const double t128 = (double)((tiles128 + 255) / 256) * 1.0 / 0.6;    // lower MFMA efficiency
-  if (t256 <= t128)
+  const int64_t tiles128x256 = ((m + 127) / 128) * ((n + 255) / 256);
+  if (tiles256 >= 256)
     return launch_tile<256, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
+                                       c, stream);
+  if (tiles128x256 >= 192)
+    return launch_tile<128, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
                                        c, stream);
   return launch_tile<128, 128, 2, 2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
                                      c, stream);

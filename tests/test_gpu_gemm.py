@@ -95,6 +95,18 @@ def test_many_tiles_ragged(m, n, k):
     _check(c1, qa, qw)
 
 
+@pytest.mark.parametrize("m,n,k", [(2000, 3100, 512), (2000, 3100, 560)])
+def test_mid_size_ragged(m, n, k):
+    """Shapes with fewer 256x256 tiles than CUs but at least 192 of 128x256
+    (the 128x256 tile path), ragged in all three dimensions, fast and
+    masked-K paths; checked in full."""
+    a = W.adversarial(m + 11, m, k)
+    w = W.adversarial(n + 13, n, k)
+    qa, qw = Q.quantize(a), Q.quantize(w)
+    log(f"gemm mid size m={m} n={n} k={k}")
+    _check(_gemm_dev(qa, qw), qa, qw)
+
+
 def test_k_zero_writes_zeros():
     import paper_2605_31035_amd as M
     e = torch.empty((4, 0), dtype=torch.uint8, device="cuda")
