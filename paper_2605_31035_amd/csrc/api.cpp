@@ -51,6 +51,9 @@ int mixfp4_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uin
   if (!empty && (!aligned(x, 16) || !aligned(codes, 16))) return MIXFP4_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();   // drop stale errors so a launch failure is ours
+  if (flags == MIXFP4_SCALE_COMPUTE && !empty && mixfp4::quantize_is_small(rows, k))
+    return launch_status(mixfp4::launch_quantize_small(x, rows, k, ldx, codes, scales,
+                                                       tensor_scale, s));
   if (flags == MIXFP4_SCALE_COMPUTE) {
     const int st = launch_status(mixfp4::launch_tensor_scale(
         x, empty ? 0 : rows, k, ldx, empty ? nullptr : scales,

@@ -336,24 +336,27 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
   }
 }
 
-template <bool kContig>
-__global__ __launch_bounds__(kThreads) void quantize_kernel(
-    const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
-    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
-    const float* __restrict__ tensor_scale) {
-  // {E4M3(c), fl32(1 / E4M3(c))} for every 7-bit code ({0, 0} for the zero
-  // scale and the NaN code)
-  __shared__ float2 tab[128];
+// {E4M3(c), fl32(1 / E4M3(c))} for every 7-bit code ({0, 0} for the zero
+// scale and the NaN code), built by the first 128 threads; the caller
+// synchronizes before use.
+__device__ __forceinline__ void fill_scale_table(float2* tab) {
   if (threadIdx.x < 128) {
     const float v = e4m3_value(threadIdx.x);
     const bool ok = threadIdx.x > 0 && threadIdx.x < 127;
     tab[threadIdx.x] = ok ? make_float2(v, __fdiv_rn(1.0f, v)) : make_float2(0.0f, 0.0f);
   }
-  __syncthreads();
-  const float s32 = *tensor_scale;
-  // The division steps stay in the normal range for every element that can
-  // get a nonzero code when 2^-90 <= s32 <= 2^120; beyond that both X and s32
-  // are rescaled by 2^64 or 2^-64 first.
+}
+
+// Quantize blocks [this thread's grid-stride share] with tensor scale s32.
+// The division steps stay in the normal range for every element that can get
+// a nonzero code when 2^-90 <= s32 <= 2^120; beyond that both X and s32 are
+// rescaled by 2^64 or 2^-64 first.
+template <bool kContig>
+__device__ __forceinline__ void quantize_all(const uint16_t* __restrict__ x, int64_t nbk,
+                                             int64_t ldx, int64_t nblocks,
+                                             uint8_t* __restrict__ codes,
+                                             uint8_t* __restrict__ scales, float s32,
+                                             const float2* tab) {
   if (s32 >= 0x1p-90f && s32 <= 0x1p120f) {
     quantize_loop<kContig, false>(x, nbk, ldx, nblocks, codes, scales, 1.0f, s32,
                                   __fdiv_rn(1.0f, s32), tab);
@@ -363,6 +366,93 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     quantize_loop<kContig, true>(x, nbk, ldx, nblocks, codes, scales, xmul, sx,
                                  __fdiv_rn(1.0f, sx), tab);
   }
+}
+
+template <bool kContig>
+__global__ __launch_bounds__(kThreads) void quantize_kernel(
+    const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
+    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
+    const float* __restrict__ tensor_scale) {
+  __shared__ float2 tab[128];
+  fill_scale_table(tab);
+  __syncthreads();
+  quantize_all<kContig>(x, nbk, ldx, nblocks, codes, scales, *tensor_scale, tab);
+}
+
+// Small tensors with the tensor scale computed (at most kSmallElems
+// elements): one launch, at most one block per thread.  Every workgroup reads
+// the whole tensor for max|X| (a few hundred KB, from L2 after the first), so
+// all of them hold the same s32 without talking to each other; workgroup 0
+// stores it.  The read walks blocks in the order of the quantize assignment
+// (block w * kSmallThreads + t of workgroup w goes to its thread t), so each
+// thread keeps its own block from that pass and quantizes it without a
+// second read.  The maximum is order-independent: the result is the
+// two-pass one, bit for bit.
+constexpr int kSmallThreads = 1024;
+constexpr int64_t kSmallElems = int64_t(1) << 18;
+
+template <bool kContig>
+__global__ __launch_bounds__(kSmallThreads) void quantize_small_kernel(
+    const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
+    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, float* __restrict__ tensor_scale) {
+  __shared__ float2 tab[128];
+  __shared__ uint32_t wave_max[kSmallThreads / 64];
+  fill_scale_table(tab);
+  auto block_ptr = [&](int64_t g) -> const uint16_t* {
+    if (kContig) return x + (g << 4);
+    const int64_t r = g / nbk;
+    return x + r * ldx + ((g - r * nbk) << 4);
+  };
+  // max|X| as bf16 magnitude bits; eight blocks in flight per thread
+  constexpr int kInFlight = 8;
+  const int64_t rounds = (nblocks + kSmallThreads - 1) / kSmallThreads;
+  const int64_t mine = blockIdx.x;                  // round holding this thread's block
+  uint32_t mx = 0u;
+  uint4 k0 = make_uint4(0, 0, 0, 0), k1 = k0;
+  for (int64_t r0 = 0; r0 < rounds; r0 += kInFlight) {
+    uint4 v0[kInFlight], v1[kInFlight];
+#pragma unroll
+    for (int j = 0; j < kInFlight; ++j) {
+      int64_t g = (r0 + j) * kSmallThreads + threadIdx.x;
+      g = g < nblocks ? g : nblocks - 1;           // past the end: re-read the last block
+      const uint16_t* src = block_ptr(g);
+      v0[j] = *reinterpret_cast<const uint4*>(src);
+      v1[j] = *reinterpret_cast<const uint4*>(src + 8);
+    }
+#pragma unroll
+    for (int j = 0; j < kInFlight; ++j) {
+      mx = max(mx, max(absmax8(v0[j]), absmax8(v1[j])));
+      if (r0 + j == mine) {
+        k0 = v0[j];
+        k1 = v1[j];
+      }
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+  if ((threadIdx.x & 63) == 0) wave_max[threadIdx.x >> 6] = mx;
+  __syncthreads();                                  // also publishes the scale table
+  uint32_t r = wave_max[0];
+#pragma unroll
+  for (int w = 1; w < kSmallThreads / 64; ++w) r = max(r, wave_max[w]);
+  const float s32 = tensor_scale_of(r);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *tensor_scale = s32;
+
+  const int64_t g = mine * kSmallThreads + threadIdx.x;
+  if (g >= nblocks) return;
+  const bool direct = s32 >= 0x1p-90f && s32 <= 0x1p120f;
+  float xs[16];
+  if (direct) {
+    to_fp8_domain<false>(k0, k1, 1.0f, s32, __fdiv_rn(1.0f, s32), xs);
+  } else {
+    const float xmul = s32 < 1.0f ? 0x1p64f : 0x1p-64f;
+    const float sx = s32 * xmul;
+    to_fp8_domain<true>(k0, k1, xmul, sx, __fdiv_rn(1.0f, sx), xs);
+  }
+  uint2 out;
+  uint32_t sb;
+  quantize_xs(xs, tab, out, sb);
+  *reinterpret_cast<uint2*>(codes + (g << 3)) = out;
+  scales[g] = (uint8_t)sb;
 }
 
 // Workgroups of kThreads that the device keeps resident at once for
@@ -420,6 +510,22 @@ hipError_t launch_tensor_scale(const uint16_t* x, int64_t rows, int64_t k, int64
   finalize_scale<<<1, 1, 0, stream>>>(p);
   return hipGetLastError();
 }
+
+hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                                 uint8_t* codes, uint8_t* scales, float* tensor_scale,
+                                 hipStream_t stream) {
+  const int64_t nbk = k / kBlock, nblocks = rows * nbk;
+  const int64_t g = (nblocks + kSmallThreads - 1) / kSmallThreads;   // one block per thread
+  if (ldx == k)
+    quantize_small_kernel<true><<<(unsigned)g, kSmallThreads, 0, stream>>>(
+        x, nbk, ldx, nblocks, codes, scales, tensor_scale);
+  else
+    quantize_small_kernel<false><<<(unsigned)g, kSmallThreads, 0, stream>>>(
+        x, nbk, ldx, nblocks, codes, scales, tensor_scale);
+  return hipGetLastError();
+}
+
+bool quantize_is_small(int64_t rows, int64_t k) { return rows * k <= kSmallElems; }
 
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
                            uint8_t* codes, uint8_t* scales, const float* tensor_scale,

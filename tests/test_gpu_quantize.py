@@ -85,6 +85,17 @@ def test_extreme_tensor_scales(exp, s32):
     _assert_same(bits, s32=given, label=f"2^{exp} data")
 
 
+@pytest.mark.parametrize("rows,k,pad", [(64, 4096, 0), (65, 4096, 0), (1, 1 << 18, 0),
+                                        (16, 8192, 0), (3, 48, 8), (100, 1024, 64)])
+def test_small_and_large_compute_paths(rows, k, pad):
+    """Tensors of at most 2^18 elements get their tensor scale and codes in one
+    launch (every workgroup reduces max|X| itself); larger ones take the
+    amax / reduce / quantize sequence.  Both sides of the threshold, strided
+    rows included, must give the oracle's bits."""
+    bits = W.adversarial(rows * 7 + k, rows, k)
+    _assert_same(bits, ldx_pad=pad, label=f"compute path {rows}x{k}")
+
+
 def test_empty_inputs():
     import paper_2605_31035_amd as M
     x = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
