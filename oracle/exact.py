@@ -69,8 +69,9 @@ def bf16_value(bits: int) -> Fraction:
     return -v if s else v
 
 
-def quantize_block(xb_bits, s32: Fraction):
+def quantize_block(xb_bits, s32: Fraction, mode: str = "select"):
     """Algorithm 1 on one 16-element block of bf16 bit patterns with a given s32.
+    ``mode`` "e2m1" / "e1m2" keeps that branch regardless of the errors.
     Returns (scale_byte, [nibbles], err_e2m1, err_e1m2)."""
     X = [bf16_value(int(b)) for b in xb_bits]
     x = [round_f32(v / s32) for v in X]                      # X_FP8 in fp32
@@ -91,6 +92,8 @@ def quantize_block(xb_bits, s32: Fraction):
         results[name] = (scode, codes, err)
     ef, ei = results["F"][2], results["I"][2]
     t = 0 if ef < ei else 1
+    if mode != "select":
+        t = 0 if mode == "e2m1" else 1
     scode, mags, _ = results["I" if t else "F"]
     nibs = [((int(b) >> 15) << 3) | c for b, c in zip(xb_bits, mags)]
     return (t << 7) | scode, nibs, ef, ei
@@ -103,9 +106,10 @@ def tensor_scale(x_bits) -> Fraction:
     return round_f32(amax / 2688)
 
 
-def quantize(x_bits_2d, s32=None):
-    """Brute-force Algorithm 1 on a small [rows, K] uint16 array.  Returns
-    (codes bytes [rows][K/2], scale bytes [rows][K/16], s32 Fraction)."""
+def quantize(x_bits_2d, s32=None, mode: str = "select"):
+    """Brute-force Algorithm 1 on a small [rows, K] uint16 array (``mode`` as
+    in ``quantize_block``).  Returns (codes bytes [rows][K/2], scale bytes
+    [rows][K/16], s32 Fraction)."""
     rows = [list(map(int, r)) for r in x_bits_2d]
     flat = [b for r in rows for b in r]
     s = tensor_scale(flat) if s32 is None else Fraction(s32)
@@ -113,7 +117,7 @@ def quantize(x_bits_2d, s32=None):
     for r in rows:
         crow, srow = [], []
         for j in range(0, len(r), 16):
-            sb, nibs, _, _ = quantize_block(r[j:j + 16], s)
+            sb, nibs, _, _ = quantize_block(r[j:j + 16], s, mode)
             srow.append(sb)
             crow.extend(nibs[i] | (nibs[i + 1] << 4) for i in range(0, 16, 2))
         codes.append(crow)

@@ -87,11 +87,20 @@ def _fraction_sum(row) -> Fraction:
     return sum((Fraction(float(t)) for t in row), Fraction(0))
 
 
-def quantize(x_bits: np.ndarray, s32=None) -> Quantized:
+MODES = ("select", "e2m1", "e1m2")
+
+
+def quantize(x_bits: np.ndarray, s32=None, mode: str = "select") -> Quantized:
     """Algorithm 1 on a bf16 tensor ``x_bits`` (uint16 [rows, K], K % 16 == 0).
 
     ``s32`` None computes the tensor scale (Algorithm 1); otherwise the given
-    fp32 value is used as s32."""
+    fp32 value is used as s32.  ``mode`` "select" is MixFP4 (the branch with
+    the smaller error, ties to E1M2).  "e2m1" and "e1m2" take one branch of
+    Algorithm 1 for every block, with everything else unchanged: the E2M1
+    branch alone is NVFP4 (Sec. 2.1: block scale E4M3(max/6), E2M1 codes) and
+    the E1M2 branch alone is the INT4-style format, with the same tensor-scale
+    rule; T still records the branch."""
+    assert mode in MODES
     x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
     rows, k = x_bits.shape
     assert k % BLOCK == 0
@@ -129,6 +138,8 @@ def quantize(x_bits: np.ndarray, s32=None) -> Quantized:
             delta[i] = 0.0 if exact == 0 else (1.0 if exact > 0 else -1.0) * max(abs(float(exact)), 5e-324)
     delta = delta.reshape(rows, nb)
     t = (~(delta < 0)).astype(np.uint8)                    # E2M1 iff Err_E2M1 < Err_E1M2
+    if mode != "select":
+        t = np.full_like(t, 0 if mode == "e2m1" else 1)
 
     mag = np.where(t[..., None] == 1, qi, qf).astype(np.uint8)
     sign = (x_bits.reshape(rows, nb, BLOCK) >> 15).astype(np.uint8)

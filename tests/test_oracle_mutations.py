@@ -125,3 +125,39 @@ def test_catches_inverted_selection(monkeypatch):
 def test_catches_wrong_tensor_divisor(monkeypatch):
     monkeypatch.setattr(Q, "TENSOR_DIVISOR", np.float32(2687.0))
     assert not _pins_pass()
+
+
+def _forced_pins_pass() -> bool:
+    """The forced-mode pins (tests/test_oracle_forced.py) as one predicate."""
+    from tests import test_oracle_forced as TF
+    try:
+        TF.test_e2m1_mode_is_nvfp4()
+        TF.test_e1m2_mode_is_int4()
+        TF.test_forced_matches_bruteforce("e2m1", 0, None)
+        TF.test_forced_matches_bruteforce("e1m2", 1, 0.37)
+    except AssertionError:
+        return False
+    return True
+
+
+def test_unmutated_forced_pins_pass():
+    assert _forced_pins_pass()
+
+
+def test_catches_forced_mode_ignored(monkeypatch):
+    orig = Q.quantize
+    monkeypatch.setattr(Q, "quantize", lambda x_bits, s32=None, mode="select": orig(x_bits, s32))
+    assert not _forced_pins_pass()
+
+
+def test_catches_forced_mode_wrong_scale(monkeypatch):
+    orig = Q.quantize
+
+    def mutated(x_bits, s32=None, mode="select"):
+        q = orig(x_bits, s32, mode)
+        if mode == "e1m2":      # E1M2 codes under the E2M1 branch's scale
+            q.scales[:] = (q.scales & 0x80) | q.sf_code
+        return q
+
+    monkeypatch.setattr(Q, "quantize", mutated)
+    assert not _forced_pins_pass()
