@@ -135,20 +135,21 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
     s32 = torch.empty(1, dtype=torch.float32, device=dev)
     M.mixfp4_quantize(xq, None, codes, scales, scale_out=s32)     # s32 for the given mode
 
-    def timed(given: bool) -> float:
+    def timed(given: bool, mode: str = "mixfp4") -> float:
         for _ in range(3):
-            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32)
+            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32, mode=mode)
         torch.cuda.synchronize()
         e = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)]
         e[0].record()
         for i in range(iters):
-            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32)
+            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32, mode=mode)
             e[i + 1].record()
         torch.cuda.synchronize()
         return float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(iters)]))
 
     ms_given = timed(True)
     ms_compute = timed(False)
+    ms_nvfp4 = timed(True, "e2m1")
     n = xq.numel()
     del xq, codes, scales
     torch.cuda.empty_cache()
@@ -164,6 +165,9 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
         "compute_mode_GBps": round(n * QUANT_BYTES_PER_ELEM / (ms_compute * 1e-3) / 1e9, 1),
         "compute_mode_note": "tensor scale computed on the device (amax pass + quantize); "
                              "GB/s counts the same 2.5625 B/element",
+        "e2m1_only_us": round(ms_nvfp4 * 1e3, 2),
+        "e2m1_only_GBps": round(n * QUANT_BYTES_PER_ELEM / (ms_nvfp4 * 1e-3) / 1e9, 1),
+        "e2m1_only_note": "the same kernel forced to the E2M1 branch (NVFP4 encoding), s32 given",
     }
 
 

@@ -48,6 +48,12 @@ typedef enum {
 /* Tensor-scale modes of mixfp4_quantize (flags argument). */
 #define MIXFP4_SCALE_COMPUTE 0u /* compute s32 = max|X| / 2688 on the device  */
 #define MIXFP4_SCALE_GIVEN 1u   /* read s32 from *tensor_scale                */
+/* Format modes (OR-ed with one of the above; at most one of them).  Each
+ * takes one branch of Algorithm 1 for every block, with the tensor scale,
+ * rounding and packing unchanged, and sets T accordingly, so dequantize and
+ * GEMM read the result like any MixFP4 tensor:                             */
+#define MIXFP4_FORCE_E2M1 2u    /* E2M1 only (T = 0): NVFP4 (Sec. 2.1)        */
+#define MIXFP4_FORCE_E1M2 4u    /* E1M2 x2 only (T = 1): INT4 codes           */
 
 /*
  * mixfp4_quantize - Algorithm 1 ("MixFP4 data type quantization") on a bf16
@@ -72,7 +78,9 @@ typedef enum {
  *   tensor_scale 1 float, 4-byte aligned.  COMPUTE: written with
  *                fl32(max|X| / 2688), or 1.0f if X is all zero (Algorithm 1).
  *                GIVEN: read; must be finite and > 0.
- *   flags        MIXFP4_SCALE_COMPUTE or MIXFP4_SCALE_GIVEN.
+ *   flags        MIXFP4_SCALE_COMPUTE or MIXFP4_SCALE_GIVEN, optionally OR-ed
+ *                with one of MIXFP4_FORCE_E2M1 / MIXFP4_FORCE_E1M2; any other
+ *                bit, or both FORCE bits, returns MIXFP4_ERR_FLAGS.
  */
 int mixfp4_quantize(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
                     uint8_t *codes, uint8_t *scales, float *tensor_scale,
@@ -123,7 +131,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 100
+#define MIXFP4_ABI_VERSION 101
 
 #ifdef __cplusplus
 }

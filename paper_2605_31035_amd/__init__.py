@@ -6,7 +6,7 @@ the library's HIP kernels.  There is no CPU fallback: if the library is
 missing or fails to load, importing the low-level handle raises.
 
 Functions (same names as the C ABI in include/mixfp4.h):
-  mixfp4_quantize(x, tensor_scale=None, out=None) -> (codes, scales, s32)
+  mixfp4_quantize(x, tensor_scale=None, ..., mode="mixfp4") -> (codes, scales, s32)
   mixfp4_dequantize(codes, scales, tensor_scale=None) -> fp32 tensor
   mixfp4_gemm(a, w) -> C = A W^T (fp32), a/w are (codes, scales, s32) triples
 """
@@ -20,10 +20,13 @@ import torch
 from ._lib import LIB_PATH, MixFP4Error, lib
 
 __all__ = ["mixfp4_quantize", "mixfp4_dequantize", "mixfp4_gemm", "MixFP4Error",
-           "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN"]
+           "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN", "FORCE_E2M1", "FORCE_E1M2"]
 
 SCALE_COMPUTE = 0
 SCALE_GIVEN = 1
+FORCE_E2M1 = 2
+FORCE_E1M2 = 4
+_MODES = {"mixfp4": 0, "e2m1": FORCE_E2M1, "e1m2": FORCE_E1M2}
 
 
 def _stream(device) -> ctypes.c_void_p:
@@ -44,12 +47,16 @@ def _check(status: int):
 
 def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
                     codes: torch.Tensor | None = None, scales: torch.Tensor | None = None,
-                    scale_out: torch.Tensor | None = None):
+                    scale_out: torch.Tensor | None = None, mode: str = "mixfp4"):
     """Quantize a bf16 [rows, k] CUDA tensor (Algorithm 1).
 
     ``tensor_scale`` None computes s32 = max|X| / 2688 on the device (into
     ``scale_out`` if given); a 1-element fp32 tensor is used as the given s32.
+    ``mode`` "mixfp4" selects the format per block; "e2m1" (NVFP4) and "e1m2"
+    (INT4) take that branch for every block.
     Returns (codes uint8 [rows, k/2], scales uint8 [rows, k/16], s32 fp32 [1])."""
+    if mode not in _MODES:
+        raise ValueError(f"mode must be one of {sorted(_MODES)}")
     if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_cuda:
         raise ValueError("x must be a 2-D bfloat16 CUDA tensor")
     if x.stride(1) != 1:
@@ -67,7 +74,7 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
         ts = tensor_scale
         flags = SCALE_GIVEN
     st = lib.mixfp4_quantize(_ptr(x), rows, k, x.stride(0) if rows > 0 else k, _ptr(codes),
-                             _ptr(scales), _ptr(ts), flags, _stream(dev))
+                             _ptr(scales), _ptr(ts), flags | _MODES[mode], _stream(dev))
     _check(st)
     return codes, scales, ts
 

@@ -31,7 +31,7 @@ const char* mixfp4_status_string(int status) {
     case MIXFP4_ERR_NULL: return "MIXFP4_ERR_NULL: a required pointer is NULL";
     case MIXFP4_ERR_SHAPE: return "MIXFP4_ERR_SHAPE: bad size (negative, K % 16 != 0, ldx < K or ldx % 8 != 0)";
     case MIXFP4_ERR_ALIGN: return "MIXFP4_ERR_ALIGN: pointer misaligned";
-    case MIXFP4_ERR_FLAGS: return "MIXFP4_ERR_FLAGS: unknown flags";
+    case MIXFP4_ERR_FLAGS: return "MIXFP4_ERR_FLAGS: unknown flag bits or both FORCE flags";
     case MIXFP4_ERR_LAUNCH: return "MIXFP4_ERR_LAUNCH: kernel launch failed";
     default: return "unknown mixfp4 status";
   }
@@ -41,7 +41,11 @@ const char* mixfp4_last_launch_error(void) { return g_last_launch_error; }
 
 int mixfp4_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
                     uint8_t* scales, float* tensor_scale, unsigned flags, void* stream) {
-  if (flags != MIXFP4_SCALE_COMPUTE && flags != MIXFP4_SCALE_GIVEN) return MIXFP4_ERR_FLAGS;
+  if ((flags & ~(MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) != 0u ||
+      (flags & (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) == (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2))
+    return MIXFP4_ERR_FLAGS;
+  const bool given = (flags & MIXFP4_SCALE_GIVEN) != 0u;
+  const int mode = (flags & MIXFP4_FORCE_E2M1) ? 1 : (flags & MIXFP4_FORCE_E1M2) ? 2 : 0;
   if (rows < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;
   if (rows > 0 && (ldx < k || (ldx % 8) != 0)) return MIXFP4_ERR_SHAPE;
   if (!tensor_scale) return MIXFP4_ERR_NULL;
@@ -51,17 +55,18 @@ int mixfp4_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uin
   if (!empty && (!aligned(x, 16) || !aligned(codes, 16))) return MIXFP4_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();   // drop stale errors so a launch failure is ours
-  if (flags == MIXFP4_SCALE_COMPUTE && !empty && mixfp4::quantize_is_small(rows, k))
+  if (!given && !empty && mixfp4::quantize_is_small(rows, k))
     return launch_status(mixfp4::launch_quantize_small(x, rows, k, ldx, codes, scales,
-                                                       tensor_scale, s));
-  if (flags == MIXFP4_SCALE_COMPUTE) {
+                                                       tensor_scale, mode, s));
+  if (!given) {
     const int st = launch_status(mixfp4::launch_tensor_scale(
         x, empty ? 0 : rows, k, ldx, empty ? nullptr : scales,
         empty ? 0 : rows * (k / mixfp4::kBlock), tensor_scale, s));
     if (st != MIXFP4_OK) return st;
   }
   if (empty) return MIXFP4_OK;
-  return launch_status(mixfp4::launch_quantize(x, rows, k, ldx, codes, scales, tensor_scale, s));
+  return launch_status(
+      mixfp4::launch_quantize(x, rows, k, ldx, codes, scales, tensor_scale, mode, s));
 }
 
 int mixfp4_dequantize(const uint8_t* codes, const uint8_t* scales, const float* tensor_scale,

@@ -16,15 +16,16 @@ constexpr int kBlock = 16;
 hipError_t launch_tensor_scale(const uint16_t* x, int64_t rows, int64_t k,
                                int64_t ldx, uint8_t* scratch, int64_t scratch_bytes,
                                float* tensor_scale, hipStream_t stream);
+// `mode`: 0 MixFP4 selection, 1 E2M1 only (NVFP4), 2 E1M2 only (INT4).
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k,
                            int64_t ldx, uint8_t* codes, uint8_t* scales,
-                           const float* tensor_scale, hipStream_t stream);
+                           const float* tensor_scale, int mode, hipStream_t stream);
 // Tensor scale and quantization in one launch, for tensors with
 // quantize_is_small(rows, k) (rows * k at most 2^18); rows, k > 0.
 bool quantize_is_small(int64_t rows, int64_t k);
 hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k,
                                  int64_t ldx, uint8_t* codes, uint8_t* scales,
-                                 float* tensor_scale, hipStream_t stream);
+                                 float* tensor_scale, int mode, hipStream_t stream);
 hipError_t launch_dequantize(const uint8_t* codes, const uint8_t* scales,
                              const float* tensor_scale, int64_t rows,
                              int64_t k, float* out, hipStream_t stream);

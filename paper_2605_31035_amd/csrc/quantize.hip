@@ -146,26 +146,31 @@ __device__ __forceinline__ void to_fp8_domain(uint4 v0, uint4 v1, float xmul, fl
   }
 }
 
-// Elements J, J+1 (J even) of a block:
-//   E2M1: y = fl32(x / s_F) rounded by the gfx950 FP4 converter (scale 1:
-//   nearest, ties to the even code, saturating at 6, sign kept) into nibble
-//   pair (J%8)/2 of pf[J/8];
-//   E1M2 (x2 = INT4): y = fl32(|x| / s_I); adding 2^23 rounds it to an
-//   integer (ties to even) held in the low mantissa bits, accumulated into
-//   pi[J/8] at nibble J%8 together with a constant removed afterwards;
-//   ai[J/2 % 2] += |x| * q_I.
+// Elements J, J+1 (J even) of a block, E2M1 branch: y = fl32(x / s_F)
+// rounded by the gfx950 FP4 converter (scale 1: nearest, ties to the even
+// code, saturating at 6, sign kept) into nibble pair (J%8)/2 of pf[J/8].
 template <int J>
-__device__ __forceinline__ void encode_pair(const float (&xs)[16], float sf, float rf, float si,
-                                            float ri, uint32_t (&pf)[2], uint32_t (&pi)[2],
-                                            float (&ai)[2]) {
+__device__ __forceinline__ void encode_f_pair(const float (&xs)[16], float sf, float rf,
+                                              uint32_t (&pf)[2]) {
   const float yf0 = div_rn(xs[J], sf, rf), yf1 = div_rn(xs[J + 1], sf, rf);
   pf[J >> 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(pf[J >> 3], yf0, yf1, 1.0f, (J & 7) >> 1);
+}
+
+// Elements J, J+1 (J even), E1M2 (x2 = INT4) branch: y = fl32(|x| / s_I);
+// adding 2^23 rounds it to an integer (ties to even) held in the low mantissa
+// bits, accumulated into pi[J/8] at nibble J%8 together with a constant
+// removed afterwards.  With kErr, ai[J/2 % 2] += |x| * q_I.
+template <int J, bool kErr>
+__device__ __forceinline__ void encode_i_pair(const float (&xs)[16], float si, float ri,
+                                              uint32_t (&pi)[2], float (&ai)[2]) {
   const float a0 = fabsf(xs[J]), a1 = fabsf(xs[J + 1]);
   const uint32_t b0 = __float_as_uint(div_rn(a0, si, ri) + 0x1p23f);
   const uint32_t b1 = __float_as_uint(div_rn(a1, si, ri) + 0x1p23f);
-  float& acc = ai[(J >> 1) & 1];
-  acc = __builtin_fmaf(a0, __uint_as_float(b0) - 0x1p23f, acc);
-  acc = __builtin_fmaf(a1, __uint_as_float(b1) - 0x1p23f, acc);
+  if (kErr) {
+    float& acc = ai[(J >> 1) & 1];
+    acc = __builtin_fmaf(a0, __uint_as_float(b0) - 0x1p23f, acc);
+    acc = __builtin_fmaf(a1, __uint_as_float(b1) - 0x1p23f, acc);
+  }
   pi[J >> 3] += b0 << (4 * (J & 7));
   pi[J >> 3] += b1 << (4 * ((J + 1) & 7));
 }
@@ -202,8 +207,28 @@ __device__ __forceinline__ void exact_pair(const float (&xs)[16], const uint32_t
   }
 }
 
+// Format modes: MixFP4 selection (Algorithm 1), or one branch for every
+// block (E2M1 = NVFP4, E1M2 = INT4); T records the branch either way.
+constexpr int kSelect = 0, kForceE2M1 = 1, kForceE1M2 = 2;
+
+// E1M2 codes of the 16 elements with saturation at 7 (a subnormal or
+// saturated s_I admits codes above 7; rare path): codes into pi, with kErr
+// also sum |x| q_I into ai.
+template <bool kErr>
+__device__ __forceinline__ void encode_i_saturated(const float (&xs)[16], float si, float ri,
+                                                   uint32_t (&pi)[2], float (&ai)[2]) {
+  pi[0] = pi[1] = 0u;
+  ai[0] = ai[1] = 0.0f;
+  for (int j = 0; j < 16; ++j) {
+    const float q = fminf(rintf(div_rn(fabsf(xs[j]), si, ri)), 7.0f);
+    if (kErr) ai[j & 1] = __builtin_fmaf(fabsf(xs[j]), q, ai[j & 1]);
+    pi[j >> 3] |= (uint32_t)q << (4 * (j & 7));
+  }
+}
+
 // Codes and scale byte of one block from x (Algorithm 1 after the tensor
 // scale).
+template <int kMode>
 __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2* __restrict__ tab,
                                             uint2& out, uint32_t& scale_byte) {
   // fl32 rounding is monotonic, so bm is also fl32(max|X| / s32).
@@ -215,9 +240,9 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
   // converter (scale 1: nearest, ties to the even code; checked against the
   // software rounding on every fp32 value in [0, 448]).
   constexpr float kR6 = 1.0f / 6.0f, kR7 = 1.0f / 7.0f;
-  const s16x2 sc = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(
-      s16x2{0, 0}, fminf(div_rn(bm, 6.0f, kR6), 448.0f), fminf(div_rn(bm, 7.0f, kR7), 448.0f),
-      1.0f, false);
+  const float cand6 = kMode == kForceE1M2 ? 0.0f : fminf(div_rn(bm, 6.0f, kR6), 448.0f);
+  const float cand7 = kMode == kForceE2M1 ? 0.0f : fminf(div_rn(bm, 7.0f, kR7), 448.0f);
+  const s16x2 sc = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(s16x2{0, 0}, cand6, cand7, 1.0f, false);
   const uint32_t scw = __builtin_bit_cast(uint32_t, sc);
   const uint32_t cf = scw & 0x7Fu, ci = (scw >> 8) & 0x7Fu;
   const float2 ef = tab[cf], ei = tab[ci];
@@ -225,16 +250,45 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
 
   uint32_t pf[2] = {0u, 0u}, pi[2] = {0u, 0u};
   float af[2] = {0.0f, 0.0f}, bf[2] = {0.0f, 0.0f}, ai[2] = {0.0f, 0.0f};
-  encode_pair<0>(xs, sf, rf, si, ri, pf, pi, ai);
-  encode_pair<2>(xs, sf, rf, si, ri, pf, pi, ai);
-  encode_pair<4>(xs, sf, rf, si, ri, pf, pi, ai);
-  encode_pair<6>(xs, sf, rf, si, ri, pf, pi, ai);
-  encode_pair<8>(xs, sf, rf, si, ri, pf, pi, ai);
-  encode_pair<10>(xs, sf, rf, si, ri, pf, pi, ai);
-  encode_pair<12>(xs, sf, rf, si, ri, pf, pi, ai);
-  encode_pair<14>(xs, sf, rf, si, ri, pf, pi, ai);
+  if constexpr (kMode != kForceE1M2) {
+    encode_f_pair<0>(xs, sf, rf, pf);
+    encode_f_pair<2>(xs, sf, rf, pf);
+    encode_f_pair<4>(xs, sf, rf, pf);
+    encode_f_pair<6>(xs, sf, rf, pf);
+    encode_f_pair<8>(xs, sf, rf, pf);
+    encode_f_pair<10>(xs, sf, rf, pf);
+    encode_f_pair<12>(xs, sf, rf, pf);
+    encode_f_pair<14>(xs, sf, rf, pf);
+  }
+  if constexpr (kMode == kForceE2M1) {
+    out = make_uint2(pf[0], pf[1]);
+    scale_byte = cf;
+    return;
+  }
+  constexpr bool kErr = kMode == kSelect;
+  encode_i_pair<0, kErr>(xs, si, ri, pi, ai);
+  encode_i_pair<2, kErr>(xs, si, ri, pi, ai);
+  encode_i_pair<4, kErr>(xs, si, ri, pi, ai);
+  encode_i_pair<6, kErr>(xs, si, ri, pi, ai);
+  encode_i_pair<8, kErr>(xs, si, ri, pi, ai);
+  encode_i_pair<10, kErr>(xs, si, ri, pi, ai);
+  encode_i_pair<12, kErr>(xs, si, ri, pi, ai);
+  encode_i_pair<14, kErr>(xs, si, ri, pi, ai);
   pi[0] -= kMagicPack;
   pi[1] -= kMagicPack;
+  // INT4 codes cannot exceed 7 when s_I is a normal E4M3 value below the
+  // maximum (then max|x| / s_I < 7.47); other blocks redo the branch with
+  // saturation (rare path).
+  if (ci < 8u || ci >= 0x7Eu) encode_i_saturated<kErr>(xs, si, ri, pi, ai);
+  if constexpr (kMode == kForceE1M2) {
+    // sign of X into bit 3 of every nibble
+    uint32_t sg[2] = {0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 16; ++j) sg[j >> 3] |= (__float_as_uint(xs[j]) >> 31) << (4 * (j & 7) + 3);
+    out = make_uint2(pi[0] | sg[0], pi[1] | sg[1]);
+    scale_byte = 0x80u | ci;
+    return;
+  }
   error_pair<0>(xs, pf, af, bf);
   error_pair<2>(xs, pf, af, bf);
   error_pair<4>(xs, pf, af, bf);
@@ -243,21 +297,8 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
   error_pair<10>(xs, pf, af, bf);
   error_pair<12>(xs, pf, af, bf);
   error_pair<14>(xs, pf, af, bf);
-  // INT4 codes cannot exceed 7 when s_I is a normal E4M3 value below the
-  // maximum (then max|x| / s_I < 7.47); other blocks redo the branch with
-  // saturation (rare path).
-  if (ci < 8u || ci >= 0x7Eu) {
-    pi[0] = pi[1] = 0u;
-    ai[0] = ai[1] = 0.0f;
-    for (int j = 0; j < 16; ++j) {
-      const float q = fminf(rintf(div_rn(fabsf(xs[j]), si, ri)), 7.0f);
-      ai[j & 1] = __builtin_fmaf(fabsf(xs[j]), q, ai[j & 1]);
-      pi[j >> 3] |= (uint32_t)q << (4 * (j & 7));
-    }
-  }
   const uint32_t bi = __builtin_amdgcn_udot8(pi[0], pi[0], __builtin_amdgcn_udot8(pi[1], pi[1], 0u, false),
                                              false);
-
   // Err_F - Err_I with Err_T = sum x^2 - 2 s_T sum |x| q_T + s_T^2 sum q_T^2
   // (the sum of x^2 cancels):  est = (sf^2 bf - si^2 bi) + 2 (si ai - sf af).
   // bf and bi are exact (multiples of 1/4, integers) and so are sf^2 bf and
@@ -299,7 +340,7 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
 // loaded as soon as the current one has been turned into x, so its load
 // overlaps this block's arithmetic (measured: a second block in flight, or
 // more waves per SIMD, gains nothing; the kernel is bound by VALU issue).
-template <bool kContig, bool kScaled>
+template <bool kContig, bool kScaled, int kMode>
 __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, int64_t nbk,
                                               int64_t ldx, int64_t nblocks,
                                               uint8_t* __restrict__ codes,
@@ -330,7 +371,7 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
     load(g + stride, a0, a1);
     uint2 out;
     uint32_t sb;
-    quantize_xs(xs, tab, out, sb);
+    quantize_xs<kMode>(xs, tab, out, sb);
     *reinterpret_cast<uint2*>(codes + (g << 3)) = out;
     scales[g] = (uint8_t)sb;
   }
@@ -351,24 +392,24 @@ __device__ __forceinline__ void fill_scale_table(float2* tab) {
 // The division steps stay in the normal range for every element that can get
 // a nonzero code when 2^-90 <= s32 <= 2^120; beyond that both X and s32 are
 // rescaled by 2^64 or 2^-64 first.
-template <bool kContig>
+template <bool kContig, int kMode>
 __device__ __forceinline__ void quantize_all(const uint16_t* __restrict__ x, int64_t nbk,
                                              int64_t ldx, int64_t nblocks,
                                              uint8_t* __restrict__ codes,
                                              uint8_t* __restrict__ scales, float s32,
                                              const float2* tab) {
   if (s32 >= 0x1p-90f && s32 <= 0x1p120f) {
-    quantize_loop<kContig, false>(x, nbk, ldx, nblocks, codes, scales, 1.0f, s32,
+    quantize_loop<kContig, false, kMode>(x, nbk, ldx, nblocks, codes, scales, 1.0f, s32,
                                   __fdiv_rn(1.0f, s32), tab);
   } else {
     const float xmul = s32 < 1.0f ? 0x1p64f : 0x1p-64f;
     const float sx = s32 * xmul;
-    quantize_loop<kContig, true>(x, nbk, ldx, nblocks, codes, scales, xmul, sx,
+    quantize_loop<kContig, true, kMode>(x, nbk, ldx, nblocks, codes, scales, xmul, sx,
                                  __fdiv_rn(1.0f, sx), tab);
   }
 }
 
-template <bool kContig>
+template <bool kContig, int kMode>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
@@ -376,7 +417,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
   __shared__ float2 tab[128];
   fill_scale_table(tab);
   __syncthreads();
-  quantize_all<kContig>(x, nbk, ldx, nblocks, codes, scales, *tensor_scale, tab);
+  quantize_all<kContig, kMode>(x, nbk, ldx, nblocks, codes, scales, *tensor_scale, tab);
 }
 
 // Small tensors with the tensor scale computed (at most kSmallElems
@@ -391,7 +432,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
 constexpr int kSmallThreads = 1024;
 constexpr int64_t kSmallElems = int64_t(1) << 18;
 
-template <bool kContig>
+template <bool kContig, int kMode>
 __global__ __launch_bounds__(kSmallThreads) void quantize_small_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, float* __restrict__ tensor_scale) {
@@ -450,21 +491,22 @@ __global__ __launch_bounds__(kSmallThreads) void quantize_small_kernel(
   }
   uint2 out;
   uint32_t sb;
-  quantize_xs(xs, tab, out, sb);
+  quantize_xs<kMode>(xs, tab, out, sb);
   *reinterpret_cast<uint2*>(codes + (g << 3)) = out;
   scales[g] = (uint8_t)sb;
 }
 
 // Workgroups of kThreads that the device keeps resident at once for
-// quantize_kernel<kContig> (occupancy per CU x CU count), cached per device.
-template <bool kContig>
+// quantize_kernel<kContig, kMode> (occupancy per CU x CU count), cached per
+// device.
+template <bool kContig, int kMode>
 int64_t resident_groups() {
   static int64_t cached[64] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
   if (!cached[dev]) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, quantize_kernel<kContig>, kThreads,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, quantize_kernel<kContig, kMode>, kThreads,
                                                      0) != hipSuccess ||
         per_cu <= 0)
       per_cu = 4;
@@ -511,40 +553,65 @@ hipError_t launch_tensor_scale(const uint16_t* x, int64_t rows, int64_t k, int64
   return hipGetLastError();
 }
 
-hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
-                                 uint8_t* codes, uint8_t* scales, float* tensor_scale,
-                                 hipStream_t stream) {
+namespace {
+
+template <int kMode>
+hipError_t launch_small_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                             uint8_t* codes, uint8_t* scales, float* tensor_scale,
+                             hipStream_t stream) {
   const int64_t nbk = k / kBlock, nblocks = rows * nbk;
   const int64_t g = (nblocks + kSmallThreads - 1) / kSmallThreads;   // one block per thread
   if (ldx == k)
-    quantize_small_kernel<true><<<(unsigned)g, kSmallThreads, 0, stream>>>(
+    quantize_small_kernel<true, kMode><<<(unsigned)g, kSmallThreads, 0, stream>>>(
         x, nbk, ldx, nblocks, codes, scales, tensor_scale);
   else
-    quantize_small_kernel<false><<<(unsigned)g, kSmallThreads, 0, stream>>>(
+    quantize_small_kernel<false, kMode><<<(unsigned)g, kSmallThreads, 0, stream>>>(
         x, nbk, ldx, nblocks, codes, scales, tensor_scale);
   return hipGetLastError();
+}
+
+template <int kMode>
+hipError_t launch_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
+                       uint8_t* scales, const float* tensor_scale, hipStream_t stream) {
+  const int64_t nbk = k / kBlock;
+  const int64_t nblocks = rows * nbk;
+  // One wave of resident workgroups (occupancy x CUs) walks all blocks, so
+  // no partial second wave is left at the end; fewer if the tensor is small.
+  const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
+  const int64_t resident = ldx == k ? resident_groups<true, kMode>() : resident_groups<false, kMode>();
+  const int g = (int)(wanted < resident ? wanted : resident);
+  if (ldx == k)
+    quantize_kernel<true, kMode><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, codes, scales,
+                                                              tensor_scale);
+  else
+    quantize_kernel<false, kMode><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, codes,
+                                                               scales, tensor_scale);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                                 uint8_t* codes, uint8_t* scales, float* tensor_scale, int mode,
+                                 hipStream_t stream) {
+  if (mode == kForceE2M1)
+    return launch_small_mode<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
+  if (mode == kForceE1M2)
+    return launch_small_mode<kForceE1M2>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
+  return launch_small_mode<kSelect>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
 }
 
 bool quantize_is_small(int64_t rows, int64_t k) { return rows * k <= kSmallElems; }
 
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
-                           uint8_t* codes, uint8_t* scales, const float* tensor_scale,
+                           uint8_t* codes, uint8_t* scales, const float* tensor_scale, int mode,
                            hipStream_t stream) {
-  const int64_t nbk = k / kBlock;
-  const int64_t nblocks = rows * nbk;
-  if (nblocks == 0) return hipSuccess;
-  // One wave of resident workgroups (occupancy x CUs) walks all blocks, so
-  // no partial second wave is left at the end; fewer if the tensor is small.
-  const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
-  const int64_t resident = ldx == k ? resident_groups<true>() : resident_groups<false>();
-  const int g = (int)(wanted < resident ? wanted : resident);
-  if (ldx == k)
-    quantize_kernel<true><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, codes, scales,
-                                                       tensor_scale);
-  else
-    quantize_kernel<false><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, codes, scales,
-                                                        tensor_scale);
-  return hipGetLastError();
+  if (rows * (k / kBlock) == 0) return hipSuccess;
+  if (mode == kForceE2M1)
+    return launch_mode<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
+  if (mode == kForceE1M2)
+    return launch_mode<kForceE1M2>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
+  return launch_mode<kSelect>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
 }
 
 }  // namespace mixfp4

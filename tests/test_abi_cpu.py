@@ -53,7 +53,10 @@ def q(lib, x=A16, rows=4, k=32, ldx=32, codes=A16, scales=A16, ts=A16, flags=0):
 
 
 def test_quantize_rejects(lib):
-    assert q(lib, flags=7) == 4
+    assert q(lib, flags=7) == 4          # both FORCE bits (with GIVEN)
+    assert q(lib, flags=6) == 4          # both FORCE bits
+    assert q(lib, flags=8) == 4          # unknown bit
+    assert q(lib, flags=0x80000002) == 4
     assert q(lib, k=24) == 2
     assert q(lib, k=-16) == 2
     assert q(lib, rows=-1) == 2

@@ -8,7 +8,7 @@ import workloads as W
 from oracle import gemm as G
 from oracle import quant as Q
 from tests._golden import handworked_gemm
-from tests._gpu import dev_f32, dev_u8, gpu_quantize, host, log
+from tests._gpu import dev_bf16, dev_f32, dev_u8, gpu_quantize, host, log
 
 pytestmark = pytest.mark.gpu
 
@@ -105,6 +105,25 @@ def test_mid_size_ragged(m, n, k):
     qa, qw = Q.quantize(a), Q.quantize(w)
     log(f"gemm mid size m={m} n={n} k={k}")
     _check(_gemm_dev(qa, qw), qa, qw)
+
+
+def test_forced_format_operands():
+    """A quantized E2M1-only (NVFP4) and W E1M2-only (INT4) on the GPU: the
+    GEMM decodes them through T like any MixFP4 operand."""
+    import paper_2605_31035_amd as M
+    a = W.adversarial(71, 300, 512)
+    w = W.adversarial(72, 200, 512)
+    qa = Q.quantize(a, mode="e2m1")
+    qw = Q.quantize(w, mode="e1m2")
+    log("gemm forced-format operands 300x200x512")
+    ga = M.mixfp4_quantize(dev_bf16(a), mode="e2m1")
+    gw = M.mixfp4_quantize(dev_bf16(w), mode="e1m2")
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(ga[0]), qa.codes)
+    np.testing.assert_array_equal(host(gw[1]), qw.scales)
+    c = M.mixfp4_gemm(ga, gw)
+    torch.cuda.synchronize()
+    _check(host(c), qa, qw)
 
 
 def test_k_zero_writes_zeros():

@@ -7,7 +7,7 @@ import torch
 import workloads as W
 from oracle import quant as Q
 from tests._golden import handworked_blocks
-from tests._gpu import dev_f32, dev_u8, gpu_quantize, host, log
+from tests._gpu import dev_bf16, dev_f32, dev_u8, gpu_quantize, host, log
 
 pytestmark = pytest.mark.gpu
 
@@ -94,6 +94,26 @@ def test_small_and_large_compute_paths(rows, k, pad):
     rows included, must give the oracle's bits."""
     bits = W.adversarial(rows * 7 + k, rows, k)
     _assert_same(bits, ldx_pad=pad, label=f"compute path {rows}x{k}")
+
+
+@pytest.mark.parametrize("mode", ["e2m1", "e1m2"])
+@pytest.mark.parametrize("rows,k,s32", [(3, 48, None), (64, 4096, None), (65, 4096, None),
+                                        (257, 80, 0.37), (1000, 272, None)])
+def test_forced_format_modes(mode, rows, k, s32):
+    """E2M1-only (NVFP4) and E1M2-only (INT4) modes, small one-launch and
+    large paths, computed and given tensor scales: the oracle's bits."""
+    import paper_2605_31035_amd as M
+    bits = W.adversarial(rows + 3 * k, rows, k)
+    given = None if s32 is None else np.float32(s32)
+    log(f"quantize forced {mode} {rows}x{k} s32={given}")
+    x = dev_bf16(bits)
+    ts = None if given is None else dev_f32(given)
+    codes, scales, s = M.mixfp4_quantize(x, ts, mode=mode)
+    torch.cuda.synchronize()
+    ref = Q.quantize(bits, s32=given, mode=mode)
+    assert host(s)[0] == ref.s32
+    np.testing.assert_array_equal(host(scales), ref.scales)
+    np.testing.assert_array_equal(host(codes), ref.codes)
 
 
 def test_empty_inputs():
