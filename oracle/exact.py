@@ -69,9 +69,31 @@ def bf16_value(bits: int) -> Fraction:
     return -v if s else v
 
 
-def quantize_block(xb_bits, s32: Fraction, mode: str = "select"):
+def stochastic(y: Fraction, book, u: int) -> int:
+    """App. D's stochastic rounding of y >= 0 between its two neighbours in
+    ``book``: v = y + (eps - 1/2) * spacing with eps = (u + 1/2) / 256, then
+    the nearer neighbour (ties to the even code); at or above the largest
+    entry, the largest (App. D's clamp)."""
+    top = max(book, key=lambda cv: cv[1])
+    if y >= top[1]:
+        return top[0]
+    lo = max((cv for cv in book if cv[1] <= y), key=lambda cv: cv[1])
+    hi = min((cv for cv in book if cv[1] > y), key=lambda cv: cv[1])
+    eps = Fraction(2 * u + 1, 512)
+    v = y + (eps - Fraction(1, 2)) * (hi[1] - lo[1])
+    dlo, dhi = abs(v - lo[1]), abs(hi[1] - v)
+    if dhi < dlo or (dhi == dlo and hi[0] % 2 == 0):
+        return hi[0]
+    return lo[0]
+
+
+def quantize_block(xb_bits, s32: Fraction, mode: str = "select", draws=None):
     """Algorithm 1 on one 16-element block of bf16 bit patterns with a given s32.
     ``mode`` "e2m1" / "e1m2" keeps that branch regardless of the errors.
+    ``draws`` (16 integers in [0, 256)) switches the chosen branch's codes to
+    stochastic rounding of the fp32 quotient fl32(|x| / s8), with draw 255 - u
+    for an element whose sign bit is set (App. D's signed rule); scales and
+    the format choice stay those of round-to-nearest.
     Returns (scale_byte, [nibbles], err_e2m1, err_e1m2)."""
     X = [bf16_value(int(b)) for b in xb_bits]
     x = [round_f32(v / s32) for v in X]                      # X_FP8 in fp32
@@ -95,6 +117,13 @@ def quantize_block(xb_bits, s32: Fraction, mode: str = "select"):
     if mode != "select":
         t = 0 if mode == "e2m1" else 1
     scode, mags, _ = results["I" if t else "F"]
+    if draws is not None:
+        book = E1M2X2 if t else E2M1
+        s8 = E4M3[scode][1]
+        mags = []
+        for b, v, u in zip(xb_bits, x, draws):
+            y = round_f32(abs(v) / s8) if s8 != 0 else Fraction(0)
+            mags.append(stochastic(y, book, 255 - int(u) if int(b) >> 15 else int(u)))
     nibs = [((int(b) >> 15) << 3) | c for b, c in zip(xb_bits, mags)]
     return (t << 7) | scode, nibs, ef, ei
 
@@ -106,18 +135,20 @@ def tensor_scale(x_bits) -> Fraction:
     return round_f32(amax / 2688)
 
 
-def quantize(x_bits_2d, s32=None, mode: str = "select"):
+def quantize(x_bits_2d, s32=None, mode: str = "select", draws=None):
     """Brute-force Algorithm 1 on a small [rows, K] uint16 array (``mode`` as
-    in ``quantize_block``).  Returns (codes bytes [rows][K/2], scale bytes
+    in ``quantize_block``; ``draws`` None, or [rows, K] integers in [0, 256)
+    for stochastic rounding).  Returns (codes bytes [rows][K/2], scale bytes
     [rows][K/16], s32 Fraction)."""
     rows = [list(map(int, r)) for r in x_bits_2d]
     flat = [b for r in rows for b in r]
     s = tensor_scale(flat) if s32 is None else Fraction(s32)
     codes, scales = [], []
-    for r in rows:
+    for ri, r in enumerate(rows):
         crow, srow = [], []
         for j in range(0, len(r), 16):
-            sb, nibs, _, _ = quantize_block(r[j:j + 16], s, mode)
+            dr = None if draws is None else [int(v) for v in draws[ri][j:j + 16]]
+            sb, nibs, _, _ = quantize_block(r[j:j + 16], s, mode, dr)
             srow.append(sb)
             crow.extend(nibs[i] | (nibs[i + 1] << 4) for i in range(0, 16, 2))
         codes.append(crow)

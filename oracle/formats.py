@@ -99,3 +99,33 @@ def e4m3_encode(v: np.ndarray) -> np.ndarray:
 def e4m3_decode(code: np.ndarray) -> np.ndarray:
     """Value of a 7-bit E4M3 magnitude code (App. B.3 forces bit 7 to zero)."""
     return E4M3_VALUES[np.asarray(code, dtype=np.int64) & 0x7F]
+
+
+def stochastic_round_to_codebook(y: np.ndarray, values: np.ndarray, u: np.ndarray) -> np.ndarray:
+    """Stochastic rounding (App. D) of magnitudes y >= 0 onto ``values``
+    (ascending, index = code) with draws u in [0, 256).
+
+    App. D rounds the integer grid as round(q + eps - 1/2) with eps uniform on
+    (0, 1), so q lands on one of its two neighbours with probability falling
+    linearly with the distance.  Here, for y between neighbours lo <= y < hi
+    (spacing d = hi - lo), that rule is applied on the local lattice:
+    y + (eps - 1/2) d rounded to the nearer of lo and hi, ties to the even
+    code, with eps = (u + 1/2) / 256.  y at or above the last value gives the
+    last code (the clamp of App. D).  The caller passes u already mirrored
+    for negative elements (255 - u), which makes the magnitude rule equal to
+    App. D's signed one.
+
+    The comparison z = 512 (y - lo) + (2u + 1) d against 512 d is exact in
+    float64 wherever it can come out either way (y is an fp32 value)."""
+    y = np.asarray(y, dtype=np.float64)
+    u = np.asarray(u, dtype=np.float64)
+    n = values.size
+    lo = np.searchsorted(values, y, side="right") - 1      # values[lo] <= y < values[lo+1]
+    lo = np.clip(lo, 0, n - 2)
+    d = values[lo + 1] - values[lo]
+    z = 512.0 * (y - values[lo]) + (2.0 * u + 1.0) * d
+    full = 512.0 * d
+    hi_even = (lo + 1) % 2 == 0
+    idx = np.where((z > full) | ((z == full) & hi_even), lo + 1, lo)
+    idx = np.where(y >= values[-1], n - 1, idx)
+    return idx.astype(np.int64)

@@ -12,6 +12,7 @@ Follows, in order:
   Sec. 3.2 / App. B.3:            T stored in bit 7 of the E4M3 block scale.
   App. B.2:                       nibble = [s | p2 p1 p0].
   App. B.1:                       blocks of V = 16 values along the reduction dim.
+  App. D (optional):              stochastic rounding of the chosen branch's codes.
 
 Readings of passages the paper leaves open (all listed in the design notes):
   * X_FP8 = fl32(X / s32) with IEEE fp32 division; s32 = fl32(amax / 2688),
@@ -23,6 +24,10 @@ Readings of passages the paper leaves open (all listed in the design notes):
   * The nibble's sign bit is the sign bit of X, also when the code is zero.
   * Layout: element 2j in the low nibble of byte j; codes [rows, K/2],
     scales [rows, K/16], both row-major.
+  * Stochastic rounding: App. D's rule on the local lattice of each grid
+    (see ``formats.stochastic_round_to_codebook``), applied to the fp32
+    quotient, with Philox4x32-10 draws of 8 bits per element
+    (``oracle.philox``); scales and the format choice stay round-to-nearest.
 """
 from __future__ import annotations
 
@@ -32,6 +37,7 @@ from fractions import Fraction
 import numpy as np
 
 from . import formats as F
+from . import philox
 
 BLOCK = 16
 TENSOR_DIVISOR = np.float32(2688.0)     # 6 * 448 = 7 * 384 (Algorithm 1)
@@ -87,10 +93,19 @@ def _fraction_sum(row) -> Fraction:
     return sum((Fraction(float(t)) for t in row), Fraction(0))
 
 
+def signed_draws(u: np.ndarray, sign: np.ndarray) -> np.ndarray:
+    """App. D rounds the signed quotient: q + eps - 1/2 for q < 0 is the
+    magnitude |q| + (1 - eps) - 1/2 negated, so a negative element uses the
+    magnitude rule with eps' = 1 - eps, i.e. draw 255 - u."""
+    return np.where(sign == 1, 255 - u, u)
+
+
 MODES = ("select", "e2m1", "e1m2")
+ROUNDINGS = ("nearest", "stochastic")
 
 
-def quantize(x_bits: np.ndarray, s32=None, mode: str = "select") -> Quantized:
+def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str = "nearest",
+             seed: int = 0, offset: int = 0) -> Quantized:
     """Algorithm 1 on a bf16 tensor ``x_bits`` (uint16 [rows, K], K % 16 == 0).
 
     ``s32`` None computes the tensor scale (Algorithm 1); otherwise the given
@@ -99,8 +114,16 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select") -> Quantized:
     Algorithm 1 for every block, with everything else unchanged: the E2M1
     branch alone is NVFP4 (Sec. 2.1: block scale E4M3(max/6), E2M1 codes) and
     the E1M2 branch alone is the INT4-style format, with the same tensor-scale
-    rule; T still records the branch."""
-    assert mode in MODES
+    rule; T still records the branch.
+
+    ``rounding`` "stochastic" writes the codes of the chosen branch by the
+    stochastic rounding of App. D (``formats.stochastic_round_to_codebook``)
+    of the same fp32 quotient y = fl32(|x| / s8), with the draws u of
+    ``philox.block_bytes(rows, K, seed, offset)`` (255 - u for an element
+    whose sign bit is set).  Block scales and the format choice are those of
+    round-to-nearest: the choice does not depend on the draws, so each code
+    stays an unbiased estimate of y on its grid."""
+    assert mode in MODES and rounding in ROUNDINGS
     x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
     rows, k = x_bits.shape
     assert k % BLOCK == 0
@@ -120,10 +143,10 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select") -> Quantized:
             y = np.where(s8_32[..., None] > 0, xb / s8_32[..., None], np.float32(0)).astype(np.float32)
         q = F.round_to_codebook(y.astype(np.float64), grid)
         d = grid[q] * s8[..., None]                          # dequantized, exact in fp64
-        return code, s8, q, d
+        return code, s8, q, d, y
 
-    cf, sf, qf, df = branch(6, F.F_GRID)
-    ci, si, qi, di = branch(7, F.I_GRID)
+    cf, sf, qf, df, yf = branch(6, F.F_GRID)
+    ci, si, qi, di, yi = branch(7, F.I_GRID)
 
     # Err_E2M1 - Err_E1M2 = sum((x - Df)^2 - (x - Di)^2) = sum((Di - Df) * (2x - Df - Di)).
     # Each term is exact in fp64; the block sum is certified exact or redone
@@ -141,8 +164,13 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select") -> Quantized:
     if mode != "select":
         t = np.full_like(t, 0 if mode == "e2m1" else 1)
 
-    mag = np.where(t[..., None] == 1, qi, qf).astype(np.uint8)
     sign = (x_bits.reshape(rows, nb, BLOCK) >> 15).astype(np.uint8)
+    if rounding == "stochastic":
+        u = philox.block_bytes(rows, k, seed, offset).reshape(rows, nb, BLOCK).astype(np.int64)
+        u = signed_draws(u, sign)
+        qf = F.stochastic_round_to_codebook(yf, F.F_GRID, u)
+        qi = F.stochastic_round_to_codebook(yi, F.I_GRID, u)
+    mag = np.where(t[..., None] == 1, qi, qf).astype(np.uint8)
     nib = (sign << 3) | mag
     nib = nib.reshape(rows, k)
     codes = (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)

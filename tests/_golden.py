@@ -50,3 +50,22 @@ def handworked_gemm():
         k, *v = line.split()
         d[k] = [float(x) for x in v]
     return d
+
+
+def philox_kat():
+    out = []
+    for line in _lines("philox4x32_kat.txt"):
+        rounds, ctr, key, words = [p.strip() for p in line.split("|")]
+        out.append(dict(rounds=int(rounds),
+                        counter=[int(v, 16) for v in ctr.split()],
+                        key=[int(v, 16) for v in key.split()],
+                        out=[int(v, 16) for v in words.split()]))
+    return out
+
+
+def sr_handworked():
+    out = []
+    for line in _lines("sr_handworked.txt"):
+        grid, y, u, code, _ = [p.strip() for p in line.split("|")]
+        out.append(dict(grid=grid, y=float(Fraction(y)), u=int(u), code=int(code)))
+    return out

@@ -161,3 +161,98 @@ def test_catches_forced_mode_wrong_scale(monkeypatch):
 
     monkeypatch.setattr(Q, "quantize", mutated)
     assert not _forced_pins_pass()
+
+
+def _sr_pins_pass() -> bool:
+    """The stochastic-rounding pins (tests/test_oracle_sr.py) as one predicate."""
+    from tests import test_oracle_sr as TS
+    try:
+        TS.test_handworked_roundings()
+        TS.test_int4_branch_is_appendix_d_formula(1)
+        TS.test_e2m1_branch_is_formula_on_uniform_pieces(4)
+        TS.test_ties_against_bruteforce()
+        TS.test_scales_and_choice_are_round_to_nearest()
+    except AssertionError:
+        return False
+    return True
+
+
+def test_unmutated_sr_pins_pass():
+    assert _sr_pins_pass()
+
+
+def test_catches_sr_without_half_offset(monkeypatch):
+    orig = F.stochastic_round_to_codebook
+    # eps = u / 256 instead of (u + 1/2) / 256: equivalent to shifting u by -1/2
+    monkeypatch.setattr(F, "stochastic_round_to_codebook",
+                        lambda y, values, u: orig(y, values, np.asarray(u, np.float64) - 0.5))
+    assert not _sr_pins_pass()
+
+
+def test_catches_sr_unmirrored_negatives(monkeypatch):
+    monkeypatch.setattr(Q, "signed_draws", lambda u, sign: u)
+    assert not _sr_pins_pass()
+
+
+def test_catches_sr_ties_down(monkeypatch):
+    orig = F.stochastic_round_to_codebook
+
+    def ties_down(y, values, u):
+        idx = orig(y, values, u)
+        y = np.asarray(y, np.float64)
+        u = np.asarray(u, np.float64)
+        lo = np.searchsorted(values, y, side="right") - 1
+        lo = np.clip(lo, 0, values.size - 2)
+        d = values[lo + 1] - values[lo]
+        tie = 512.0 * (y - values[lo]) + (2.0 * u + 1.0) * d == 512.0 * d
+        return np.where(tie & (y < values[-1]), lo, idx)
+
+    monkeypatch.setattr(F, "stochastic_round_to_codebook", ties_down)
+    assert not _sr_pins_pass()
+
+
+def _hadamard_pins_pass() -> bool:
+    from tests import test_oracle_hadamard as TH
+    try:
+        TH.test_unit_vectors()
+        TH.test_matches_rational_butterflies(32)
+        TH.test_near_midpoint_elements(128)
+        TH.test_signs_act_on_inputs()
+        TH.test_overflow_and_zeros()
+    except AssertionError:
+        return False
+    return True
+
+
+def test_unmutated_hadamard_pins_pass():
+    assert _hadamard_pins_pass()
+
+
+def test_catches_hadamard_signs_on_outputs(monkeypatch):
+    from oracle import hadamard as HD
+    orig = HD.hadamard
+
+    def on_outputs(x_bits, b, signs=None):
+        y = orig(x_bits, b)
+        if signs is None:
+            return y
+        flip = np.tile(np.asarray(signs) < 0, y.shape[1] // b)
+        return np.where(flip[None, :] & ((y & 0x7FFF) != 0), y ^ 0x8000, y).astype(np.uint16)
+
+    monkeypatch.setattr(HD, "hadamard", on_outputs)
+    assert not _hadamard_pins_pass()
+
+
+def test_catches_hadamard_double_rounding(monkeypatch):
+    from oracle import hadamard as HD
+    orig = HD.round_to_bf16
+    # round to fp32 first, then to bf16
+    monkeypatch.setattr(HD, "round_to_bf16",
+                        lambda y: orig(np.asarray(y, np.float64).astype(np.float32).astype(np.float64)))
+    assert not _hadamard_pins_pass()
+
+
+def test_catches_hadamard_unnormalized(monkeypatch):
+    from oracle import hadamard as HD
+    monkeypatch.setattr(HD, "sylvester", lambda b, _o=HD.sylvester: 2 * _o(b))
+    assert not _hadamard_pins_pass()
