@@ -135,25 +135,43 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
     s32 = torch.empty(1, dtype=torch.float32, device=dev)
     M.mixfp4_quantize(xq, None, codes, scales, scale_out=s32)     # s32 for the given mode
 
-    def timed(given: bool, mode: str = "mixfp4") -> float:
+    signs = torch.tensor(np.where(np.random.default_rng(4).random(128) < 0.5, -1, 1)
+                         .astype(np.int8), device=dev)
+
+    def time_calls(fn) -> float:
         for _ in range(3):
-            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32, mode=mode)
+            fn()
         torch.cuda.synchronize()
         e = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)]
         e[0].record()
         for i in range(iters):
-            M.mixfp4_quantize(xq, s32 if given else None, codes, scales, scale_out=s32, mode=mode)
+            fn()
             e[i + 1].record()
         torch.cuda.synchronize()
         return float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(iters)]))
 
+    def timed(given: bool, mode: str = "mixfp4", **kw) -> float:
+        return time_calls(lambda: M.mixfp4_quantize(xq, s32 if given else None, codes, scales,
+                                                    scale_out=s32, mode=mode, **kw))
+
     ms_given = timed(True)
     ms_compute = timed(False)
     ms_nvfp4 = timed(True, "e2m1")
+    ms_sr = timed(True, rounding="stochastic", seed=1, offset=0)
+    ms_rht = timed(True, hadamard_block=128, hadamard_signs=signs)
+    ms_rht_sr = timed(True, rounding="stochastic", seed=1, hadamard_block=128,
+                      hadamard_signs=signs)
     n = xq.numel()
-    del xq, codes, scales
+    del codes, scales
+    torch.cuda.empty_cache()
+    yq = torch.empty_like(xq)
+    ms_had = time_calls(lambda: M.mixfp4_hadamard(xq, 128, signs, out=yq))
+    del xq, yq
     torch.cuda.empty_cache()
     gbps = n * QUANT_BYTES_PER_ELEM / (ms_given * 1e-3) / 1e9
+
+    def rate(ms, bpe=QUANT_BYTES_PER_ELEM):
+        return round(n * bpe / (ms * 1e-3) / 1e9, 1)
     return {
         "workload": "quantize-only Q[16384,16384] bf16 (2^28 elements), seed 4 block mixture: "
                     "90% of 16-blocks N(0,0.1), 10% Laplace(0,1) with one x40 spike",
@@ -168,6 +186,18 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
         "e2m1_only_us": round(ms_nvfp4 * 1e3, 2),
         "e2m1_only_GBps": round(n * QUANT_BYTES_PER_ELEM / (ms_nvfp4 * 1e-3) / 1e9, 1),
         "e2m1_only_note": "the same kernel forced to the E2M1 branch (NVFP4 encoding), s32 given",
+        "stochastic_us": round(ms_sr * 1e3, 2), "stochastic_GBps": rate(ms_sr),
+        "stochastic_note": "MixFP4 selection with stochastic rounding of the codes (App. D), "
+                           "Philox4x32-10 draws per block, s32 given",
+        "rht128_quantize_us": round(ms_rht * 1e3, 2), "rht128_quantize_GBps": rate(ms_rht),
+        "rht128_sr_quantize_us": round(ms_rht_sr * 1e3, 2),
+        "rht128_sr_quantize_GBps": rate(ms_rht_sr),
+        "rht_note": "random Hadamard rotation with 128-blocks fused before the quantizer "
+                    "(exact fp64 transform, rounded to bf16), s32 given; with and without "
+                    "stochastic rounding",
+        "hadamard128_us": round(ms_had * 1e3, 2), "hadamard128_GBps": rate(ms_had, 4.0),
+        "hadamard_note": "standalone mixfp4_hadamard, 128-blocks with signs: 2 B read + 2 B "
+                         "written per element",
     }
 
 

@@ -39,7 +39,8 @@ extern "C" {
 typedef enum {
   MIXFP4_OK = 0,
   MIXFP4_ERR_NULL = 1,    /* a required pointer is NULL                      */
-  MIXFP4_ERR_SHAPE = 2,   /* negative size, K % 16 != 0, ldx < K, ldx % 8    */
+  MIXFP4_ERR_SHAPE = 2,   /* negative size, K % 16 != 0, ldx < K, ldx % 8,
+                             or a bad Hadamard block size                 */
   MIXFP4_ERR_ALIGN = 3,   /* a pointer misses its required alignment         */
   MIXFP4_ERR_FLAGS = 4,   /* unknown flag bits                               */
   MIXFP4_ERR_LAUNCH = 5   /* the HIP runtime rejected a kernel launch        */
@@ -54,6 +55,8 @@ typedef enum {
  * GEMM read the result like any MixFP4 tensor:                             */
 #define MIXFP4_FORCE_E2M1 2u    /* E2M1 only (T = 0): NVFP4 (Sec. 2.1)        */
 #define MIXFP4_FORCE_E1M2 4u    /* E1M2 x2 only (T = 1): INT4 codes           */
+/* Stochastic rounding of the codes (App. D); mixfp4_quantize_ex only.      */
+#define MIXFP4_STOCHASTIC 8u
 
 /*
  * mixfp4_quantize - Algorithm 1 ("MixFP4 data type quantization") on a bf16
@@ -80,11 +83,72 @@ typedef enum {
  *                GIVEN: read; must be finite and > 0.
  *   flags        MIXFP4_SCALE_COMPUTE or MIXFP4_SCALE_GIVEN, optionally OR-ed
  *                with one of MIXFP4_FORCE_E2M1 / MIXFP4_FORCE_E1M2; any other
- *                bit, or both FORCE bits, returns MIXFP4_ERR_FLAGS.
+ *                bit (MIXFP4_STOCHASTIC included: it needs the seed of
+ *                mixfp4_quantize_ex), or both FORCE bits, returns
+ *                MIXFP4_ERR_FLAGS.
  */
 int mixfp4_quantize(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
                     uint8_t *codes, uint8_t *scales, float *tensor_scale,
                     unsigned flags, void *stream);
+
+/*
+ * mixfp4_quantize_ex - mixfp4_quantize with the two steps the paper's FP4
+ * training recipe puts around the quantizer (Sec. 3.2, Fig. 7; Sec. 4.3):
+ * an optional random Hadamard rotation of X first, and optional stochastic
+ * rounding of the codes (App. D).  With hadamard_block == 0 and without
+ * MIXFP4_STOCHASTIC it is mixfp4_quantize.
+ *
+ *   x ... tensor_scale  as for mixfp4_quantize; with a rotation, COMPUTE
+ *                mode takes s32 from the rotated tensor (two passes over X).
+ *   flags        as for mixfp4_quantize, plus MIXFP4_STOCHASTIC.
+ *   hadamard_block  0 (no rotation) or b in {16, 32, 64, 128, 256} with
+ *                k % b == 0: X is first replaced by the bf16 result of
+ *                mixfp4_hadamard(X, b, hadamard_signs), bit for bit, and
+ *                that tensor is quantized.  Anything else: MIXFP4_ERR_SHAPE.
+ *   hadamard_signs  device array of b bytes (bit 7 set = -1) or NULL.
+ *   seed, offset Philox4x32-10 (Salmon et al., SC 2011) key and the high
+ *                64 bits of its counter; block g = row * k/16 + column block
+ *                takes counter (g, offset), and element j of the block the
+ *                draw u = byte j % 4 of output word j / 4 (least significant
+ *                first).  Ignored without MIXFP4_STOCHASTIC.
+ *
+ * Stochastic rounding replaces only the codes of the branch Algorithm 1
+ * chose (scales, T and s32 are those of round-to-nearest, so the choice is
+ * independent of the draws).  For the fp32 quotient y = |x| / s8 between
+ * grid neighbours lo <= y < lo + d, the code is that of the nearer of lo and
+ * lo + d to y + (eps - 1/2) d, ties to the even code, with
+ * eps = (u + 1/2) / 256 for X >= 0 and (255 - u + 1/2) / 256 for X < 0 (App.
+ * D's round(q + eps - 1/2) on the signed quotient); y at or above the
+ * largest grid value gives that value.  Deterministic for a given seed and
+ * offset, and bit-identical to the CPU oracle.
+ */
+int mixfp4_quantize_ex(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
+                       uint8_t *codes, uint8_t *scales, float *tensor_scale,
+                       unsigned flags, int32_t hadamard_block,
+                       const int8_t *hadamard_signs, uint64_t seed,
+                       uint64_t offset, void *stream);
+
+/*
+ * mixfp4_hadamard - block-diagonal (random) Hadamard transform along k, the
+ * rotation applied before quantization in the paper's training recipe (RHT,
+ * Sec. 3.2 / Fig. 7) and in its rotated PTQ runs (Sec. 4.2):
+ *   y[r, c b + j] = sum_i s_i x[r, c b + i] H_b[i, j] / sqrt(b),
+ * H_b the Sylvester Hadamard matrix (entry (-1)^popcount(i & j)), s_i = -1
+ * where bit 7 of signs[i] is set, +1 otherwise (all +1 for signs == NULL).
+ * Each output is the exact value rounded once to bf16 (nearest, ties to
+ * even; Inf on overflow; an exactly zero result is +0), provided the nonzero
+ * inputs of each b-block span at most a factor 2^(45 - log2 b) in magnitude
+ * (2^37 at b = 256), which keeps every fp64 partial sum exact; beyond that
+ * the sums are fp64 with their rounding.
+ *
+ *   x        bf16 [rows, k], row pitch ldx (>= k, % 8 == 0), 16-byte aligned.
+ *   block    b in {16, 32, 64, 128, 256}, k % b == 0 (else MIXFP4_ERR_SHAPE).
+ *   signs    device array of b bytes, or NULL.
+ *   y        out, bf16 [rows, k] contiguous, 16-byte aligned, not aliasing x.
+ */
+int mixfp4_hadamard(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
+                    int32_t block, const int8_t *signs, uint16_t *y,
+                    void *stream);
 
 /*
  * mixfp4_dequantize - decode MixFP4 back to fp32 (App. B.2-B.3):
@@ -131,7 +195,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 101
+#define MIXFP4_ABI_VERSION 102
 
 #ifdef __cplusplus
 }

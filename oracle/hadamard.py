@@ -22,9 +22,10 @@ Readings (the paper does not fix them; listed in the design notes):
     vector for every block of every row;
   * b is a power of two from 16 to 256 and divides K.
 
-Exactness here: the block sums are exact in float64 when certified (every
-nonzero term is a multiple of 2^u and the absolute sum stays below 2^(u+53));
-other blocks are summed with rationals.  For b a power of 4 the division by
+Exactness here: the block sums are a float64 matrix product, exact when the
+block is certified (every nonzero input is a multiple of 2^u and the absolute
+sum stays below 2^(u+53)); elements of other blocks are summed with
+rationals.  For b a power of 4 the division by
 sqrt(b) is exact; otherwise the float64 quotient is within 2^-51 of the exact
 one, and every element whose bf16 rounding is not settled by that bound is
 decided exactly by comparing squares of integers.
@@ -71,20 +72,21 @@ def round_to_bf16(y: np.ndarray) -> np.ndarray:
     return (r.astype(np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
 
 
-def _certified_sums(terms: np.ndarray):
-    """Row sums of exactly representable float64 ``terms`` [n, b] and a mask
-    of rows whose float64 sum is exact in any order (see module header)."""
-    s = terms.sum(axis=-1)
-    nz = terms != 0
-    m, e = np.frexp(terms)
+def _certified_blocks(x: np.ndarray) -> np.ndarray:
+    """Mask of Hadamard blocks (rows of ``x`` [n, b], exact float64 values)
+    whose sums sum_i +-x_i are exact in float64 in any order: every nonzero
+    x_i is a multiple of 2^u (u = the lowest set bit over the block) and
+    sum |x_i| < 2^(u + 53), so every partial sum is a multiple of 2^u below
+    2^(u + 53) and representable."""
+    nz = x != 0
+    m, e = np.frexp(x)
     mi = np.abs(np.ldexp(m, 53)).astype(np.int64)
     low = mi & (-mi)
     lowexp = np.where(nz, e.astype(np.float64) - 53.0 + np.log2(np.maximum(low, 1).astype(np.float64)),
                       np.inf)
     u = lowexp.min(axis=-1)
-    total = np.abs(terms).sum(axis=-1) * (1.0 + 2.0 ** -40)
-    ok = np.isinf(u) | (total < np.ldexp(1.0, np.clip(u + 53, -1074, 1023).astype(np.int64)))
-    return s, ok
+    total = np.abs(x).sum(axis=-1) * (1.0 + 2.0 ** -40)
+    return np.isinf(u) | (total < np.ldexp(1.0, np.clip(u + 53, -1074, 1023).astype(np.int64)))
 
 
 def bf16_bits_value(bits: int) -> Fraction:
@@ -148,22 +150,16 @@ def hadamard(x_bits: np.ndarray, b: int, signs=None) -> np.ndarray:
         return x_bits.copy()
     level = int(round(math.log2(b)))
     H = sylvester(b).astype(np.float64)
-    xall = bf16_bits_to_f64(x_bits).reshape(-1, b) * s[None, :]          # exact (sign flips)
-    out = np.empty(xall.shape, dtype=np.uint16)
-    step = max(1, (1 << 22) // (b * b))
-    for c0 in range(0, xall.shape[0], step):
-        x = xall[c0:c0 + step]
-        n = x.shape[0]
-        # terms[c, j, i] = x[c, i] H[i, j], exact; their sum over i is y[c, j] sqrt(b)
-        terms = (x[:, None, :] * H.T[None, :, :]).reshape(n * b, b)
-        S, ok = _certified_sums(terms)
-        v = S / math.sqrt(2.0 ** level)                  # exact for even level, else within 2^-52
-        res = round_to_bf16(v)
-        if level % 2:
-            # settled when both ends of the error interval round alike
-            ok &= round_to_bf16(v * (1.0 - 2.0 ** -50)) == round_to_bf16(v * (1.0 + 2.0 ** -50))
-        res = np.where(S == 0, np.uint16(0), res)
-        for i in np.flatnonzero(~ok):
-            res[i] = _exact_element(terms[i], level)
-        out[c0:c0 + n] = res.reshape(n, b)
-    return out.reshape(rows, k)
+    x = bf16_bits_to_f64(x_bits).reshape(-1, b) * s[None, :]           # exact (sign flips)
+    # S[c, j] = sum_i x[c, i] H[i, j]: a float64 product, exact for certified blocks
+    S = x @ H
+    ok = np.repeat(_certified_blocks(x)[:, None], b, axis=1)
+    v = S / math.sqrt(2.0 ** level)                      # exact for even level, else within 2^-52
+    res = round_to_bf16(v)
+    if level % 2:
+        # settled when both ends of the error interval round alike
+        ok &= round_to_bf16(v * (1.0 - 2.0 ** -50)) == round_to_bf16(v * (1.0 + 2.0 ** -50))
+    res = np.where(S == 0, np.uint16(0), res)
+    for c, j in np.argwhere(~ok):
+        res[c, j] = _exact_element(x[c] * H[:, j], level)
+    return res.reshape(rows, k)

@@ -54,12 +54,16 @@ def philox4x32(counter: np.ndarray, key: np.ndarray, rounds: int = ROUNDS) -> np
     return np.stack([c0, c1, c2, c3], axis=-1).astype(np.uint32)
 
 
-def block_bytes(rows: int, k: int, seed: int, offset: int = 0) -> np.ndarray:
+def block_bytes(rows: int, k: int, seed: int, offset: int = 0, row_index=None) -> np.ndarray:
     """The integers u (uint8 [rows, K]) that the stochastic-rounding quantizer
-    draws for a [rows, K] tensor under ``seed`` and ``offset`` (64-bit each)."""
+    draws for a [rows, K] tensor under ``seed`` and ``offset`` (64-bit each).
+    ``row_index`` (optional) gives the rows' indices in a larger tensor, for
+    checking a sample of its rows."""
     assert k % 16 == 0
     nb = k // 16
-    g = np.arange(rows * nb, dtype=np.uint64)
+    r = np.arange(rows, dtype=np.uint64) if row_index is None else np.asarray(row_index, np.uint64)
+    assert r.shape == (rows,)
+    g = (r[:, None] * np.uint64(nb) + np.arange(nb, dtype=np.uint64)[None, :]).reshape(-1)
     ctr = np.stack([g & MASK, g >> np.uint64(32),
                     np.full_like(g, offset & MASK), np.full_like(g, (offset >> 32) & MASK)], axis=-1)
     key = np.array([seed & MASK, (seed >> 32) & MASK], dtype=np.uint64)

@@ -105,7 +105,7 @@ ROUNDINGS = ("nearest", "stochastic")
 
 
 def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str = "nearest",
-             seed: int = 0, offset: int = 0) -> Quantized:
+             seed: int = 0, offset: int = 0, row_index=None) -> Quantized:
     """Algorithm 1 on a bf16 tensor ``x_bits`` (uint16 [rows, K], K % 16 == 0).
 
     ``s32`` None computes the tensor scale (Algorithm 1); otherwise the given
@@ -122,7 +122,8 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str =
     ``philox.block_bytes(rows, K, seed, offset)`` (255 - u for an element
     whose sign bit is set).  Block scales and the format choice are those of
     round-to-nearest: the choice does not depend on the draws, so each code
-    stays an unbiased estimate of y on its grid."""
+    stays an unbiased estimate of y on its grid.  ``row_index`` numbers the
+    rows within a larger tensor (the draws depend on the block index there)."""
     assert mode in MODES and rounding in ROUNDINGS
     x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
     rows, k = x_bits.shape
@@ -166,7 +167,8 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str =
 
     sign = (x_bits.reshape(rows, nb, BLOCK) >> 15).astype(np.uint8)
     if rounding == "stochastic":
-        u = philox.block_bytes(rows, k, seed, offset).reshape(rows, nb, BLOCK).astype(np.int64)
+        u = philox.block_bytes(rows, k, seed, offset, row_index).reshape(rows, nb, BLOCK)
+        u = u.astype(np.int64)
         u = signed_draws(u, sign)
         qf = F.stochastic_round_to_codebook(yf, F.F_GRID, u)
         qi = F.stochastic_round_to_codebook(yi, F.I_GRID, u)

@@ -6,7 +6,11 @@ the library's HIP kernels.  There is no CPU fallback: if the library is
 missing or fails to load, importing the low-level handle raises.
 
 Functions (same names as the C ABI in include/mixfp4.h):
-  mixfp4_quantize(x, tensor_scale=None, ..., mode="mixfp4") -> (codes, scales, s32)
+  mixfp4_quantize(x, tensor_scale=None, ..., mode="mixfp4", rounding="nearest",
+                  seed=0, offset=0, hadamard_block=0, hadamard_signs=None)
+      -> (codes, scales, s32)   (the C call is mixfp4_quantize_ex when
+                                  rotating or rounding stochastically)
+  mixfp4_hadamard(x, block, signs=None) -> bf16 tensor
   mixfp4_dequantize(codes, scales, tensor_scale=None) -> fp32 tensor
   mixfp4_gemm(a, w) -> C = A W^T (fp32), a/w are (codes, scales, s32) triples
 """
@@ -19,13 +23,15 @@ import torch
 
 from ._lib import LIB_PATH, MixFP4Error, lib
 
-__all__ = ["mixfp4_quantize", "mixfp4_dequantize", "mixfp4_gemm", "MixFP4Error",
-           "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN", "FORCE_E2M1", "FORCE_E1M2"]
+__all__ = ["mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_hadamard", "mixfp4_dequantize",
+           "mixfp4_gemm", "MixFP4Error", "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN",
+           "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC"]
 
 SCALE_COMPUTE = 0
 SCALE_GIVEN = 1
 FORCE_E2M1 = 2
 FORCE_E1M2 = 4
+STOCHASTIC = 8
 _MODES = {"mixfp4": 0, "e2m1": FORCE_E2M1, "e1m2": FORCE_E1M2}
 
 
@@ -47,16 +53,23 @@ def _check(status: int):
 
 def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
                     codes: torch.Tensor | None = None, scales: torch.Tensor | None = None,
-                    scale_out: torch.Tensor | None = None, mode: str = "mixfp4"):
+                    scale_out: torch.Tensor | None = None, mode: str = "mixfp4",
+                    rounding: str = "nearest", seed: int = 0, offset: int = 0,
+                    hadamard_block: int = 0, hadamard_signs: torch.Tensor | None = None):
     """Quantize a bf16 [rows, k] CUDA tensor (Algorithm 1).
 
     ``tensor_scale`` None computes s32 = max|X| / 2688 on the device (into
     ``scale_out`` if given); a 1-element fp32 tensor is used as the given s32.
     ``mode`` "mixfp4" selects the format per block; "e2m1" (NVFP4) and "e1m2"
-    (INT4) take that branch for every block.
+    (INT4) take that branch for every block.  ``rounding`` "stochastic"
+    writes the codes by App. D's stochastic rounding with Philox draws of
+    (``seed``, ``offset``).  ``hadamard_block`` b > 0 rotates X first
+    (mixfp4_hadamard with ``hadamard_signs``, an int8 CUDA tensor of b signs).
     Returns (codes uint8 [rows, k/2], scales uint8 [rows, k/16], s32 fp32 [1])."""
     if mode not in _MODES:
         raise ValueError(f"mode must be one of {sorted(_MODES)}")
+    if rounding not in ("nearest", "stochastic"):
+        raise ValueError("rounding must be 'nearest' or 'stochastic'")
     if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_cuda:
         raise ValueError("x must be a 2-D bfloat16 CUDA tensor")
     if x.stride(1) != 1:
@@ -73,10 +86,51 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
     else:
         ts = tensor_scale
         flags = SCALE_GIVEN
-    st = lib.mixfp4_quantize(_ptr(x), rows, k, x.stride(0) if rows > 0 else k, _ptr(codes),
-                             _ptr(scales), _ptr(ts), flags | _MODES[mode], _stream(dev))
+    flags |= _MODES[mode]
+    ldx = x.stride(0) if rows > 0 else k
+    if rounding == "nearest" and hadamard_block == 0:
+        st = lib.mixfp4_quantize(_ptr(x), rows, k, ldx, _ptr(codes), _ptr(scales), _ptr(ts),
+                                 flags, _stream(dev))
+    else:
+        if rounding == "stochastic":
+            flags |= STOCHASTIC
+        signs = _signs_arg(hadamard_signs, hadamard_block)
+        st = lib.mixfp4_quantize_ex(_ptr(x), rows, k, ldx, _ptr(codes), _ptr(scales), _ptr(ts),
+                                    flags, hadamard_block, _ptr(signs),
+                                    seed & 0xFFFFFFFFFFFFFFFF, offset & 0xFFFFFFFFFFFFFFFF,
+                                    _stream(dev))
     _check(st)
     return codes, scales, ts
+
+
+mixfp4_quantize_ex = mixfp4_quantize
+
+
+def _signs_arg(signs, block):
+    if signs is None:
+        return None
+    if signs.dtype != torch.int8 or not signs.is_cuda or not signs.is_contiguous() \
+            or signs.numel() != block:
+        raise ValueError("hadamard signs must be a contiguous int8 CUDA tensor of `block` entries")
+    return signs
+
+
+def mixfp4_hadamard(x: torch.Tensor, block: int, signs: torch.Tensor | None = None,
+                    out: torch.Tensor | None = None) -> torch.Tensor:
+    """Block-diagonal Hadamard transform of a bf16 [rows, k] CUDA tensor along
+    k: each block of ``block`` elements times diag(signs) H / sqrt(block),
+    rounded once to bf16.  ``signs``: int8 CUDA tensor of ``block`` entries
+    (negative = -1) or None."""
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_cuda or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D bfloat16 CUDA tensor with unit stride along K")
+    rows, k = x.shape
+    if out is None:
+        out = torch.empty((rows, k), dtype=torch.bfloat16, device=x.device)
+    sg = _signs_arg(signs, block)
+    st = lib.mixfp4_hadamard(_ptr(x), rows, k, x.stride(0) if rows > 0 else k, block, _ptr(sg),
+                             _ptr(out), _stream(x.device))
+    _check(st)
+    return out
 
 
 def mixfp4_dequantize(codes: torch.Tensor, scales: torch.Tensor,

@@ -19,6 +19,55 @@ int launch_status(hipError_t e) {
   return MIXFP4_ERR_LAUNCH;
 }
 
+bool valid_hadamard_block(int32_t b) {
+  return b == 16 || b == 32 || b == 64 || b == 128 || b == 256;
+}
+
+int quantize_impl(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
+                  uint8_t* scales, float* tensor_scale, unsigned flags, int32_t hadamard_block,
+                  const int8_t* hadamard_signs, uint64_t seed, uint64_t offset, void* stream) {
+  const unsigned known =
+      MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2 | MIXFP4_STOCHASTIC;
+  if ((flags & ~known) != 0u ||
+      (flags & (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) == (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2))
+    return MIXFP4_ERR_FLAGS;
+  const bool given = (flags & MIXFP4_SCALE_GIVEN) != 0u;
+  mixfp4::QuantOptions opt;
+  opt.mode = (flags & MIXFP4_FORCE_E2M1) ? 1 : (flags & MIXFP4_FORCE_E1M2) ? 2 : 0;
+  opt.sr = (flags & MIXFP4_STOCHASTIC) != 0u;
+  opt.srp = {(uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)offset, (uint32_t)(offset >> 32)};
+  if (rows < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;
+  if (rows > 0 && (ldx < k || (ldx % 8) != 0)) return MIXFP4_ERR_SHAPE;
+  if (hadamard_block != 0) {
+    if (!valid_hadamard_block(hadamard_block) || (k % hadamard_block) != 0) return MIXFP4_ERR_SHAPE;
+    opt.had = true;
+    opt.hp = mixfp4::hadamard_params(hadamard_block, hadamard_signs);
+  }
+  if (!tensor_scale) return MIXFP4_ERR_NULL;
+  const bool empty = rows == 0 || k == 0;
+  if (!empty && (!x || !codes || !scales)) return MIXFP4_ERR_NULL;
+  if (!aligned(tensor_scale, 4)) return MIXFP4_ERR_ALIGN;
+  if (!empty && (!aligned(x, 16) || !aligned(codes, 16))) return MIXFP4_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();   // drop stale errors so a launch failure is ours
+  if (!given && !empty && !opt.had && mixfp4::quantize_is_small(rows, k))
+    return launch_status(mixfp4::launch_quantize_small(x, rows, k, ldx, codes, scales,
+                                                       tensor_scale, opt, s));
+  if (!given) {
+    const int64_t nscr = empty ? 0 : rows * (k / mixfp4::kBlock);
+    const hipError_t e =
+        opt.had ? mixfp4::launch_tensor_scale_rotated(x, empty ? 0 : rows, k, ldx, opt.hp,
+                                                      empty ? nullptr : scales, nscr,
+                                                      tensor_scale, s)
+                : mixfp4::launch_tensor_scale(x, empty ? 0 : rows, k, ldx,
+                                              empty ? nullptr : scales, nscr, tensor_scale, s);
+    const int st = launch_status(e);
+    if (st != MIXFP4_OK) return st;
+  }
+  if (empty) return MIXFP4_OK;
+  return launch_status(mixfp4::launch_quantize(x, rows, k, ldx, codes, scales, tensor_scale, opt, s));
+}
+
 }  // namespace
 
 extern "C" {
@@ -29,7 +78,7 @@ const char* mixfp4_status_string(int status) {
   switch (status) {
     case MIXFP4_OK: return "MIXFP4_OK";
     case MIXFP4_ERR_NULL: return "MIXFP4_ERR_NULL: a required pointer is NULL";
-    case MIXFP4_ERR_SHAPE: return "MIXFP4_ERR_SHAPE: bad size (negative, K % 16 != 0, ldx < K or ldx % 8 != 0)";
+    case MIXFP4_ERR_SHAPE: return "MIXFP4_ERR_SHAPE: bad size (negative, K % 16 != 0, ldx < K, ldx % 8 != 0, or a Hadamard block that is not 16..256 or does not divide K)";
     case MIXFP4_ERR_ALIGN: return "MIXFP4_ERR_ALIGN: pointer misaligned";
     case MIXFP4_ERR_FLAGS: return "MIXFP4_ERR_FLAGS: unknown flag bits or both FORCE flags";
     case MIXFP4_ERR_LAUNCH: return "MIXFP4_ERR_LAUNCH: kernel launch failed";
@@ -41,32 +90,31 @@ const char* mixfp4_last_launch_error(void) { return g_last_launch_error; }
 
 int mixfp4_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
                     uint8_t* scales, float* tensor_scale, unsigned flags, void* stream) {
-  if ((flags & ~(MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) != 0u ||
-      (flags & (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) == (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2))
-    return MIXFP4_ERR_FLAGS;
-  const bool given = (flags & MIXFP4_SCALE_GIVEN) != 0u;
-  const int mode = (flags & MIXFP4_FORCE_E2M1) ? 1 : (flags & MIXFP4_FORCE_E1M2) ? 2 : 0;
-  if (rows < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;
+  if (flags & MIXFP4_STOCHASTIC) return MIXFP4_ERR_FLAGS;   // needs the seed of _ex
+  return quantize_impl(x, rows, k, ldx, codes, scales, tensor_scale, flags, 0, nullptr, 0, 0,
+                       stream);
+}
+
+int mixfp4_quantize_ex(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
+                       uint8_t* scales, float* tensor_scale, unsigned flags,
+                       int32_t hadamard_block, const int8_t* hadamard_signs, uint64_t seed,
+                       uint64_t offset, void* stream) {
+  return quantize_impl(x, rows, k, ldx, codes, scales, tensor_scale, flags, hadamard_block,
+                       hadamard_signs, seed, offset, stream);
+}
+
+int mixfp4_hadamard(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, int32_t block,
+                    const int8_t* signs, uint16_t* y, void* stream) {
+  if (!valid_hadamard_block(block)) return MIXFP4_ERR_SHAPE;
+  if (rows < 0 || k < 0 || (k % block) != 0) return MIXFP4_ERR_SHAPE;
   if (rows > 0 && (ldx < k || (ldx % 8) != 0)) return MIXFP4_ERR_SHAPE;
-  if (!tensor_scale) return MIXFP4_ERR_NULL;
-  const bool empty = rows == 0 || k == 0;
-  if (!empty && (!x || !codes || !scales)) return MIXFP4_ERR_NULL;
-  if (!aligned(tensor_scale, 4)) return MIXFP4_ERR_ALIGN;
-  if (!empty && (!aligned(x, 16) || !aligned(codes, 16))) return MIXFP4_ERR_ALIGN;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  (void)hipGetLastError();   // drop stale errors so a launch failure is ours
-  if (!given && !empty && mixfp4::quantize_is_small(rows, k))
-    return launch_status(mixfp4::launch_quantize_small(x, rows, k, ldx, codes, scales,
-                                                       tensor_scale, mode, s));
-  if (!given) {
-    const int st = launch_status(mixfp4::launch_tensor_scale(
-        x, empty ? 0 : rows, k, ldx, empty ? nullptr : scales,
-        empty ? 0 : rows * (k / mixfp4::kBlock), tensor_scale, s));
-    if (st != MIXFP4_OK) return st;
-  }
-  if (empty) return MIXFP4_OK;
-  return launch_status(
-      mixfp4::launch_quantize(x, rows, k, ldx, codes, scales, tensor_scale, mode, s));
+  if (rows == 0 || k == 0) return MIXFP4_OK;
+  if (!x || !y) return MIXFP4_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(y, 16)) return MIXFP4_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launch_status(mixfp4::launch_hadamard(x, rows, k, ldx,
+                                               mixfp4::hadamard_params(block, signs), y,
+                                               static_cast<hipStream_t>(stream)));
 }
 
 int mixfp4_dequantize(const uint8_t* codes, const uint8_t* scales, const float* tensor_scale,

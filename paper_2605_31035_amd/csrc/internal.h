@@ -9,6 +9,31 @@ namespace mixfp4 {
 // Block size along the reduction dimension (App. B.1, V = 16).
 constexpr int kBlock = 16;
 
+// Stochastic rounding: Philox4x32-10 key (seed) and counter words 2-3
+// (offset); words 0-1 of the counter are the block index.
+struct SrParams {
+  uint32_t seed_lo, seed_hi, off_lo, off_hi;
+};
+
+// Block-diagonal Hadamard rotation with blocks of b = 16 << lanes_log2.
+struct HadamardParams {
+  const int8_t* signs;   // b signs on the device (bit 7 set = -1), or NULL for all +1
+  int lanes_log2;        // log2(b / 16), 0..4
+  int odd;               // log2(b) odd: 1 / sqrt(b) is irrational
+  double scale;          // 1 / sqrt(b) in fp64 (exact for even log2 b)
+  double b;              // b as a double (for the midpoint decision)
+};
+HadamardParams hadamard_params(int b, const int8_t* signs);
+
+// Options of one quantize call beyond the format mode.
+struct QuantOptions {
+  int mode = 0;              // 0 MixFP4 selection, 1 E2M1 only (NVFP4), 2 E1M2 only (INT4)
+  bool sr = false;           // stochastic rounding of the codes
+  SrParams srp{};
+  bool had = false;          // rotate first
+  HadamardParams hp{};
+};
+
 // Launchers: shapes are validated by the ABI layer before these are called.
 // Tensor scale s32 = max|X| / 2688 (1.0 for all-zero X) into *tensor_scale.
 // `scratch` (may be NULL) is device memory of `scratch_bytes` that the call
@@ -16,16 +41,26 @@ constexpr int kBlock = 16;
 hipError_t launch_tensor_scale(const uint16_t* x, int64_t rows, int64_t k,
                                int64_t ldx, uint8_t* scratch, int64_t scratch_bytes,
                                float* tensor_scale, hipStream_t stream);
-// `mode`: 0 MixFP4 selection, 1 E2M1 only (NVFP4), 2 E1M2 only (INT4).
+// Tensor scale of the rotated tensor (the amax pass of a rotate-and-quantize
+// call); same contract as launch_tensor_scale.
+hipError_t launch_tensor_scale_rotated(const uint16_t* x, int64_t rows, int64_t k,
+                                       int64_t ldx, const HadamardParams& hp,
+                                       uint8_t* scratch, int64_t scratch_bytes,
+                                       float* tensor_scale, hipStream_t stream);
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k,
                            int64_t ldx, uint8_t* codes, uint8_t* scales,
-                           const float* tensor_scale, int mode, hipStream_t stream);
+                           const float* tensor_scale, const QuantOptions& opt,
+                           hipStream_t stream);
 // Tensor scale and quantization in one launch, for tensors with
-// quantize_is_small(rows, k) (rows * k at most 2^18); rows, k > 0.
+// quantize_is_small(rows, k) (rows * k at most 2^18); rows, k > 0; no rotation.
 bool quantize_is_small(int64_t rows, int64_t k);
 hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k,
                                  int64_t ldx, uint8_t* codes, uint8_t* scales,
-                                 float* tensor_scale, int mode, hipStream_t stream);
+                                 float* tensor_scale, const QuantOptions& opt,
+                                 hipStream_t stream);
+// Standalone rotation: y [rows, k] contiguous bf16.
+hipError_t launch_hadamard(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                           const HadamardParams& hp, uint16_t* y, hipStream_t stream);
 hipError_t launch_dequantize(const uint8_t* codes, const uint8_t* scales,
                              const float* tensor_scale, int64_t rows,
                              int64_t k, float* out, hipStream_t stream);

@@ -25,8 +25,12 @@
 //     sum_i (D_I - D_F)(2|x| - D_F - D_I) decides (every term exact, only
 //     elements whose two dequantized values differ contribute, so the sum
 //     is exact in any order).
+#include <cmath>
+
 #include "formats.h"
+#include "hadamard.h"
 #include "internal.h"
+#include "philox.h"
 
 namespace mixfp4 {
 namespace {
@@ -226,11 +230,46 @@ __device__ __forceinline__ void encode_i_saturated(const float (&xs)[16], float 
   }
 }
 
+// Stochastic rounding (App. D) of the block onto the chosen grid: y =
+// fl32(|x| / s) (the same quotient round-to-nearest takes), and between its
+// grid neighbours lo <= y < lo + d the rule round(y + (eps - 1/2) d) with
+// eps = (u + 1/2) / 256, u the element's draw (255 - u for a negative X,
+// which turns App. D's signed rule into this magnitude rule).  In units of
+// the local spacing, w = 512 (y - lo) / d is exact in fp32 and the rule
+// reads: up iff w > 511 - 2u, ties (w == 511 - 2u) to the even code.  y at
+// or above the largest magnitude clamps to code 7.  E2M1 spacing: 1/2 below
+// 2, 1 below 4, 2 up to 6; E1M2 (x2): 1 everywhere.
+__device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], float s, float r, bool int4,
+                                          uint4 rnd) {
+  const uint32_t words[4] = {rnd.x, rnd.y, rnd.z, rnd.w};
+  uint32_t o[2] = {0u, 0u};
+#pragma unroll
+  for (int j = 0; j < 16; ++j) {
+    const uint32_t xb = __float_as_uint(xs[j]);
+    const uint32_t neg = xb >> 31;
+    const float y = div_rn(__uint_as_float(xb & 0x7FFFFFFFu), s, r);
+    const uint32_t u = ((words[j >> 2] >> (8 * (j & 3))) & 0xFFu) ^ (neg ? 0xFFu : 0u);
+    const float thr = (float)(511 - 2 * (int)u);
+    const float inv_d = int4 ? 1.0f : (y < 2.0f ? 2.0f : (y < 4.0f ? 1.0f : 0.5f));
+    const uint32_t base = int4 ? 0u : (y < 2.0f ? 0u : (y < 4.0f ? 2u : 4u));
+    const float z = y * inv_d;
+    const float lat = floorf(z);
+    const float w = (z - lat) * 512.0f;
+    uint32_t code = (uint32_t)lat + base;
+    code += (w > thr || (w == thr && (code & 1u))) ? 1u : 0u;
+    code = y >= (int4 ? 7.0f : 6.0f) ? 7u : code;
+    o[j >> 3] |= (code | (neg << 3)) << (4 * (j & 7));
+  }
+  return make_uint2(o[0], o[1]);
+}
+
 // Codes and scale byte of one block from x (Algorithm 1 after the tensor
-// scale).
-template <int kMode>
+// scale).  With kSR the chosen branch's codes are written by stochastic
+// rounding with the draws in `rnd`; scales and the format choice stay those
+// of round-to-nearest.
+template <int kMode, bool kSR>
 __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2* __restrict__ tab,
-                                            uint2& out, uint32_t& scale_byte) {
+                                            uint2& out, uint32_t& scale_byte, uint4 rnd) {
   // fl32 rounding is monotonic, so bm is also fl32(max|X| / s32).
   float bm = 0.0f;
 #pragma unroll
@@ -261,7 +300,7 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
     encode_f_pair<14>(xs, sf, rf, pf);
   }
   if constexpr (kMode == kForceE2M1) {
-    out = make_uint2(pf[0], pf[1]);
+    out = kSR ? sr_codes(xs, sf, rf, false, rnd) : make_uint2(pf[0], pf[1]);
     scale_byte = cf;
     return;
   }
@@ -285,7 +324,7 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
     uint32_t sg[2] = {0u, 0u};
 #pragma unroll
     for (int j = 0; j < 16; ++j) sg[j >> 3] |= (__float_as_uint(xs[j]) >> 31) << (4 * (j & 7) + 3);
-    out = make_uint2(pi[0] | sg[0], pi[1] | sg[1]);
+    out = kSR ? sr_codes(xs, si, ri, true, rnd) : make_uint2(pi[0] | sg[0], pi[1] | sg[1]);
     scale_byte = 0x80u | ci;
     return;
   }
@@ -331,8 +370,12 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
     t1 = !(d < 0.0);
   }
   // Sign of X into bit 3 of every nibble: the E2M1 codes already carry it.
-  out.x = t1 ? (pi[0] | (pf[0] & 0x88888888u)) : pf[0];
-  out.y = t1 ? (pi[1] | (pf[1] & 0x88888888u)) : pf[1];
+  if constexpr (kSR) {
+    out = sr_codes(xs, t1 ? si : sf, t1 ? ri : rf, t1, rnd);
+  } else {
+    out.x = t1 ? (pi[0] | (pf[0] & 0x88888888u)) : pf[0];
+    out.y = t1 ? (pi[1] | (pf[1] & 0x88888888u)) : pf[1];
+  }
   scale_byte = t1 ? (0x80u | ci) : cf;
 }
 
@@ -340,12 +383,19 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
 // loaded as soon as the current one has been turned into x, so its load
 // overlaps this block's arithmetic (measured: a second block in flight, or
 // more waves per SIMD, gains nothing; the kernel is bound by VALU issue).
-template <bool kContig, bool kScaled, int kMode>
+//
+// kSR: stochastic rounding with Philox draws per block (its global index).
+// kHad: each block is first rotated (block-diagonal Hadamard across the
+// L = b / 16 lanes holding one Hadamard block; the grid stride is a multiple
+// of 256, so a thread keeps its position in its Hadamard block and every
+// Hadamard block is processed by lanes of one wave in one iteration).
+template <bool kContig, bool kScaled, int kMode, bool kSR, bool kHad>
 __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, int64_t nbk,
                                               int64_t ldx, int64_t nblocks,
                                               uint8_t* __restrict__ codes,
                                               uint8_t* __restrict__ scales, float xmul, float sx,
-                                              float rx, const float2* tab) {
+                                              float rx, const float2* tab, const SrParams& sr,
+                                              const HadamardParams& hp) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   // Loads are unconditional (a block index past the end reads the last
   // block, whose data is then never used), so they need no branch and no
@@ -363,15 +413,23 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
     q = *reinterpret_cast<const uint4*>(src + 8);
   };
   int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  SignMasks sm;
+  if constexpr (kHad) sm = load_sign_masks(hp, (int)(threadIdx.x & ((1u << hp.lanes_log2) - 1u)));
   uint4 a0, a1;
   load(g, a0, a1);
   for (; g < nblocks; g += stride) {
     float xs[16];
-    to_fp8_domain<kScaled>(a0, a1, xmul, sx, rx, xs);
+    if constexpr (kHad) {
+      uint4 r0 = a0, r1 = a1;
+      hadamard_rotate(r0, r1, sm, hp);
+      to_fp8_domain<kScaled>(r0, r1, xmul, sx, rx, xs);
+    } else {
+      to_fp8_domain<kScaled>(a0, a1, xmul, sx, rx, xs);
+    }
     load(g + stride, a0, a1);
     uint2 out;
     uint32_t sb;
-    quantize_xs<kMode>(xs, tab, out, sb);
+    quantize_xs<kMode, kSR>(xs, tab, out, sb, kSR ? block_draws(g, sr) : make_uint4(0, 0, 0, 0));
     *reinterpret_cast<uint2*>(codes + (g << 3)) = out;
     scales[g] = (uint8_t)sb;
   }
@@ -392,32 +450,34 @@ __device__ __forceinline__ void fill_scale_table(float2* tab) {
 // The division steps stay in the normal range for every element that can get
 // a nonzero code when 2^-90 <= s32 <= 2^120; beyond that both X and s32 are
 // rescaled by 2^64 or 2^-64 first.
-template <bool kContig, int kMode>
+template <bool kContig, int kMode, bool kSR, bool kHad>
 __device__ __forceinline__ void quantize_all(const uint16_t* __restrict__ x, int64_t nbk,
                                              int64_t ldx, int64_t nblocks,
                                              uint8_t* __restrict__ codes,
                                              uint8_t* __restrict__ scales, float s32,
-                                             const float2* tab) {
+                                             const float2* tab, const SrParams& sr,
+                                             const HadamardParams& hp) {
   if (s32 >= 0x1p-90f && s32 <= 0x1p120f) {
-    quantize_loop<kContig, false, kMode>(x, nbk, ldx, nblocks, codes, scales, 1.0f, s32,
-                                  __fdiv_rn(1.0f, s32), tab);
+    quantize_loop<kContig, false, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, 1.0f,
+                                                    s32, __fdiv_rn(1.0f, s32), tab, sr, hp);
   } else {
     const float xmul = s32 < 1.0f ? 0x1p64f : 0x1p-64f;
     const float sx = s32 * xmul;
-    quantize_loop<kContig, true, kMode>(x, nbk, ldx, nblocks, codes, scales, xmul, sx,
-                                 __fdiv_rn(1.0f, sx), tab);
+    quantize_loop<kContig, true, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xmul, sx,
+                                                   __fdiv_rn(1.0f, sx), tab, sr, hp);
   }
 }
 
-template <bool kContig, int kMode>
+template <bool kContig, int kMode, bool kSR, bool kHad>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
-    const float* __restrict__ tensor_scale) {
+    const float* __restrict__ tensor_scale, SrParams sr, HadamardParams hp) {
   __shared__ float2 tab[128];
   fill_scale_table(tab);
   __syncthreads();
-  quantize_all<kContig, kMode>(x, nbk, ldx, nblocks, codes, scales, *tensor_scale, tab);
+  quantize_all<kContig, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, *tensor_scale, tab,
+                                          sr, hp);
 }
 
 // Small tensors with the tensor scale computed (at most kSmallElems
@@ -432,10 +492,11 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
 constexpr int kSmallThreads = 1024;
 constexpr int64_t kSmallElems = int64_t(1) << 18;
 
-template <bool kContig, int kMode>
+template <bool kContig, int kMode, bool kSR>
 __global__ __launch_bounds__(kSmallThreads) void quantize_small_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
-    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, float* __restrict__ tensor_scale) {
+    uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, float* __restrict__ tensor_scale,
+    SrParams sr) {
   __shared__ float2 tab[128];
   __shared__ uint32_t wave_max[kSmallThreads / 64];
   fill_scale_table(tab);
@@ -491,31 +552,90 @@ __global__ __launch_bounds__(kSmallThreads) void quantize_small_kernel(
   }
   uint2 out;
   uint32_t sb;
-  quantize_xs<kMode>(xs, tab, out, sb);
+  quantize_xs<kMode, kSR>(xs, tab, out, sb, kSR ? block_draws(g, sr) : make_uint4(0, 0, 0, 0));
   *reinterpret_cast<uint2*>(codes + (g << 3)) = out;
   scales[g] = (uint8_t)sb;
 }
 
+// Per-workgroup max|Y| of the rotated tensor (bf16 magnitude bits of the
+// rounded results), same lane-per-block walk as the quantizer so that every
+// Hadamard block sits in consecutive lanes of one wave.  Results go to
+// partials[blockIdx.x] or, without partials, into *out by atomic max.
+template <bool kContig>
+__global__ __launch_bounds__(kThreads) void amax_rotated_kernel(
+    const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks, HadamardParams hp,
+    uint32_t* __restrict__ partials, uint32_t* __restrict__ out) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const SignMasks sm = load_sign_masks(hp, (int)(threadIdx.x & ((1u << hp.lanes_log2) - 1u)));
+  uint32_t m = 0u;
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nblocks; g += stride) {
+    const uint16_t* src;
+    if (kContig) {
+      src = x + (g << 4);
+    } else {
+      const int64_t r = g / nbk;
+      src = x + r * ldx + ((g - r * nbk) << 4);
+    }
+    uint4 v0 = *reinterpret_cast<const uint4*>(src);
+    uint4 v1 = *reinterpret_cast<const uint4*>(src + 8);
+    hadamard_rotate(v0, v1, sm, hp);
+    m = max(m, max(absmax8(v0), absmax8(v1)));
+  }
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  __shared__ uint32_t wave_max[kThreads / 64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) wave_max[wave] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t r = wave_max[0];
+    for (int w = 1; w < kThreads / 64; ++w) r = max(r, wave_max[w]);
+    if (partials) partials[blockIdx.x] = r;
+    else if (r) atomicMax(out, r << 16);
+  }
+}
+
+// Standalone rotation: y[g] = rotated block g (y contiguous [rows, k]).
+template <bool kContig>
+__global__ __launch_bounds__(kThreads) void hadamard_kernel(const uint16_t* __restrict__ x,
+                                                            int64_t nbk, int64_t ldx,
+                                                            int64_t nblocks, HadamardParams hp,
+                                                            uint16_t* __restrict__ y) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const SignMasks sm = load_sign_masks(hp, (int)(threadIdx.x & ((1u << hp.lanes_log2) - 1u)));
+  for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nblocks; g += stride) {
+    const uint16_t* src;
+    if (kContig) {
+      src = x + (g << 4);
+    } else {
+      const int64_t r = g / nbk;
+      src = x + r * ldx + ((g - r * nbk) << 4);
+    }
+    uint4 v0 = *reinterpret_cast<const uint4*>(src);
+    uint4 v1 = *reinterpret_cast<const uint4*>(src + 8);
+    hadamard_rotate(v0, v1, sm, hp);
+    uint4* dst = reinterpret_cast<uint4*>(y + (g << 4));
+    dst[0] = v0;
+    dst[1] = v1;
+  }
+}
+
 // Workgroups of kThreads that the device keeps resident at once for
-// quantize_kernel<kContig, kMode> (occupancy per CU x CU count), cached per
-// device.
-template <bool kContig, int kMode>
-int64_t resident_groups() {
-  static int64_t cached[64] = {0};
+// `kernel` (occupancy per CU x CU count); `cache` holds one value per device.
+template <typename Kernel>
+int64_t resident_groups(Kernel kernel, int64_t (&cache)[64]) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
-  if (!cached[dev]) {
+  if (!cache[dev]) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, quantize_kernel<kContig, kMode>, kThreads,
-                                                     0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess ||
         per_cu <= 0)
       per_cu = 4;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cus <= 0)
       cus = 256;
-    cached[dev] = (int64_t)per_cu * cus;
+    cache[dev] = (int64_t)per_cu * cus;
   }
-  return cached[dev];
+  return cache[dev];
 }
 
 int grid_for(int64_t work, int per_thread) {
@@ -525,93 +645,185 @@ int grid_for(int64_t work, int per_thread) {
   return (int)g;
 }
 
+// Per-workgroup maxima: to the caller's scratch (the scale-byte output, which
+// the quantize kernel overwrites afterwards) when it holds at least 16 slots,
+// else an atomic on *tensor_scale.  `run(grid, partials, out)` launches the
+// maximum kernel; `grid` is capped by the slots.
+template <typename Run>
+hipError_t tensor_scale_with(int64_t work, int grid, uint8_t* scratch, int64_t scratch_bytes,
+                             float* tensor_scale, hipStream_t stream, Run run) {
+  const uintptr_t base = reinterpret_cast<uintptr_t>(scratch);
+  const uintptr_t aligned = (base + 3u) & ~uintptr_t(3);
+  const int64_t slots = scratch ? (scratch_bytes - (int64_t)(aligned - base)) / 4 : 0;
+  if (work > 0 && slots >= 16) {
+    if (grid > slots) grid = (int)slots;
+    uint32_t* partials = reinterpret_cast<uint32_t*>(aligned);
+    run(grid, partials, (uint32_t*)nullptr);
+    reduce_scale<<<1, kThreads, 0, stream>>>(partials, grid, tensor_scale);
+    return hipGetLastError();
+  }
+  uint32_t* p = reinterpret_cast<uint32_t*>(tensor_scale);
+  clear_u32<<<1, 1, 0, stream>>>(p);
+  if (work > 0) run(grid, (uint32_t*)nullptr, p);
+  finalize_scale<<<1, 1, 0, stream>>>(p);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+HadamardParams hadamard_params(int b, const int8_t* signs) {
+  HadamardParams hp{};
+  int level = 0;
+  while ((1 << level) < b) ++level;
+  hp.signs = signs;
+  hp.lanes_log2 = level - 4;
+  hp.odd = level & 1;
+  // 1 / sqrt(b) = 2^-(level / 2) (times the fp64 sqrt(1/2) for odd levels)
+  hp.scale = std::ldexp(hp.odd ? 0.70710678118654752440 : 1.0, -(level / 2));
+  hp.b = (double)b;
+  return hp;
+}
 
 hipError_t launch_tensor_scale(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
                                uint8_t* scratch, int64_t scratch_bytes, float* tensor_scale,
                                hipStream_t stream) {
   const int64_t total = rows * (k >> 3);
-  // Per-workgroup maxima go to the caller's scale-byte output, which the
-  // quantize kernel overwrites afterwards; tiny outputs use an atomic instead.
-  const uintptr_t base = reinterpret_cast<uintptr_t>(scratch);
-  const uintptr_t aligned = (base + 3u) & ~uintptr_t(3);
-  const int64_t slots = scratch ? (scratch_bytes - (int64_t)(aligned - base)) / 4 : 0;
   // up to 1024 workgroups x 256 threads x 4 loads of 16 B keeps ~16 MB in flight
   int g = grid_for(total, 4);
   if (g > 1024) g = 1024;
-  if (total > 0 && slots >= 16) {
-    if (g > slots) g = (int)slots;
-    uint32_t* partials = reinterpret_cast<uint32_t*>(aligned);
-    amax_kernel<<<g, kThreads, 0, stream>>>(x, rows, k, ldx, partials, nullptr);
-    reduce_scale<<<1, kThreads, 0, stream>>>(partials, g, tensor_scale);
-    return hipGetLastError();
-  }
-  uint32_t* p = reinterpret_cast<uint32_t*>(tensor_scale);
-  clear_u32<<<1, 1, 0, stream>>>(p);
-  if (total > 0) amax_kernel<<<g, kThreads, 0, stream>>>(x, rows, k, ldx, nullptr, p);
-  finalize_scale<<<1, 1, 0, stream>>>(p);
-  return hipGetLastError();
+  return tensor_scale_with(total, g, scratch, scratch_bytes, tensor_scale, stream,
+                           [&](int grid, uint32_t* partials, uint32_t* out) {
+                             amax_kernel<<<grid, kThreads, 0, stream>>>(x, rows, k, ldx, partials,
+                                                                         out);
+                           });
+}
+
+hipError_t launch_tensor_scale_rotated(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                                       const HadamardParams& hp, uint8_t* scratch,
+                                       int64_t scratch_bytes, float* tensor_scale,
+                                       hipStream_t stream) {
+  const int64_t nbk = k / kBlock, nblocks = rows * nbk;
+  static int64_t cache_c[64], cache_s[64];
+  const int64_t resident = ldx == k ? resident_groups(amax_rotated_kernel<true>, cache_c)
+                                    : resident_groups(amax_rotated_kernel<false>, cache_s);
+  const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
+  int g = (int)(wanted < resident ? wanted : resident);
+  if (g < 1) g = 1;
+  return tensor_scale_with(nblocks, g, scratch, scratch_bytes, tensor_scale, stream,
+                           [&](int grid, uint32_t* partials, uint32_t* out) {
+                             if (ldx == k)
+                               amax_rotated_kernel<true><<<grid, kThreads, 0, stream>>>(
+                                   x, nbk, ldx, nblocks, hp, partials, out);
+                             else
+                               amax_rotated_kernel<false><<<grid, kThreads, 0, stream>>>(
+                                   x, nbk, ldx, nblocks, hp, partials, out);
+                           });
 }
 
 namespace {
 
-template <int kMode>
+template <int kMode, bool kSR>
 hipError_t launch_small_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
                              uint8_t* codes, uint8_t* scales, float* tensor_scale,
-                             hipStream_t stream) {
+                             const SrParams& sr, hipStream_t stream) {
   const int64_t nbk = k / kBlock, nblocks = rows * nbk;
   const int64_t g = (nblocks + kSmallThreads - 1) / kSmallThreads;   // one block per thread
   if (ldx == k)
-    quantize_small_kernel<true, kMode><<<(unsigned)g, kSmallThreads, 0, stream>>>(
-        x, nbk, ldx, nblocks, codes, scales, tensor_scale);
+    quantize_small_kernel<true, kMode, kSR><<<(unsigned)g, kSmallThreads, 0, stream>>>(
+        x, nbk, ldx, nblocks, codes, scales, tensor_scale, sr);
   else
-    quantize_small_kernel<false, kMode><<<(unsigned)g, kSmallThreads, 0, stream>>>(
-        x, nbk, ldx, nblocks, codes, scales, tensor_scale);
+    quantize_small_kernel<false, kMode, kSR><<<(unsigned)g, kSmallThreads, 0, stream>>>(
+        x, nbk, ldx, nblocks, codes, scales, tensor_scale, sr);
   return hipGetLastError();
 }
 
-template <int kMode>
+template <int kMode, bool kSR, bool kHad>
 hipError_t launch_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
-                       uint8_t* scales, const float* tensor_scale, hipStream_t stream) {
+                       uint8_t* scales, const float* tensor_scale, const QuantOptions& opt,
+                       hipStream_t stream) {
   const int64_t nbk = k / kBlock;
   const int64_t nblocks = rows * nbk;
   // One wave of resident workgroups (occupancy x CUs) walks all blocks, so
   // no partial second wave is left at the end; fewer if the tensor is small.
+  static int64_t cache_c[64], cache_s[64];
   const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
-  const int64_t resident = ldx == k ? resident_groups<true, kMode>() : resident_groups<false, kMode>();
+  const int64_t resident =
+      ldx == k ? resident_groups(quantize_kernel<true, kMode, kSR, kHad>, cache_c)
+               : resident_groups(quantize_kernel<false, kMode, kSR, kHad>, cache_s);
   const int g = (int)(wanted < resident ? wanted : resident);
   if (ldx == k)
-    quantize_kernel<true, kMode><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, codes, scales,
-                                                              tensor_scale);
+    quantize_kernel<true, kMode, kSR, kHad><<<g, kThreads, 0, stream>>>(
+        x, nbk, ldx, nblocks, codes, scales, tensor_scale, opt.srp, opt.hp);
   else
-    quantize_kernel<false, kMode><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, codes,
-                                                               scales, tensor_scale);
+    quantize_kernel<false, kMode, kSR, kHad><<<g, kThreads, 0, stream>>>(
+        x, nbk, ldx, nblocks, codes, scales, tensor_scale, opt.srp, opt.hp);
   return hipGetLastError();
+}
+
+template <int kMode>
+hipError_t launch_mode_opts(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                            uint8_t* codes, uint8_t* scales, const float* tensor_scale,
+                            const QuantOptions& opt, hipStream_t stream) {
+  if (opt.sr)
+    return opt.had ? launch_mode<kMode, true, true>(x, rows, k, ldx, codes, scales, tensor_scale,
+                                                    opt, stream)
+                   : launch_mode<kMode, true, false>(x, rows, k, ldx, codes, scales,
+                                                     tensor_scale, opt, stream);
+  return opt.had ? launch_mode<kMode, false, true>(x, rows, k, ldx, codes, scales, tensor_scale,
+                                                   opt, stream)
+                 : launch_mode<kMode, false, false>(x, rows, k, ldx, codes, scales, tensor_scale,
+                                                    opt, stream);
+}
+
+template <int kMode>
+hipError_t launch_small_opts(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                             uint8_t* codes, uint8_t* scales, float* tensor_scale,
+                             const QuantOptions& opt, hipStream_t stream) {
+  return opt.sr ? launch_small_mode<kMode, true>(x, rows, k, ldx, codes, scales, tensor_scale,
+                                                 opt.srp, stream)
+                : launch_small_mode<kMode, false>(x, rows, k, ldx, codes, scales, tensor_scale,
+                                                  opt.srp, stream);
 }
 
 }  // namespace
 
 hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
-                                 uint8_t* codes, uint8_t* scales, float* tensor_scale, int mode,
-                                 hipStream_t stream) {
-  if (mode == kForceE2M1)
-    return launch_small_mode<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
-  if (mode == kForceE1M2)
-    return launch_small_mode<kForceE1M2>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
-  return launch_small_mode<kSelect>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
+                                 uint8_t* codes, uint8_t* scales, float* tensor_scale,
+                                 const QuantOptions& opt, hipStream_t stream) {
+  if (opt.mode == kForceE2M1)
+    return launch_small_opts<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
+  if (opt.mode == kForceE1M2)
+    return launch_small_opts<kForceE1M2>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
+  return launch_small_opts<kSelect>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
 }
 
 bool quantize_is_small(int64_t rows, int64_t k) { return rows * k <= kSmallElems; }
 
 hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
-                           uint8_t* codes, uint8_t* scales, const float* tensor_scale, int mode,
-                           hipStream_t stream) {
+                           uint8_t* codes, uint8_t* scales, const float* tensor_scale,
+                           const QuantOptions& opt, hipStream_t stream) {
   if (rows * (k / kBlock) == 0) return hipSuccess;
-  if (mode == kForceE2M1)
-    return launch_mode<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
-  if (mode == kForceE1M2)
-    return launch_mode<kForceE1M2>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
-  return launch_mode<kSelect>(x, rows, k, ldx, codes, scales, tensor_scale, stream);
+  if (opt.mode == kForceE2M1)
+    return launch_mode_opts<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
+  if (opt.mode == kForceE1M2)
+    return launch_mode_opts<kForceE1M2>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
+  return launch_mode_opts<kSelect>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
+}
+
+hipError_t launch_hadamard(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                           const HadamardParams& hp, uint16_t* y, hipStream_t stream) {
+  const int64_t nbk = k / kBlock, nblocks = rows * nbk;
+  if (nblocks == 0) return hipSuccess;
+  static int64_t cache_c[64], cache_s[64];
+  const int64_t resident = ldx == k ? resident_groups(hadamard_kernel<true>, cache_c)
+                                    : resident_groups(hadamard_kernel<false>, cache_s);
+  const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
+  const int g = (int)(wanted < resident ? wanted : resident);
+  if (ldx == k)
+    hadamard_kernel<true><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, hp, y);
+  else
+    hadamard_kernel<false><<<g, kThreads, 0, stream>>>(x, nbk, ldx, nblocks, hp, y);
+  return hipGetLastError();
 }
 
 }  // namespace mixfp4

@@ -55,7 +55,8 @@ def q(lib, x=A16, rows=4, k=32, ldx=32, codes=A16, scales=A16, ts=A16, flags=0):
 def test_quantize_rejects(lib):
     assert q(lib, flags=7) == 4          # both FORCE bits (with GIVEN)
     assert q(lib, flags=6) == 4          # both FORCE bits
-    assert q(lib, flags=8) == 4          # unknown bit
+    assert q(lib, flags=8) == 4          # STOCHASTIC needs mixfp4_quantize_ex
+    assert q(lib, flags=16) == 4         # unknown bit
     assert q(lib, flags=0x80000002) == 4
     assert q(lib, k=24) == 2
     assert q(lib, k=-16) == 2
@@ -97,3 +98,36 @@ def test_gemm_rejects(lib):
     assert f(*args(c=P(0x10002))) == 3
     assert f(*args(ats=P(0x10002))) == 3
     assert f(*args(m=0, ac=P(0), c=P(0))) == 0                # empty output: no-op
+
+
+def qx(lib, x=A16, rows=4, k=256, ldx=256, codes=A16, scales=A16, ts=A16, flags=0, block=0,
+       signs=None, seed=0, offset=0):
+    return lib.mixfp4_quantize_ex(x, rows, k, ldx, codes, scales, ts, flags, block, signs, seed,
+                                  offset, None)
+
+
+def test_quantize_ex_rejects(lib):
+    assert qx(lib, flags=16) == 4
+    assert qx(lib, flags=6 | 8) == 4
+    for bad in (8, 48, 512, -16, 1):
+        assert qx(lib, block=bad) == 2, bad
+    assert qx(lib, k=96, ldx=96, block=64) == 2       # block does not divide k
+    assert qx(lib, k=24, ldx=24) == 2
+    assert qx(lib, x=P(0), block=16) == 1
+    assert qx(lib, ts=P(0), flags=8) == 1
+    assert qx(lib, codes=P(0x10008), block=128) == 3
+    # empty input in GIVEN mode: nothing to launch, success
+    assert qx(lib, rows=0, flags=1 | 8, block=256) == 0
+
+
+def test_hadamard_rejects(lib):
+    f = lib.mixfp4_hadamard
+    for bad in (0, 8, 24, 512):
+        assert f(A16, 2, 256, 256, bad, None, A16, None) == 2, bad
+    assert f(A16, 2, 96, 96, 64, None, A16, None) == 2
+    assert f(A16, 2, 128, 120, 16, None, A16, None) == 2   # ldx < k
+    assert f(A16, 2, 128, 132, 16, None, A16, None) == 2   # ldx % 8
+    assert f(P(0), 2, 128, 128, 16, None, A16, None) == 1
+    assert f(A16, 2, 128, 128, 16, None, P(0), None) == 1
+    assert f(A16, 2, 128, 128, 16, None, P(0x10008), None) == 3
+    assert f(A16, 0, 128, 128, 16, None, P(0), None) == 0     # empty: nothing to do

@@ -172,3 +172,13 @@ def test_on_grid_values_are_fixed():
     for seed in range(4):
         qs = Q.quantize(bits, s32=1.0, mode="e2m1", rounding="stochastic", seed=seed)
         assert np.array_equal(qn.codes, qs.codes)
+
+
+def test_row_index_matches_full_tensor():
+    """Rows quantized on their own with their global row numbers get the
+    codes they get inside the whole tensor."""
+    bits = W.adversarial(31, 40, 96)
+    full = Q.quantize(bits, s32=0.5, rounding="stochastic", seed=9, offset=2)
+    rows = np.array([0, 7, 39])
+    part = Q.quantize(bits[rows], s32=0.5, rounding="stochastic", seed=9, offset=2, row_index=rows)
+    assert np.array_equal(part.codes, full.codes[rows])
