@@ -57,6 +57,8 @@ typedef enum {
 #define MIXFP4_FORCE_E1M2 4u    /* E1M2 x2 only (T = 1): INT4 codes           */
 /* Stochastic rounding of the codes (App. D); mixfp4_quantize_ex only.      */
 #define MIXFP4_STOCHASTIC 8u
+/* Quantize X^T (blocks of 16 consecutive rows of X); mixfp4_quantize_ex only.*/
+#define MIXFP4_TRANSPOSE 16u
 
 /*
  * mixfp4_quantize - Algorithm 1 ("MixFP4 data type quantization") on a bf16
@@ -100,11 +102,19 @@ int mixfp4_quantize(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
  *
  *   x ... tensor_scale  as for mixfp4_quantize; with a rotation, COMPUTE
  *                mode takes s32 from the rotated tensor (two passes over X).
- *   flags        as for mixfp4_quantize, plus MIXFP4_STOCHASTIC.
+ *   flags        as for mixfp4_quantize, plus MIXFP4_STOCHASTIC and
+ *                MIXFP4_TRANSPOSE.
  *   hadamard_block  0 (no rotation) or b in {16, 32, 64, 128, 256} with
  *                k % b == 0: X is first replaced by the bf16 result of
  *                mixfp4_hadamard(X, b, hadamard_signs), bit for bit, and
  *                that tensor is quantized.  Anything else: MIXFP4_ERR_SHAPE.
+ *
+ * MIXFP4_TRANSPOSE quantizes X^T (the operands of the weight-gradient GEMM
+ * dW = dY^T X, which reduces over the token rows): the result is exactly
+ * that of this call on the contiguous transpose of X [rows, k] (rotation,
+ * rounding, stochastic draws and s32 included), without forming it.  Then
+ * rows % 16 == 0, codes is [k, rows/2] and scales is [k, rows/16]; a rotation
+ * runs along the rows and needs b <= 64 with rows % b == 0.
  *   hadamard_signs  device array of b bytes (bit 7 set = -1) or NULL.
  *   seed, offset Philox4x32-10 (Salmon et al., SC 2011) key and the high
  *                64 bits of its counter; block g = row * k/16 + column block
@@ -127,6 +137,27 @@ int mixfp4_quantize_ex(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
                        unsigned flags, int32_t hadamard_block,
                        const int8_t *hadamard_signs, uint64_t seed,
                        uint64_t offset, void *stream);
+
+/*
+ * mixfp4_quantize_2d - 2D block quantization of a weight W [rows, k], as the
+ * FP4 training recipe the paper follows does for weights (Sec. 3.2, Fig. 7;
+ * Sec. 4.3): Algorithm 1 with the block being a 16 x 16 tile of W (one
+ * block maximum, one pair of candidate scales, one error comparison over the
+ * 256 elements, one T); the tensor scale as in mixfp4_quantize.  The result
+ * is written in the MixFP4 layout of W and, if codes_t is not NULL, of W^T:
+ *   codes [rows, k/2], scales [rows, k/16]    (each tile's scale byte on
+ *                                              each of its 16 rows)
+ *   codes_t [k, rows/2], scales_t [k, rows/16]
+ * so FPROP (A W^T: mixfp4_gemm(A, W)) and DGRAD (dY W: mixfp4_gemm(dY, W^T))
+ * read the same quantized values.  rows % 16 == 0, k % 16 == 0, ldw as ldx
+ * of mixfp4_quantize; codes and codes_t 16-byte aligned; codes_t and
+ * scales_t both NULL or both given.  flags: MIXFP4_SCALE_COMPUTE/GIVEN and
+ * at most one FORCE flag.  Bit-identical to the CPU oracle.
+ */
+int mixfp4_quantize_2d(const uint16_t *w, int64_t rows, int64_t k, int64_t ldw,
+                       uint8_t *codes, uint8_t *scales, uint8_t *codes_t,
+                       uint8_t *scales_t, float *tensor_scale, unsigned flags,
+                       void *stream);
 
 /*
  * mixfp4_hadamard - block-diagonal (random) Hadamard transform along k, the
@@ -195,7 +226,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 102
+#define MIXFP4_ABI_VERSION 103
 
 #ifdef __cplusplus
 }

@@ -104,6 +104,47 @@ MODES = ("select", "e2m1", "e1m2")
 ROUNDINGS = ("nearest", "stochastic")
 
 
+def _algorithm1_blocks(xb: np.ndarray, mode: str):
+    """Algorithm 1 after the tensor scale, on blocks ``xb`` = |X_FP8| of shape
+    [..., L] (fp32; L = 16 for the 1D format, 256 for a 16x16 tile):
+    candidate scales, both grids, the exact error comparison and the choice.
+    Returns the E4M3 codes of both candidate scales, both code arrays, both
+    fp32 quotients, the exact Err_E2M1 - Err_E1M2 and T."""
+    L = xb.shape[-1]
+    bm = xb.max(axis=-1)                                    # block-max |X_FP8|
+
+    def branch(divisor, grid):
+        cand = (bm / np.float32(divisor)).astype(np.float32)
+        code = F.e4m3_encode(cand.astype(np.float64))
+        s8 = F.e4m3_decode(code)                            # exact float64
+        s8_32 = s8.astype(np.float32)
+        with np.errstate(divide="ignore", invalid="ignore"):
+            y = np.where(s8_32[..., None] > 0, xb / s8_32[..., None], np.float32(0)).astype(np.float32)
+        q = F.round_to_codebook(y.astype(np.float64), grid)
+        d = grid[q] * s8[..., None]                          # dequantized, exact in fp64
+        return code, s8, q, d, y
+
+    cf, sf, qf, df, yf = branch(6, F.F_GRID)
+    ci, si, qi, di, yi = branch(7, F.I_GRID)
+
+    # Err_E2M1 - Err_E1M2 = sum((x - Df)^2 - (x - Di)^2) = sum((Di - Df) * (2x - Df - Di)).
+    # Each term is exact in fp64; the block sum is certified exact or redone
+    # with rationals.
+    xd = xb.astype(np.float64)
+    terms = (di - df) * ((2.0 * xd - df) - di)
+    delta, ok = _exact_block_sums(terms.reshape(-1, L))
+    if not ok.all():
+        flat_terms = terms.reshape(-1, L)
+        for i in np.flatnonzero(~ok):
+            exact = _fraction_sum(flat_terms[i])
+            delta[i] = 0.0 if exact == 0 else (1.0 if exact > 0 else -1.0) * max(abs(float(exact)), 5e-324)
+    delta = delta.reshape(bm.shape)
+    t = (~(delta < 0)).astype(np.uint8)                    # E2M1 iff Err_E2M1 < Err_E1M2
+    if mode != "select":
+        t = np.full_like(t, 0 if mode == "e2m1" else 1)
+    return cf, ci, qf, qi, yf, yi, delta, t
+
+
 def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str = "nearest",
              seed: int = 0, offset: int = 0, row_index=None) -> Quantized:
     """Algorithm 1 on a bf16 tensor ``x_bits`` (uint16 [rows, K], K % 16 == 0).
@@ -133,37 +174,7 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str =
     x = (X / s32).astype(np.float32)                       # X_FP8, IEEE fp32 division
     nb = k // BLOCK
     xb = np.abs(x).reshape(rows, nb, BLOCK)
-    bm = xb.max(axis=-1)                                    # block-max |X_FP8|
-
-    def branch(divisor, grid):
-        cand = (bm / np.float32(divisor)).astype(np.float32)
-        code = F.e4m3_encode(cand.astype(np.float64))
-        s8 = F.e4m3_decode(code)                            # exact float64
-        s8_32 = s8.astype(np.float32)
-        with np.errstate(divide="ignore", invalid="ignore"):
-            y = np.where(s8_32[..., None] > 0, xb / s8_32[..., None], np.float32(0)).astype(np.float32)
-        q = F.round_to_codebook(y.astype(np.float64), grid)
-        d = grid[q] * s8[..., None]                          # dequantized, exact in fp64
-        return code, s8, q, d, y
-
-    cf, sf, qf, df, yf = branch(6, F.F_GRID)
-    ci, si, qi, di, yi = branch(7, F.I_GRID)
-
-    # Err_E2M1 - Err_E1M2 = sum((x - Df)^2 - (x - Di)^2) = sum((Di - Df) * (2x - Df - Di)).
-    # Each term is exact in fp64; the block sum is certified exact or redone
-    # with rationals.
-    xd = xb.astype(np.float64)
-    terms = (di - df) * ((2.0 * xd - df) - di)
-    delta, ok = _exact_block_sums(terms.reshape(-1, BLOCK))
-    if not ok.all():
-        flat_terms = terms.reshape(-1, BLOCK)
-        for i in np.flatnonzero(~ok):
-            exact = _fraction_sum(flat_terms[i])
-            delta[i] = 0.0 if exact == 0 else (1.0 if exact > 0 else -1.0) * max(abs(float(exact)), 5e-324)
-    delta = delta.reshape(rows, nb)
-    t = (~(delta < 0)).astype(np.uint8)                    # E2M1 iff Err_E2M1 < Err_E1M2
-    if mode != "select":
-        t = np.full_like(t, 0 if mode == "e2m1" else 1)
+    cf, ci, qf, qi, yf, yi, delta, t = _algorithm1_blocks(xb, mode)
 
     sign = (x_bits.reshape(rows, nb, BLOCK) >> 15).astype(np.uint8)
     if rounding == "stochastic":
@@ -220,3 +231,51 @@ def dequantize_exact(codes, scales, s32=None) -> np.ndarray:
     unit = decode_unit(codes, scales)
     s = 1.0 if s32 is None else float(np.float32(s32))
     return unit * s
+
+
+@dataclass
+class Quantized2D:
+    """A weight quantized in 16x16 tiles, in both K-major layouts."""
+    codes: np.ndarray      # uint8 [N, K/2]   (W, blocks along K)
+    scales: np.ndarray     # uint8 [N, K/16]  (each tile's byte on its 16 rows)
+    codes_t: np.ndarray    # uint8 [K, N/2]   (W^T, blocks along N)
+    scales_t: np.ndarray   # uint8 [K, N/16]
+    s32: np.float32
+    t: np.ndarray          # uint8 [N/16, K/16]
+    tile_scales: np.ndarray  # uint8 [N/16, K/16] scale bytes
+
+
+def _pack(nib: np.ndarray) -> np.ndarray:
+    return (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
+
+
+def quantize_2d(x_bits: np.ndarray, s32=None, mode: str = "select") -> Quantized2D:
+    """2D block quantization of a weight W (uint16 bf16 [N, K], N and K
+    multiples of 16): Algorithm 1 with the block being a 16 x 16 tile of W
+    (one block max, one pair of candidate scales, one error comparison over
+    the 256 elements, one T), as the FP4 training recipe the paper follows
+    does for weights (Sec. 3.2, Fig. 7; Sec. 4.3).  The tensor scale is
+    Algorithm 1's.  The result is written in the 1D MixFP4 layout twice:
+    for W (blocks of 16 along K, the tile's scale byte repeated on its 16
+    rows) and for W^T (blocks of 16 along N), so both FPROP (A W^T) and
+    DGRAD (dY W = dY (W^T)^T) read it as an ordinary operand, and the two
+    dequantize to exact transposes of each other."""
+    assert mode in MODES
+    x_bits = np.ascontiguousarray(x_bits, dtype=np.uint16)
+    n, k = x_bits.shape
+    assert n % BLOCK == 0 and k % BLOCK == 0
+    s32 = tensor_scale(x_bits) if s32 is None else np.float32(s32)
+    x = (bf16_to_f32(x_bits) / s32).astype(np.float32)
+    tn, tk = n // BLOCK, k // BLOCK
+    # tiles[a, b, 16 i + j] = x[16 a + i, 16 b + j]
+    tiles = np.abs(x).reshape(tn, BLOCK, tk, BLOCK).transpose(0, 2, 1, 3).reshape(tn, tk, BLOCK * BLOCK)
+    cf, ci, qf, qi, _, _, _, t = _algorithm1_blocks(tiles, mode)
+    mag = np.where(t[..., None] == 1, qi, qf).astype(np.uint8)
+    mag = mag.reshape(tn, tk, BLOCK, BLOCK).transpose(0, 2, 1, 3).reshape(n, k)
+    nib = ((x_bits >> 15).astype(np.uint8) << 3) | mag
+    tile_scales = ((t << 7) | np.where(t == 1, ci, cf)).astype(np.uint8)
+    scales = np.repeat(tile_scales, BLOCK, axis=0)                       # [N, K/16]
+    scales_t = np.repeat(tile_scales.T, BLOCK, axis=0)                   # [K, N/16]
+    return Quantized2D(codes=_pack(nib), scales=scales, codes_t=_pack(np.ascontiguousarray(nib.T)),
+                       scales_t=np.ascontiguousarray(scales_t), s32=s32, t=t,
+                       tile_scales=tile_scales)

@@ -10,6 +10,9 @@ Functions (same names as the C ABI in include/mixfp4.h):
                   seed=0, offset=0, hadamard_block=0, hadamard_signs=None)
       -> (codes, scales, s32)   (the C call is mixfp4_quantize_ex when
                                   rotating or rounding stochastically)
+  mixfp4_quantize(..., transpose=True) quantizes X^T (WGRAD operands)
+  mixfp4_quantize_2d(w, tensor_scale=None, mode="mixfp4", transposed=True)
+      -> (codes, scales, s32) for W and (codes_t, scales_t, s32) for W^T
   mixfp4_hadamard(x, block, signs=None) -> bf16 tensor
   mixfp4_dequantize(codes, scales, tensor_scale=None) -> fp32 tensor
   mixfp4_gemm(a, w) -> C = A W^T (fp32), a/w are (codes, scales, s32) triples
@@ -25,13 +28,14 @@ from ._lib import LIB_PATH, MixFP4Error, lib
 
 __all__ = ["mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_hadamard", "mixfp4_dequantize",
            "mixfp4_gemm", "MixFP4Error", "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN",
-           "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC"]
+           "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC", "TRANSPOSE", "mixfp4_quantize_2d"]
 
 SCALE_COMPUTE = 0
 SCALE_GIVEN = 1
 FORCE_E2M1 = 2
 FORCE_E1M2 = 4
 STOCHASTIC = 8
+TRANSPOSE = 16
 _MODES = {"mixfp4": 0, "e2m1": FORCE_E2M1, "e1m2": FORCE_E1M2}
 
 
@@ -55,7 +59,8 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
                     codes: torch.Tensor | None = None, scales: torch.Tensor | None = None,
                     scale_out: torch.Tensor | None = None, mode: str = "mixfp4",
                     rounding: str = "nearest", seed: int = 0, offset: int = 0,
-                    hadamard_block: int = 0, hadamard_signs: torch.Tensor | None = None):
+                    hadamard_block: int = 0, hadamard_signs: torch.Tensor | None = None,
+                    transpose: bool = False):
     """Quantize a bf16 [rows, k] CUDA tensor (Algorithm 1).
 
     ``tensor_scale`` None computes s32 = max|X| / 2688 on the device (into
@@ -65,7 +70,10 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
     writes the codes by App. D's stochastic rounding with Philox draws of
     (``seed``, ``offset``).  ``hadamard_block`` b > 0 rotates X first
     (mixfp4_hadamard with ``hadamard_signs``, an int8 CUDA tensor of b signs).
-    Returns (codes uint8 [rows, k/2], scales uint8 [rows, k/16], s32 fp32 [1])."""
+    ``transpose`` quantizes X^T instead (blocks of 16 rows of X; a rotation
+    then runs along the rows).
+    Returns (codes uint8 [rows, k/2], scales uint8 [rows, k/16], s32 fp32 [1]),
+    or [k, rows/2] and [k, rows/16] with ``transpose``."""
     if mode not in _MODES:
         raise ValueError(f"mode must be one of {sorted(_MODES)}")
     if rounding not in ("nearest", "stochastic"):
@@ -76,10 +84,11 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
         raise ValueError("x must have unit stride along K")
     rows, k = x.shape
     dev = x.device
+    orows, ok = (k, rows) if transpose else (rows, k)
     if codes is None:
-        codes = torch.empty((rows, k // 2), dtype=torch.uint8, device=dev)
+        codes = torch.empty((orows, ok // 2), dtype=torch.uint8, device=dev)
     if scales is None:
-        scales = torch.empty((rows, k // 16), dtype=torch.uint8, device=dev)
+        scales = torch.empty((orows, ok // 16), dtype=torch.uint8, device=dev)
     if tensor_scale is None:
         ts = scale_out if scale_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
         flags = SCALE_COMPUTE
@@ -88,12 +97,14 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
         flags = SCALE_GIVEN
     flags |= _MODES[mode]
     ldx = x.stride(0) if rows > 0 else k
-    if rounding == "nearest" and hadamard_block == 0:
+    if rounding == "nearest" and hadamard_block == 0 and not transpose:
         st = lib.mixfp4_quantize(_ptr(x), rows, k, ldx, _ptr(codes), _ptr(scales), _ptr(ts),
                                  flags, _stream(dev))
     else:
         if rounding == "stochastic":
             flags |= STOCHASTIC
+        if transpose:
+            flags |= TRANSPOSE
         signs = _signs_arg(hadamard_signs, hadamard_block)
         st = lib.mixfp4_quantize_ex(_ptr(x), rows, k, ldx, _ptr(codes), _ptr(scales), _ptr(ts),
                                     flags, hadamard_block, _ptr(signs),
@@ -113,6 +124,35 @@ def _signs_arg(signs, block):
             or signs.numel() != block:
         raise ValueError("hadamard signs must be a contiguous int8 CUDA tensor of `block` entries")
     return signs
+
+
+def mixfp4_quantize_2d(w: torch.Tensor, tensor_scale: torch.Tensor | None = None,
+                       mode: str = "mixfp4", transposed: bool = True,
+                       scale_out: torch.Tensor | None = None):
+    """2D (16 x 16 tile) quantization of a bf16 weight [n, k] (n, k multiples
+    of 16).  Returns ((codes, scales, s32) of W, (codes_t, scales_t, s32) of
+    W^T or None): mixfp4_gemm(A, W-part) is FPROP, mixfp4_gemm(dY, W^T-part)
+    is DGRAD."""
+    if mode not in _MODES:
+        raise ValueError(f"mode must be one of {sorted(_MODES)}")
+    if w.dtype != torch.bfloat16 or w.dim() != 2 or not w.is_cuda or w.stride(1) != 1:
+        raise ValueError("w must be a 2-D bfloat16 CUDA tensor with unit stride along K")
+    n, k = w.shape
+    dev = w.device
+    codes = torch.empty((n, k // 2), dtype=torch.uint8, device=dev)
+    scales = torch.empty((n, k // 16), dtype=torch.uint8, device=dev)
+    codes_t = torch.empty((k, n // 2), dtype=torch.uint8, device=dev) if transposed else None
+    scales_t = torch.empty((k, n // 16), dtype=torch.uint8, device=dev) if transposed else None
+    if tensor_scale is None:
+        ts = scale_out if scale_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
+        flags = SCALE_COMPUTE
+    else:
+        ts, flags = tensor_scale, SCALE_GIVEN
+    st = lib.mixfp4_quantize_2d(_ptr(w), n, k, w.stride(0) if n > 0 else k, _ptr(codes),
+                                _ptr(scales), _ptr(codes_t), _ptr(scales_t), _ptr(ts),
+                                flags | _MODES[mode], _stream(dev))
+    _check(st)
+    return (codes, scales, ts), ((codes_t, scales_t, ts) if transposed else None)
 
 
 def mixfp4_hadamard(x: torch.Tensor, block: int, signs: torch.Tensor | None = None,

@@ -13,7 +13,8 @@ import torch  # noqa: F401  (loads the HIP runtime the library binds to)
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmixfp4.so")
 
-SYMBOLS = ("mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_hadamard", "mixfp4_dequantize",
+SYMBOLS = ("mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_quantize_2d", "mixfp4_hadamard",
+           "mixfp4_dequantize",
            "mixfp4_gemm", "mixfp4_status_string", "mixfp4_last_launch_error",
            "mixfp4_abi_version")
 
@@ -34,6 +35,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     u64 = ctypes.c_uint64
     h.mixfp4_quantize_ex.argtypes = [vp, i64, i64, i64, vp, vp, vp, u32, i32, vp, u64, u64, vp]
     h.mixfp4_quantize_ex.restype = i32
+    h.mixfp4_quantize_2d.argtypes = [vp, i64, i64, i64, vp, vp, vp, vp, vp, u32, vp]
+    h.mixfp4_quantize_2d.restype = i32
     h.mixfp4_hadamard.argtypes = [vp, i64, i64, i64, i32, vp, vp, vp]
     h.mixfp4_hadamard.restype = i32
     h.mixfp4_dequantize.argtypes = [vp, vp, vp, i64, i64, vp, vp]

@@ -20,7 +20,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmixfp4.so")
-SOURCES = ["api.cpp", "quantize.hip", "dequantize.hip", "gemm.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "quantize2d.hip", "dequantize.hip", "gemm.hip"]
 
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")

@@ -26,8 +26,8 @@ bool valid_hadamard_block(int32_t b) {
 int quantize_impl(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
                   uint8_t* scales, float* tensor_scale, unsigned flags, int32_t hadamard_block,
                   const int8_t* hadamard_signs, uint64_t seed, uint64_t offset, void* stream) {
-  const unsigned known =
-      MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2 | MIXFP4_STOCHASTIC;
+  const unsigned known = MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2 |
+                         MIXFP4_STOCHASTIC | MIXFP4_TRANSPOSE;
   if ((flags & ~known) != 0u ||
       (flags & (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) == (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2))
     return MIXFP4_ERR_FLAGS;
@@ -36,10 +36,17 @@ int quantize_impl(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8
   opt.mode = (flags & MIXFP4_FORCE_E2M1) ? 1 : (flags & MIXFP4_FORCE_E1M2) ? 2 : 0;
   opt.sr = (flags & MIXFP4_STOCHASTIC) != 0u;
   opt.srp = {(uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)offset, (uint32_t)(offset >> 32)};
+  const bool transpose = (flags & MIXFP4_TRANSPOSE) != 0u;
   if (rows < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;
   if (rows > 0 && (ldx < k || (ldx % 8) != 0)) return MIXFP4_ERR_SHAPE;
+  if (transpose && (rows % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;
   if (hadamard_block != 0) {
-    if (!valid_hadamard_block(hadamard_block) || (k % hadamard_block) != 0) return MIXFP4_ERR_SHAPE;
+    // the rotation runs along the quantized dimension: k, or the rows of X
+    // for a transposed quantization (there at most 64, one lane quad)
+    const int64_t along = transpose ? rows : k;
+    if (!valid_hadamard_block(hadamard_block) || (along % hadamard_block) != 0 ||
+        (transpose && hadamard_block > 64))
+      return MIXFP4_ERR_SHAPE;
     opt.had = true;
     opt.hp = mixfp4::hadamard_params(hadamard_block, hadamard_signs);
   }
@@ -50,6 +57,23 @@ int quantize_impl(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8
   if (!empty && (!aligned(x, 16) || !aligned(codes, 16))) return MIXFP4_ERR_ALIGN;
   hipStream_t s = static_cast<hipStream_t>(stream);
   (void)hipGetLastError();   // drop stale errors so a launch failure is ours
+  if (transpose) {
+    if (empty) {
+      if (given) return MIXFP4_OK;
+      return launch_status(mixfp4::launch_tensor_scale(x, 0, k, ldx, nullptr, 0, tensor_scale, s));
+    }
+    const int64_t nscr = rows * (k / mixfp4::kBlock);
+    if (!given) {
+      const hipError_t e =
+          opt.had ? mixfp4::launch_tensor_scale_t_rotated(x, rows, k, ldx, opt.hp, scales, nscr,
+                                                          tensor_scale, s)
+                  : mixfp4::launch_tensor_scale(x, rows, k, ldx, scales, nscr, tensor_scale, s);
+      const int st = launch_status(e);
+      if (st != MIXFP4_OK) return st;
+    }
+    return launch_status(
+        mixfp4::launch_quantize_t(x, rows, k, ldx, codes, scales, tensor_scale, opt, s));
+  }
   if (!given && !empty && !opt.had && mixfp4::quantize_is_small(rows, k))
     return launch_status(mixfp4::launch_quantize_small(x, rows, k, ldx, codes, scales,
                                                        tensor_scale, opt, s));
@@ -90,7 +114,8 @@ const char* mixfp4_last_launch_error(void) { return g_last_launch_error; }
 
 int mixfp4_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
                     uint8_t* scales, float* tensor_scale, unsigned flags, void* stream) {
-  if (flags & MIXFP4_STOCHASTIC) return MIXFP4_ERR_FLAGS;   // needs the seed of _ex
+  // stochastic rounding needs the seed of _ex; transposition is an _ex option
+  if (flags & (MIXFP4_STOCHASTIC | MIXFP4_TRANSPOSE)) return MIXFP4_ERR_FLAGS;
   return quantize_impl(x, rows, k, ldx, codes, scales, tensor_scale, flags, 0, nullptr, 0, 0,
                        stream);
 }
@@ -101,6 +126,37 @@ int mixfp4_quantize_ex(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, 
                        uint64_t offset, void* stream) {
   return quantize_impl(x, rows, k, ldx, codes, scales, tensor_scale, flags, hadamard_block,
                        hadamard_signs, seed, offset, stream);
+}
+
+int mixfp4_quantize_2d(const uint16_t* w, int64_t rows, int64_t k, int64_t ldw, uint8_t* codes,
+                       uint8_t* scales, uint8_t* codes_t, uint8_t* scales_t, float* tensor_scale,
+                       unsigned flags, void* stream) {
+  if ((flags & ~(MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) != 0u ||
+      (flags & (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) == (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2))
+    return MIXFP4_ERR_FLAGS;
+  const bool given = (flags & MIXFP4_SCALE_GIVEN) != 0u;
+  const int mode = (flags & MIXFP4_FORCE_E2M1) ? 1 : (flags & MIXFP4_FORCE_E1M2) ? 2 : 0;
+  if (rows < 0 || k < 0 || (k % mixfp4::kBlock) != 0 || (rows % mixfp4::kBlock) != 0)
+    return MIXFP4_ERR_SHAPE;
+  if (rows > 0 && (ldw < k || (ldw % 8) != 0)) return MIXFP4_ERR_SHAPE;
+  if (!tensor_scale) return MIXFP4_ERR_NULL;
+  if ((codes_t == nullptr) != (scales_t == nullptr)) return MIXFP4_ERR_NULL;
+  const bool empty = rows == 0 || k == 0;
+  if (!empty && (!w || !codes || !scales)) return MIXFP4_ERR_NULL;
+  if (!aligned(tensor_scale, 4)) return MIXFP4_ERR_ALIGN;
+  if (!empty && (!aligned(w, 16) || !aligned(codes, 16) || (codes_t && !aligned(codes_t, 16))))
+    return MIXFP4_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  if (!given) {
+    const int st = launch_status(mixfp4::launch_tensor_scale(
+        w, empty ? 0 : rows, k, ldw, empty ? nullptr : scales,
+        empty ? 0 : rows * (k / mixfp4::kBlock), tensor_scale, s));
+    if (st != MIXFP4_OK) return st;
+  }
+  if (empty) return MIXFP4_OK;
+  return launch_status(mixfp4::launch_quantize_2d(w, rows, k, ldw, codes, scales, codes_t,
+                                                  scales_t, tensor_scale, mode, s));
 }
 
 int mixfp4_hadamard(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, int32_t block,

@@ -28,25 +28,9 @@
 #include <stdint.h>
 
 #include "internal.h"
+#include "lanes.h"
 
 namespace mixfp4 {
-
-template <int kCtrl>
-__device__ __forceinline__ double dpp_f64(double v) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, kCtrl, 0xF, 0xF, false);
-  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), kCtrl, 0xF, 0xF, false);
-  return __builtin_bit_cast(double, ((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo);
-}
-
-// Value of lane (lane ^ kX) within a 16-lane row, kX in {1, 2, 4, 8}.
-template <int kX>
-__device__ __forceinline__ double lane_xor(double v) {
-  if constexpr (kX == 1) return dpp_f64<0xB1>(v);            // quad_perm [1,0,3,2]
-  if constexpr (kX == 2) return dpp_f64<0x4E>(v);            // quad_perm [2,3,0,1]
-  if constexpr (kX == 4) return dpp_f64<0x1B>(dpp_f64<0x141>(v));   // half mirror, quad reverse
-  return dpp_f64<0x128>(v);                                   // row_ror:8
-}
 
 // One butterfly stage across lanes: the lane with bit kX clear keeps
 // own + partner, the other partner - own (fma with +-1: one rounding, exact
@@ -55,7 +39,7 @@ template <int kX>
 __device__ __forceinline__ void cross_stage(double (&v)[16], int lane) {
   const double sg = (lane & kX) ? -1.0 : 1.0;
 #pragma unroll
-  for (int j = 0; j < 16; ++j) v[j] = __builtin_fma(v[j], sg, lane_xor<kX>(v[j]));
+  for (int j = 0; j < 16; ++j) v[j] = __builtin_fma(v[j], sg, xor_f64<kX>(v[j]));
 }
 
 // Round y = S * scale to bf16 (see the header comment); returns the bits.

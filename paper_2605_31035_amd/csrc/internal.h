@@ -58,6 +58,24 @@ hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k,
                                  int64_t ldx, uint8_t* codes, uint8_t* scales,
                                  float* tensor_scale, const QuantOptions& opt,
                                  hipStream_t stream);
+// 2D (16 x 16 tile) quantization of W [n, k] (n, k multiples of 16) into
+// the W layout and, when codes_t is not NULL, the W^T layout; mode as above.
+hipError_t launch_quantize_2d(const uint16_t* w, int64_t n, int64_t k, int64_t ldw,
+                              uint8_t* codes, uint8_t* scales, uint8_t* codes_t,
+                              uint8_t* scales_t, const float* tensor_scale, int mode,
+                              hipStream_t stream);
+// Quantization of X^T for a row-major X [rows, k] (rows % 16 == 0): codes_t
+// [k, rows/2], scales_t [k, rows/16]; rotation (opt.had) along the rows with
+// b <= 64.
+hipError_t launch_quantize_t(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                             uint8_t* codes_t, uint8_t* scales_t, const float* tensor_scale,
+                             const QuantOptions& opt, hipStream_t stream);
+// s32 of the rotated X^T (COMPUTE mode with opt.had and TRANSPOSE); scratch
+// as for launch_tensor_scale.
+hipError_t launch_tensor_scale_t_rotated(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                                         const HadamardParams& hp, uint8_t* scratch,
+                                         int64_t scratch_bytes, float* tensor_scale,
+                                         hipStream_t stream);
 // Standalone rotation: y [rows, k] contiguous bf16.
 hipError_t launch_hadamard(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
                            const HadamardParams& hp, uint16_t* y, hipStream_t stream);

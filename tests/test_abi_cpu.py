@@ -56,7 +56,8 @@ def test_quantize_rejects(lib):
     assert q(lib, flags=7) == 4          # both FORCE bits (with GIVEN)
     assert q(lib, flags=6) == 4          # both FORCE bits
     assert q(lib, flags=8) == 4          # STOCHASTIC needs mixfp4_quantize_ex
-    assert q(lib, flags=16) == 4         # unknown bit
+    assert q(lib, flags=16) == 4         # TRANSPOSE is a mixfp4_quantize_ex option
+    assert q(lib, flags=32) == 4         # unknown bit
     assert q(lib, flags=0x80000002) == 4
     assert q(lib, k=24) == 2
     assert q(lib, k=-16) == 2
@@ -107,8 +108,11 @@ def qx(lib, x=A16, rows=4, k=256, ldx=256, codes=A16, scales=A16, ts=A16, flags=
 
 
 def test_quantize_ex_rejects(lib):
-    assert qx(lib, flags=16) == 4
+    assert qx(lib, flags=32) == 4
     assert qx(lib, flags=6 | 8) == 4
+    assert qx(lib, flags=16, rows=4) == 2                # transpose: rows % 16
+    assert qx(lib, flags=16, rows=256, block=128) == 2   # transposed rotation: b <= 64
+    assert qx(lib, flags=16, rows=48, block=32) == 2     # rows % b
     for bad in (8, 48, 512, -16, 1):
         assert qx(lib, block=bad) == 2, bad
     assert qx(lib, k=96, ldx=96, block=64) == 2       # block does not divide k
@@ -131,3 +135,18 @@ def test_hadamard_rejects(lib):
     assert f(A16, 2, 128, 128, 16, None, P(0), None) == 1
     assert f(A16, 2, 128, 128, 16, None, P(0x10008), None) == 3
     assert f(A16, 0, 128, 128, 16, None, P(0), None) == 0     # empty: nothing to do
+
+
+def test_quantize_2d_rejects(lib):
+    def f(w=A16, rows=32, k=64, ldw=64, codes=A16, scales=A16, ct=A16, st=A16, ts=A16, flags=0):
+        return lib.mixfp4_quantize_2d(w, rows, k, ldw, codes, scales, ct, st, ts, flags, None)
+    assert f(flags=8) == 4
+    assert f(flags=6) == 4
+    assert f(rows=24) == 2
+    assert f(k=40, ldw=40) == 2
+    assert f(ldw=60) == 2
+    assert f(ts=P(0)) == 1
+    assert f(ct=P(0)) == 1                 # codes_t and scales_t go together
+    assert f(codes=P(0)) == 1
+    assert f(ct=P(0x10008)) == 3
+    assert f(rows=0, flags=1) == 0
