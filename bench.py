@@ -22,6 +22,9 @@ Prints ONE JSON line:
                 the tensor scale computed on the device
   quantize_step the activation quantizer inside the step
   decode_shape  the memory-bound m = 16 GEMM (seed 3) against HBM
+  train_step    one training step of a 7B-class linear layer (FPROP, DGRAD,
+                WGRAD with 2D weight blocks, stochastic rounding and the
+                16-row Hadamard rotation of the WGRAD inputs; seed 5)
   cpu_baseline  the CPU oracle on a bounded sample of the same step
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
 """
@@ -245,6 +248,81 @@ def measure_decode(M, torch, dev, iters: int = 50) -> dict:
     }
 
 
+def measure_train(M, torch, dev, iters: int = 10) -> dict:
+    """One training step of a 7B-class linear layer in the flow of the paper's
+    Fig. 7 (workload train_7b, seed 5): every quantization with its tensor
+    scale computed on the device, inside the timed region.
+      FPROP  quantize X; 2D-quantize W (16x16 tiles, W and W^T layouts);
+             Y = X W^T                      [2048 x 11008 x 4096]
+      DGRAD  quantize dY (stochastic rounding); dX = dY W   [2048 x 4096 x 11008]
+      WGRAD  quantize dY^T (stochastic rounding) and X^T, both after a 16-row
+             random Hadamard rotation; dW = dY^T X          [11008 x 4096 x 2048]"""
+    import workloads as W
+    log("generating train_7b workload (seed 5)")
+    wl = W.train_7b()
+    t = {n: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+         for n, b in wl.tensors.items()}
+    del wl
+    X, Wt, dY = t["X"], t["W"], t["dY"]
+    tok, d_in = X.shape
+    d_out = Wt.shape[0]
+    signs = torch.tensor(np.where(np.random.default_rng(5).random(16) < 0.5, -1, 1)
+                         .astype(np.int8), device=dev)
+    names = ["quantize X", "quantize_2d W", "fprop gemm", "quantize dY (SR)", "dgrad gemm",
+             "quantize dY^T (RHT16, SR)", "quantize X^T (RHT16)", "wgrad gemm"]
+
+    def step(e=None, it=0):
+        def mark(i):
+            if e is not None:
+                e[i].record()
+        mark(0)
+        qx = M.mixfp4_quantize(X)
+        mark(1)
+        qw, qwt = M.mixfp4_quantize_2d(Wt)
+        mark(2)
+        M.mixfp4_gemm(qx, qw)
+        mark(3)
+        qg = M.mixfp4_quantize(dY, rounding="stochastic", seed=it)
+        mark(4)
+        M.mixfp4_gemm(qg, qwt)
+        mark(5)
+        qgt = M.mixfp4_quantize(dY, rounding="stochastic", seed=it, offset=1, hadamard_block=16,
+                                hadamard_signs=signs, transpose=True)
+        mark(6)
+        qxt = M.mixfp4_quantize(X, hadamard_block=16, hadamard_signs=signs, transpose=True)
+        mark(7)
+        M.mixfp4_gemm(qgt, qxt)
+        mark(8)
+
+    for i in range(3):
+        step(it=i)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(iters)]
+    t0 = time.perf_counter()
+    for i in range(iters):
+        step(ev[i], i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / iters
+    spans = [float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev])) for j in range(8)]
+    flops = 2.0 * tok * d_in * d_out
+    out = {
+        "workload": "train_7b: X[2048,4096] Student-t nu=4 (8 channels x50), W[11008,4096] "
+                    "N(0,0.02), dY[2048,11008] 1e-4 Student-t nu=3 (16 channels x20)",
+        "ms_per_step": round(ms, 4),
+        "gemm_TFLOPs_per_step": round(3 * flops / (ms * 1e-3) / 1e12, 2),
+        "us": {n: round(v * 1e3, 2) for n, v in zip(names, spans)},
+        "gemm_TFLOPs": {n: round(flops / (spans[j] * 1e-3) / 1e12, 1)
+                        for n, j in (("fprop", 2), ("dgrad", 4), ("wgrad", 7))},
+        "quantize_GBps": {n: round(el * QUANT_BYTES_PER_ELEM / (spans[j] * 1e-3) / 1e9, 1)
+                          for n, j, el in (("quantize_2d W (COMPUTE)", 1, d_out * d_in),
+                                           ("quantize dY^T (COMPUTE, RHT16, SR)", 5, tok * d_out),
+                                           ("quantize X^T (COMPUTE, RHT16)", 6, tok * d_in))},
+    }
+    del X, Wt, dY, t
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -255,6 +333,8 @@ def main():
                     help="skip the extra decode-shape (m = 16) measurement")
     ap.add_argument("--no-quantize-only", action="store_true",
                     help="skip the quantize-only measurement on the 2^28-element tensor")
+    ap.add_argument("--no-train", action="store_true",
+                    help="skip the training-step (FPROP/DGRAD/WGRAD) measurement")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one elementwise copy of 512 MiB (read + write of known "
                          "size) so hardware byte counters can be scaled")
@@ -357,6 +437,7 @@ def main():
                           "bytes_per_elem": QUANT_BYTES_PER_ELEM},
         "quantize": None if args.no_quantize_only else measure_quantize(M, torch, dev),
         "decode_shape": None if args.no_decode else measure_decode(M, torch, dev),
+        "train_step": None if args.no_train else measure_train(M, torch, dev),
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

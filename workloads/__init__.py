@@ -261,8 +261,31 @@ def large(seed: int = 4, tensors=("A", "W", "Q")) -> Workload:
     return wl
 
 
+def train_7b(seed: int = 5, tensors=("X", "W", "dY")) -> Workload:
+    """One linear layer of a 7B-class model in training (the flow of the
+    paper's Fig. 7): X[2048,4096] ~ Student-t(nu=4) with 8 outlier K-channels
+    x50 (as prefill_7b's A), W[11008,4096] ~ N(0,0.02), and the output
+    gradient dY[2048,11008] ~ 1e-4 * Student-t(nu=3) with 16 output channels
+    x20.  GEMMs: FPROP X W^T, DGRAD dY W, WGRAD dY^T X."""
+    ss = np.random.SeedSequence(seed)
+    sx, sxc, sw, sg, sgc = ss.spawn(5)
+    wl = Workload("train_7b", seed)
+    if "X" in tensors:
+        x = student_t(sx, 2048 * 4096, 4).reshape(2048, 4096)
+        wl.notes["outlier_channels"] = _scale_channels(x, sxc, 8, 50.0)
+        wl.tensors["X"] = f32_to_bf16_bits(x)
+    if "W" in tensors:
+        wl.tensors["W"] = f32_to_bf16_bits(normal(sw, 11008 * 4096, 0.02).reshape(11008, 4096))
+    if "dY" in tensors:
+        g = (student_t(sg, 2048 * 11008, 3) * 1e-4).astype(np.float32).reshape(2048, 11008)
+        wl.notes["grad_outlier_channels"] = _scale_channels(g, sgc, 16, 20.0)
+        wl.tensors["dY"] = f32_to_bf16_bits(g)
+    wl.gemms = [("X", "W")]
+    return wl
+
+
 WORKLOADS = {"tiny": tiny, "prefill_7b": prefill_7b, "rotated": rotated,
-             "decode": decode, "large": large}
+             "decode": decode, "large": large, "train_7b": train_7b}
 
 
 def get(name: str, **kw) -> Workload:
