@@ -34,6 +34,8 @@
 // [16 B]; the 64 lanes of a fragment read and the threads of a decode write
 // both hit consecutive 16-byte words.  Rows beyond m / n and blocks beyond k
 // decode as zeros; stores are masked.
+#include <type_traits>
+
 #include "formats.h"
 #include "internal.h"
 
@@ -334,110 +336,154 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // ---------------------------------------------------------------------------
 // Decode-shape GEMM (m <= 16): HBM-bound, W is read once.
 //
-// A workgroup of 8 waves owns 128 columns of C (16 per wave) and all of K.
-// Each lane owns one W row (column n of C) and one quarter g of every
-// 128-element K step: it loads 16 code bytes (two scale blocks) and 2 scale
-// bytes, decodes its four code dwords straight into the B operands of four
-// v_mfma_f32_16x16x32_f16, and never shares them.  The K slot (g, j) of
-// MFMA i holds element 32g + 8i + j of the step -- any order works as long as
-// A uses the same one.  A (at most 16 rows) is decoded once per workgroup, 512
-// K at a time, into a double-buffered LDS chunk laid out so that the A operand
-// of MFMA i is 64 consecutive 16-byte words.  W loads run two steps ahead.
+// A workgroup owns 64 columns of C and splits K over its kW waves (4, or 2
+// when k is not a multiple of 1024); each wave walks its K range in steps of
+// 256 with no barrier and no LDS until the end.  Lane (nn, g) = (lane % 16,
+// lane / 16) owns W rows nn + 16 c (c < 4, one per 16-column MFMA group) and
+// the quarter [64 g, 64 g + 64) of every step: per row 32 code bytes and 4
+// scale bytes, loaded one step ahead.  It decodes them straight into the B
+// operands of v_mfma_f32_16x16x32_f16, and decodes its own A operand -- A
+// row nn, the same 64 elements -- once per step for all four column groups
+// (A's decode is a quarter of W's).  MFMA i of a 32-element group takes
+// elements 8 i + j in K slot (g, j); A and W use the same order.  The waves'
+// partial sums are added through LDS in a fixed order at the end.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kSkinnyRows = 16;
-constexpr int kSkinnyWaves = 8;
-constexpr int kSkinnyCols = 16 * kSkinnyWaves;     // columns of C per workgroup
-constexpr int kSkinnyChunk = 512;                  // K per A chunk (4 wave steps)
+constexpr int kSkinnyCols = 64;                    // columns of C per workgroup
+constexpr int kSkinnyStep = 256;                   // K per wave step
+constexpr int kSkinnyVec = kSkinnyStep / 128;      // 16-byte code loads per row per lane per step
+constexpr int kSkinnySw = kSkinnyStep / 256;       // scale dwords per row per lane per step
 
 struct WPack {
-  uint4 c;       // 32 codes (two scale blocks)
-  uint32_t s;    // their two scale bytes in the low 16 bits
+  uint4 c[4][kSkinnyVec];       // 4 rows x 64 codes
+  uint32_t s[4][kSkinnySw];     // their scale bytes
+};
+struct APack {
+  uint4 c[kSkinnyVec];
+  uint32_t s[kSkinnySw];
 };
 
-__global__ __launch_bounds__(64 * kSkinnyWaves, 1) void gemm_skinny_kernel(
+template <int kW>
+__global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c) {
-  // one A chunk: 4 sub-chunks x [MFMA i (4)][quarter g (4)][row (16)] 16-byte words
-  constexpr int kAWords = (kSkinnyChunk / 128) * 4 * 4 * kSkinnyRows;   // 1024 (16 KB)
-  __shared__ uint4 abuf0[kAWords];
-  __shared__ uint4 abuf1[kAWords];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  __shared__ f32x4 red[kW - 1][4][64];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nn = lane & 15, g = lane >> 4;
   const int64_t code_pitch = k / 2, scale_pitch = k / kBlock;
-  const int64_t steps = k / 128;                    // wave steps
-  const int64_t chunks = k / kSkinnyChunk;
-
-  // this lane's W row (clamped rows only feed masked-out columns)
-  const int64_t col = (int64_t)blockIdx.x * kSkinnyCols + wave * 16 + nn;
-  const int64_t wrow = col < n ? col : n - 1;
-  const uint8_t* wc = w_codes + wrow * code_pitch + 16 * g;
-  const uint8_t* ws = w_scales + wrow * scale_pitch + 2 * g;
-  auto load_w = [&](WPack& p, int64_t step) {
-    const int64_t st = step < steps ? step : steps - 1;
-    p.c = *reinterpret_cast<const uint4*>(wc + 64 * st);
-    p.s = *reinterpret_cast<const uint16_t*>(ws + 8 * st);
-  };
-
-  // A decode: thread t owns row t/32 and block t%32 of every 512-wide chunk
-  const int ra = tid >> 5, ablk = tid & 31;
-  const int64_t arow = ra < m ? ra : m - 1;
-  const uint8_t* ac = a_codes + arow * code_pitch + 8 * ablk;
-  const uint8_t* as = a_scales + arow * scale_pitch + ablk;
-  // element offset 16*ablk within the chunk -> sub-chunk h, quarter gq, MFMA index iq
-  const int ko = 16 * ablk, h = ko >> 7, gq = (ko & 127) >> 5, iq = (ko & 31) >> 3;
-  const int adst = h * 256 + (iq * 4 + gq) * 16 + ra;
-  auto decode_a = [&](uint4* buf, int64_t chunk) {
-    const int64_t ch = chunk < chunks ? chunk : chunks - 1;
-    const uint2 cc = *reinterpret_cast<const uint2*>(ac + ch * (kSkinnyChunk / 2));
-    const BlockDec d = block_dec(as[ch * (kSkinnyChunk / kBlock)]);
-    buf[adst] = decode8(cc.x, d);
-    buf[adst + 64] = decode8(cc.y, d);            // next 8 elements: MFMA index iq + 1
-  };
-
-  f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  auto wave_step = [&](const uint4* abuf, int sub, const WPack& p) {
-    const BlockDec d0 = block_dec(p.s & 0xFFu), d1 = block_dec((p.s >> 8) & 0xFFu);
-    const uint32_t cw[4] = {p.c.x, p.c.y, p.c.z, p.c.w};
+  const int64_t kq = k / kW;                        // this wave's K range
+  const int64_t steps = kq / kSkinnyStep;
+  const int64_t kbase = wave * kq;
+  const int64_t col0 = (int64_t)blockIdx.x * kSkinnyCols;
+  const uint8_t* wc[4];
+  const uint8_t* ws[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const f16x8 fb = __builtin_bit_cast(f16x8, decode8(cw[i], i < 2 ? d0 : d1));
-      const f16x8 fa = __builtin_bit_cast(f16x8, abuf[sub * 256 + i * 64 + lane]);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa, fb, acc, 0, 0, 0);
+  for (int cg = 0; cg < 4; ++cg) {
+    int64_t r = col0 + 16 * cg + nn;
+    r = r < n ? r : n - 1;                          // clamped rows feed masked-out columns
+    wc[cg] = w_codes + r * code_pitch + kbase / 2 + (kSkinnyStep / 8) * g;
+    ws[cg] = w_scales + r * scale_pitch + kbase / 16 + (kSkinnyStep / 64) * g;
+  }
+  const int64_t arow = nn < m ? nn : m - 1;
+  const uint8_t* ac = a_codes + arow * code_pitch + kbase / 2 + (kSkinnyStep / 8) * g;
+  const uint8_t* as = a_scales + arow * scale_pitch + kbase / 16 + (kSkinnyStep / 64) * g;
+  auto load_w = [&](WPack& p, int64_t st) {
+    st = st < steps ? st : steps - 1;
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg)
+#pragma unroll
+      for (int v = 0; v < kSkinnyVec; ++v)
+        p.c[cg][v] = *reinterpret_cast<const uint4*>(wc[cg] + (kSkinnyStep / 2) * st + 16 * v);
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg)
+#pragma unroll
+      for (int v = 0; v < kSkinnySw; ++v)
+        p.s[cg][v] = *reinterpret_cast<const uint32_t*>(ws[cg] + (kSkinnyStep / 16) * st + 4 * v);
+  };
+  auto load_a = [&](APack& p, int64_t st) {
+    st = st < steps ? st : steps - 1;
+#pragma unroll
+    for (int v = 0; v < kSkinnyVec; ++v)
+      p.c[v] = *reinterpret_cast<const uint4*>(ac + (kSkinnyStep / 2) * st + 16 * v);
+#pragma unroll
+    for (int v = 0; v < kSkinnySw; ++v)
+      p.s[v] = *reinterpret_cast<const uint32_t*>(as + (kSkinnyStep / 16) * st + 4 * v);
+  };
+  f32x4 acc[4];
+#pragma unroll
+  for (int cg = 0; cg < 4; ++cg) acc[cg] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  auto compute = [&](const APack& pa, const WPack& pw) {
+#pragma unroll
+    for (int v = 0; v < kSkinnyVec; ++v) {
+      // 16-byte word v holds 32 elements = blocks 2v, 2v + 1 (scale bytes 2v, 2v + 1)
+      const uint32_t sa = pa.s[v >> 1] >> (16 * (v & 1));
+      const BlockDec da0 = block_dec(sa & 0xFFu), da1 = block_dec((sa >> 8) & 0xFFu);
+      const uint32_t ca[4] = {pa.c[v].x, pa.c[v].y, pa.c[v].z, pa.c[v].w};
+      f16x8 fa[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[i] = __builtin_bit_cast(f16x8, decode8(ca[i], i < 2 ? da0 : da1));
+#pragma unroll
+      for (int cg = 0; cg < 4; ++cg) {
+        const uint32_t sw = pw.s[cg][v >> 1] >> (16 * (v & 1));
+        const BlockDec d0 = block_dec(sw & 0xFFu), d1 = block_dec((sw >> 8) & 0xFFu);
+        const uint32_t cw[4] = {pw.c[cg][v].x, pw.c[cg][v].y, pw.c[cg][v].z, pw.c[cg][v].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const f16x8 fb = __builtin_bit_cast(f16x8, decode8(cw[i], i < 2 ? d0 : d1));
+          acc[cg] = __builtin_amdgcn_mfma_f32_16x16x32_f16(fa[i], fb, acc[cg], 0, 0, 0);
+        }
+      }
     }
   };
-
-  WPack p0, p1, p2, p3;
-  load_w(p0, 0);
-  load_w(p1, 1);
-  decode_a(abuf0, 0);
-  for (int64_t ch = 0; ch < chunks; ++ch) {
-    uint4* cur = (ch & 1) ? abuf1 : abuf0;
-    uint4* nxt = (ch & 1) ? abuf0 : abuf1;
-    __syncthreads();   // chunk `ch` of A decoded; the other buffer is free
-    decode_a(nxt, ch + 1);
-    const int64_t s0 = ch * 4;
-    load_w(p2, s0 + 2);
-    wave_step(cur, 0, p0);
-    load_w(p3, s0 + 3);
-    wave_step(cur, 1, p1);
-    load_w(p0, s0 + 4);
-    wave_step(cur, 2, p2);
-    load_w(p1, s0 + 5);
-    wave_step(cur, 3, p3);
+  // Two packs alternate: step s computes pack s % 2 after issuing the loads of
+  // step s + 1 into the other one (free since step s - 1).  The pair-unrolled
+  // loop keeps the pack indices static, so no pack is copied while its loads
+  // are in flight.
+  WPack wp[2];
+  APack ap[2];
+  load_a(ap[0], 0);
+  load_w(wp[0], 0);
+  auto step = [&](auto I_, int64_t s) {
+    constexpr int I = decltype(I_)::value;
+    __builtin_amdgcn_sched_barrier(0);
+    load_a(ap[I ^ 1], s + 1);
+    load_w(wp[I ^ 1], s + 1);
+    __builtin_amdgcn_sched_barrier(0);
+    compute(ap[I], wp[I]);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  int64_t s = 0;
+  for (; s + 1 < steps; s += 2) {
+    step(I0{}, s);
+    step(I1{}, s + 1);
   }
+  if (s < steps) step(I0{}, s);
 
-  const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
-  // 16 x 16 accumulator layout: lane holds column lane%16, register r holds row 4*(lane/16) + r
-  if (col < n) {
+  if (wave > 0) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = 4 * g + r;
-      if (row < m) c[row * n + col] = acc[r] * scale;
+    for (int cg = 0; cg < 4; ++cg) red[wave - 1][cg][lane] = acc[cg];
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) {
+      f32x4 t = acc[cg];
+#pragma unroll
+      for (int w = 0; w < kW - 1; ++w) t += red[w][cg][lane];
+      const int64_t col = col0 + 16 * cg + nn;
+      // 16 x 16 accumulator layout: lane holds column lane%16, register r holds row 4*(lane/16) + r
+      if (col < n) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int row = 4 * g + r;
+          if (row < m) c[row * n + col] = t[r] * scale;
+        }
+      }
     }
   }
 }
@@ -476,10 +522,19 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     fill_zero<<<(int)g, 256, 0, stream>>>(c, m * n);
     return hipGetLastError();
   }
-  if (m <= kSkinnyRows && k % kSkinnyChunk == 0 &&
-      ((reinterpret_cast<uintptr_t>(w_scales) | reinterpret_cast<uintptr_t>(a_scales)) & 1u) == 0) {
-    gemm_skinny_kernel<<<(unsigned)((n + kSkinnyCols - 1) / kSkinnyCols), 64 * kSkinnyWaves, 0,
-                         stream>>>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
+  // decode shape: 4 waves split K when k % 1024 == 0, else 2 when k % 512 == 0
+  // (each wave's range a whole number of 256-wide steps); scale loads are
+  // 4-byte words
+  const bool skinny_aligned = ((reinterpret_cast<uintptr_t>(w_scales) |
+                                reinterpret_cast<uintptr_t>(a_scales)) & 3u) == 0;
+  if (m <= kSkinnyRows && skinny_aligned && k % (4 * kSkinnyStep) == 0) {
+    gemm_skinny_kernel<4><<<(unsigned)((n + kSkinnyCols - 1) / kSkinnyCols), 256, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
+    return hipGetLastError();
+  }
+  if (m <= kSkinnyRows && skinny_aligned && k % (2 * kSkinnyStep) == 0) {
+    gemm_skinny_kernel<2><<<(unsigned)((n + kSkinnyCols - 1) / kSkinnyCols), 128, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
     return hipGetLastError();
   }
   // Tile choice (measured on MI355X): 256 x 256 with 8 waves is the most

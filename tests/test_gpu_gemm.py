@@ -72,7 +72,8 @@ def test_ragged_shapes(m, n, k):
 @pytest.mark.parametrize("m,n,k", [(1, 1, 512), (5, 127, 1024), (16, 129, 512), (9, 1000, 2048),
                                    (16, 256, 8192), (3, 300, 1536)])
 def test_decode_shapes(m, n, k):
-    """m <= 16 with k % 512 == 0 takes the decode-shape kernel."""
+    """m <= 16 with k % 512 == 0 takes the decode-shape kernel (K split over 4
+    waves when k % 1024 == 0, else over 2; odd and single step counts)."""
     a = W.adversarial(7 * m + k, m, k)
     w = W.adversarial(11 * n + k, n, k)
     qa, qw = Q.quantize(a), Q.quantize(w)
