@@ -89,7 +89,8 @@ def stochastic(y: Fraction, book, u: int) -> int:
 
 def quantize_block(xb_bits, s32: Fraction, mode: str = "select", draws=None):
     """Algorithm 1 on one 16-element block of bf16 bit patterns with a given s32.
-    ``mode`` "e2m1" / "e1m2" keeps that branch regardless of the errors.
+    ``mode`` "e2m1" / "e1m2" keeps that branch regardless of the errors;
+    "four_six" compares E2M1 under max/6 with E2M1 under max/4 (T = 0).
     ``draws`` (16 integers in [0, 256)) switches the chosen branch's codes to
     stochastic rounding of the fp32 quotient fl32(|x| / s8), with draw 255 - u
     for an element whose sign bit is set (App. D's signed rule); scales and
@@ -99,7 +100,8 @@ def quantize_block(xb_bits, s32: Fraction, mode: str = "select", draws=None):
     x = [round_f32(v / s32) for v in X]                      # X_FP8 in fp32
     bm = max(abs(v) for v in x)
     results = {}
-    for name, div, book in (("F", 6, E2M1), ("I", 7, E1M2X2)):
+    second = ("I", 4, E2M1) if mode == "four_six" else ("I", 7, E1M2X2)
+    for name, div, book in (("F", 6, E2M1), second):
         cand = round_f32(bm / div)                           # fp32 argument of FP8_E4M3
         scode, s8 = nearest(cand, E4M3)
         codes, err = [], Fraction(0)
@@ -114,18 +116,21 @@ def quantize_block(xb_bits, s32: Fraction, mode: str = "select", draws=None):
         results[name] = (scode, codes, err)
     ef, ei = results["F"][2], results["I"][2]
     t = 0 if ef < ei else 1
-    if mode != "select":
+    if mode == "four_six":
+        t = 1 if ei < ef else 0              # E2M1 under max/4 only where strictly better
+    elif mode != "select":
         t = 0 if mode == "e2m1" else 1
     scode, mags, _ = results["I" if t else "F"]
     if draws is not None:
-        book = E1M2X2 if t else E2M1
+        book = E1M2X2 if (t and mode != "four_six") else E2M1
         s8 = E4M3[scode][1]
         mags = []
         for b, v, u in zip(xb_bits, x, draws):
             y = round_f32(abs(v) / s8) if s8 != 0 else Fraction(0)
             mags.append(stochastic(y, book, 255 - int(u) if int(b) >> 15 else int(u)))
     nibs = [((int(b) >> 15) << 3) | c for b, c in zip(xb_bits, mags)]
-    return (t << 7) | scode, nibs, ef, ei
+    tbit = 0 if mode == "four_six" else t
+    return (tbit << 7) | scode, nibs, ef, ei
 
 
 def tensor_scale(x_bits) -> Fraction:

@@ -100,7 +100,7 @@ def signed_draws(u: np.ndarray, sign: np.ndarray) -> np.ndarray:
     return np.where(sign == 1, 255 - u, u)
 
 
-MODES = ("select", "e2m1", "e1m2")
+MODES = ("select", "e2m1", "e1m2", "four_six")
 ROUNDINGS = ("nearest", "stochastic")
 
 
@@ -125,7 +125,11 @@ def _algorithm1_blocks(xb: np.ndarray, mode: str):
         return code, s8, q, d, y
 
     cf, sf, qf, df, yf = branch(6, F.F_GRID)
-    ci, si, qi, di, yi = branch(7, F.I_GRID)
+    if mode == "four_six":
+        # the second candidate is E2M1 with the block max mapped to 4
+        ci, si, qi, di, yi = branch(4, F.F_GRID)
+    else:
+        ci, si, qi, di, yi = branch(7, F.I_GRID)
 
     # Err_E2M1 - Err_E1M2 = sum((x - Df)^2 - (x - Di)^2) = sum((Di - Df) * (2x - Df - Di)).
     # Each term is exact in fp64; the block sum is certified exact or redone
@@ -140,7 +144,9 @@ def _algorithm1_blocks(xb: np.ndarray, mode: str):
             delta[i] = 0.0 if exact == 0 else (1.0 if exact > 0 else -1.0) * max(abs(float(exact)), 5e-324)
     delta = delta.reshape(bm.shape)
     t = (~(delta < 0)).astype(np.uint8)                    # E2M1 iff Err_E2M1 < Err_E1M2
-    if mode != "select":
+    if mode == "four_six":
+        t = (delta > 0).astype(np.uint8)                   # /4 only where strictly better
+    elif mode != "select":
         t = np.full_like(t, 0 if mode == "e2m1" else 1)
     return cf, ci, qf, qi, yf, yi, delta, t
 
@@ -155,7 +161,10 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str =
     Algorithm 1 for every block, with everything else unchanged: the E2M1
     branch alone is NVFP4 (Sec. 2.1: block scale E4M3(max/6), E2M1 codes) and
     the E1M2 branch alone is the INT4-style format, with the same tensor-scale
-    rule; T still records the branch.
+    rule; T still records the branch.  "four_six" is the 4/6 candidate set
+    the paper compares against (Sec. 2.3, Sec. 4.2): E2M1 under the block scale
+    E4M3(max/6) or E4M3(max/4), whichever has the smaller squared error
+    (ties keep /6); T is 0, so the result is plain NVFP4.
 
     ``rounding`` "stochastic" writes the codes of the chosen branch by the
     stochastic rounding of App. D (``formats.stochastic_round_to_codebook``)
@@ -182,12 +191,13 @@ def quantize(x_bits: np.ndarray, s32=None, mode: str = "select", rounding: str =
         u = u.astype(np.int64)
         u = signed_draws(u, sign)
         qf = F.stochastic_round_to_codebook(yf, F.F_GRID, u)
-        qi = F.stochastic_round_to_codebook(yi, F.I_GRID, u)
+        qi = F.stochastic_round_to_codebook(yi, F.F_GRID if mode == "four_six" else F.I_GRID, u)
     mag = np.where(t[..., None] == 1, qi, qf).astype(np.uint8)
     nib = (sign << 3) | mag
     nib = nib.reshape(rows, k)
     codes = (nib[:, 0::2] | (nib[:, 1::2] << 4)).astype(np.uint8)
-    scales = ((t << 7) | np.where(t == 1, ci, cf)).astype(np.uint8)
+    tbit = np.zeros_like(t) if mode == "four_six" else t
+    scales = ((tbit << 7) | np.where(t == 1, ci, cf)).astype(np.uint8)
     return Quantized(codes=codes, scales=scales, s32=s32, t=t,
                      sf_code=cf.astype(np.uint8), si_code=ci.astype(np.uint8), delta=delta)
 
@@ -273,7 +283,8 @@ def quantize_2d(x_bits: np.ndarray, s32=None, mode: str = "select") -> Quantized
     mag = np.where(t[..., None] == 1, qi, qf).astype(np.uint8)
     mag = mag.reshape(tn, tk, BLOCK, BLOCK).transpose(0, 2, 1, 3).reshape(n, k)
     nib = ((x_bits >> 15).astype(np.uint8) << 3) | mag
-    tile_scales = ((t << 7) | np.where(t == 1, ci, cf)).astype(np.uint8)
+    tbit = np.zeros_like(t) if mode == "four_six" else t
+    tile_scales = ((tbit << 7) | np.where(t == 1, ci, cf)).astype(np.uint8)
     scales = np.repeat(tile_scales, BLOCK, axis=0)                       # [N, K/16]
     scales_t = np.repeat(tile_scales.T, BLOCK, axis=0)                   # [K, N/16]
     return Quantized2D(codes=_pack(nib), scales=scales, codes_t=_pack(np.ascontiguousarray(nib.T)),

@@ -256,3 +256,42 @@ def test_catches_hadamard_unnormalized(monkeypatch):
     from oracle import hadamard as HD
     monkeypatch.setattr(HD, "sylvester", lambda b, _o=HD.sylvester: 2 * _o(b))
     assert not _hadamard_pins_pass()
+
+
+def _four_six_pins_pass() -> bool:
+    from tests import test_oracle_four_six as T46
+    try:
+        T46.test_matches_bruteforce(2, 1.0)
+        T46.test_ties_keep_six()
+        T46.test_by_construction()
+    except AssertionError:
+        return False
+    return True
+
+
+def test_unmutated_four_six_pins_pass():
+    assert _four_six_pins_pass()
+
+
+def test_catches_four_six_ties_to_four(monkeypatch):
+    orig = Q._algorithm1_blocks
+
+    def mutated(xb, mode):
+        out = list(orig(xb, mode))
+        if mode == "four_six":
+            out[7] = (out[6] >= 0).astype(np.uint8)
+        return tuple(out)
+
+    monkeypatch.setattr(Q, "_algorithm1_blocks", mutated)
+    assert not _four_six_pins_pass()
+
+
+def test_catches_four_six_wrong_divisor(monkeypatch):
+    orig = Q._algorithm1_blocks
+
+    def mutated(xb, mode):
+        # 4/6 run as MixFP4 selection: INT4 codes under max/7 instead of E2M1 under max/4
+        return orig(xb, "select" if mode == "four_six" else mode)
+
+    monkeypatch.setattr(Q, "_algorithm1_blocks", mutated)
+    assert not _four_six_pins_pass()
