@@ -160,6 +160,7 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
     ms_given = timed(True)
     ms_compute = timed(False)
     ms_nvfp4 = timed(True, "e2m1")
+    ms_46 = timed(True, "four_six")
     ms_sr = timed(True, rounding="stochastic", seed=1, offset=0)
     ms_rht = timed(True, hadamard_block=128, hadamard_signs=signs)
     ms_rht_sr = timed(True, rounding="stochastic", seed=1, hadamard_block=128,
@@ -189,6 +190,8 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
         "e2m1_only_us": round(ms_nvfp4 * 1e3, 2),
         "e2m1_only_GBps": round(n * QUANT_BYTES_PER_ELEM / (ms_nvfp4 * 1e-3) / 1e9, 1),
         "e2m1_only_note": "the same kernel forced to the E2M1 branch (NVFP4 encoding), s32 given",
+        "four_six_us": round(ms_46 * 1e3, 2), "four_six_GBps": rate(ms_46),
+        "four_six_note": "the 4/6 candidate set (E2M1 under max/6 or max/4), s32 given",
         "stochastic_us": round(ms_sr * 1e3, 2), "stochastic_GBps": rate(ms_sr),
         "stochastic_note": "MixFP4 selection with stochastic rounding of the codes (App. D), "
                            "Philox4x32-10 draws per block, s32 given",

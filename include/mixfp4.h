@@ -55,6 +55,10 @@ typedef enum {
  * GEMM read the result like any MixFP4 tensor:                             */
 #define MIXFP4_FORCE_E2M1 2u    /* E2M1 only (T = 0): NVFP4 (Sec. 2.1)        */
 #define MIXFP4_FORCE_E1M2 4u    /* E1M2 x2 only (T = 1): INT4 codes           */
+/* The 4/6 candidate set the paper compares against (Sec. 2.3, Sec. 4.2):
+ * E2M1 under the block scale E4M3(max/6) or E4M3(max/4), whichever has the
+ * smaller squared error (ties keep max/6); T = 0, i.e. plain NVFP4.        */
+#define MIXFP4_FOUR_SIX 32u
 /* Stochastic rounding of the codes (App. D); mixfp4_quantize_ex only.      */
 #define MIXFP4_STOCHASTIC 8u
 /* Quantize X^T (blocks of 16 consecutive rows of X); mixfp4_quantize_ex only.*/
@@ -84,10 +88,10 @@ typedef enum {
  *                fl32(max|X| / 2688), or 1.0f if X is all zero (Algorithm 1).
  *                GIVEN: read; must be finite and > 0.
  *   flags        MIXFP4_SCALE_COMPUTE or MIXFP4_SCALE_GIVEN, optionally OR-ed
- *                with one of MIXFP4_FORCE_E2M1 / MIXFP4_FORCE_E1M2; any other
- *                bit (MIXFP4_STOCHASTIC included: it needs the seed of
- *                mixfp4_quantize_ex), or both FORCE bits, returns
- *                MIXFP4_ERR_FLAGS.
+ *                with one of MIXFP4_FORCE_E2M1 / MIXFP4_FORCE_E1M2 /
+ *                MIXFP4_FOUR_SIX; any other bit (MIXFP4_STOCHASTIC and
+ *                MIXFP4_TRANSPOSE included: they are mixfp4_quantize_ex
+ *                options), or two format flags, returns MIXFP4_ERR_FLAGS.
  */
 int mixfp4_quantize(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
                     uint8_t *codes, uint8_t *scales, float *tensor_scale,
@@ -152,7 +156,7 @@ int mixfp4_quantize_ex(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
  * read the same quantized values.  rows % 16 == 0, k % 16 == 0, ldw as ldx
  * of mixfp4_quantize; codes and codes_t 16-byte aligned; codes_t and
  * scales_t both NULL or both given.  flags: MIXFP4_SCALE_COMPUTE/GIVEN and
- * at most one FORCE flag.  Bit-identical to the CPU oracle.
+ * at most one of FORCE_E2M1 / FORCE_E1M2 / FOUR_SIX.  Bit-identical to the CPU oracle.
  */
 int mixfp4_quantize_2d(const uint16_t *w, int64_t rows, int64_t k, int64_t ldw,
                        uint8_t *codes, uint8_t *scales, uint8_t *codes_t,
@@ -226,7 +230,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 103
+#define MIXFP4_ABI_VERSION 104
 
 #ifdef __cplusplus
 }

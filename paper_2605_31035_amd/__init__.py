@@ -36,7 +36,8 @@ FORCE_E2M1 = 2
 FORCE_E1M2 = 4
 STOCHASTIC = 8
 TRANSPOSE = 16
-_MODES = {"mixfp4": 0, "e2m1": FORCE_E2M1, "e1m2": FORCE_E1M2}
+FOUR_SIX = 32
+_MODES = {"mixfp4": 0, "e2m1": FORCE_E2M1, "e1m2": FORCE_E1M2, "four_six": FOUR_SIX}
 
 
 def _stream(device) -> ctypes.c_void_p:
@@ -66,7 +67,8 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
     ``tensor_scale`` None computes s32 = max|X| / 2688 on the device (into
     ``scale_out`` if given); a 1-element fp32 tensor is used as the given s32.
     ``mode`` "mixfp4" selects the format per block; "e2m1" (NVFP4) and "e1m2"
-    (INT4) take that branch for every block.  ``rounding`` "stochastic"
+    (INT4) take that branch for every block; "four_six" is the 4/6 baseline
+    (E2M1 under max/6 or max/4, plain NVFP4 output).  ``rounding`` "stochastic"
     writes the codes by App. D's stochastic rounding with Philox draws of
     (``seed``, ``offset``).  ``hadamard_block`` b > 0 rotates X first
     (mixfp4_hadamard with ``hadamard_signs``, an int8 CUDA tensor of b signs).

@@ -19,6 +19,19 @@ int launch_status(hipError_t e) {
   return MIXFP4_ERR_LAUNCH;
 }
 
+constexpr unsigned kModeFlags = MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2 | MIXFP4_FOUR_SIX;
+
+// Format mode of the flags: 0 MixFP4, 1 E2M1 only, 2 E1M2 only, 3 4/6; -1
+// when more than one format flag is set.
+int format_mode(unsigned flags) {
+  const unsigned f = flags & kModeFlags;
+  if (f == 0u) return 0;
+  if (f == MIXFP4_FORCE_E2M1) return 1;
+  if (f == MIXFP4_FORCE_E1M2) return 2;
+  if (f == MIXFP4_FOUR_SIX) return 3;
+  return -1;
+}
+
 bool valid_hadamard_block(int32_t b) {
   return b == 16 || b == 32 || b == 64 || b == 128 || b == 256;
 }
@@ -26,14 +39,11 @@ bool valid_hadamard_block(int32_t b) {
 int quantize_impl(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, uint8_t* codes,
                   uint8_t* scales, float* tensor_scale, unsigned flags, int32_t hadamard_block,
                   const int8_t* hadamard_signs, uint64_t seed, uint64_t offset, void* stream) {
-  const unsigned known = MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2 |
-                         MIXFP4_STOCHASTIC | MIXFP4_TRANSPOSE;
-  if ((flags & ~known) != 0u ||
-      (flags & (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) == (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2))
-    return MIXFP4_ERR_FLAGS;
+  const unsigned known = MIXFP4_SCALE_GIVEN | kModeFlags | MIXFP4_STOCHASTIC | MIXFP4_TRANSPOSE;
+  if ((flags & ~known) != 0u || format_mode(flags) < 0) return MIXFP4_ERR_FLAGS;
   const bool given = (flags & MIXFP4_SCALE_GIVEN) != 0u;
   mixfp4::QuantOptions opt;
-  opt.mode = (flags & MIXFP4_FORCE_E2M1) ? 1 : (flags & MIXFP4_FORCE_E1M2) ? 2 : 0;
+  opt.mode = format_mode(flags);
   opt.sr = (flags & MIXFP4_STOCHASTIC) != 0u;
   opt.srp = {(uint32_t)seed, (uint32_t)(seed >> 32), (uint32_t)offset, (uint32_t)(offset >> 32)};
   const bool transpose = (flags & MIXFP4_TRANSPOSE) != 0u;
@@ -104,7 +114,7 @@ const char* mixfp4_status_string(int status) {
     case MIXFP4_ERR_NULL: return "MIXFP4_ERR_NULL: a required pointer is NULL";
     case MIXFP4_ERR_SHAPE: return "MIXFP4_ERR_SHAPE: bad size (negative, K % 16 != 0, ldx < K, ldx % 8 != 0, or a Hadamard block that is not 16..256 or does not divide K)";
     case MIXFP4_ERR_ALIGN: return "MIXFP4_ERR_ALIGN: pointer misaligned";
-    case MIXFP4_ERR_FLAGS: return "MIXFP4_ERR_FLAGS: unknown flag bits or both FORCE flags";
+    case MIXFP4_ERR_FLAGS: return "MIXFP4_ERR_FLAGS: unknown flag bits, or more than one format mode";
     case MIXFP4_ERR_LAUNCH: return "MIXFP4_ERR_LAUNCH: kernel launch failed";
     default: return "unknown mixfp4 status";
   }
@@ -131,11 +141,10 @@ int mixfp4_quantize_ex(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, 
 int mixfp4_quantize_2d(const uint16_t* w, int64_t rows, int64_t k, int64_t ldw, uint8_t* codes,
                        uint8_t* scales, uint8_t* codes_t, uint8_t* scales_t, float* tensor_scale,
                        unsigned flags, void* stream) {
-  if ((flags & ~(MIXFP4_SCALE_GIVEN | MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) != 0u ||
-      (flags & (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2)) == (MIXFP4_FORCE_E2M1 | MIXFP4_FORCE_E1M2))
+  if ((flags & ~(MIXFP4_SCALE_GIVEN | kModeFlags)) != 0u || format_mode(flags) < 0)
     return MIXFP4_ERR_FLAGS;
   const bool given = (flags & MIXFP4_SCALE_GIVEN) != 0u;
-  const int mode = (flags & MIXFP4_FORCE_E2M1) ? 1 : (flags & MIXFP4_FORCE_E1M2) ? 2 : 0;
+  const int mode = format_mode(flags);
   if (rows < 0 || k < 0 || (k % mixfp4::kBlock) != 0 || (rows % mixfp4::kBlock) != 0)
     return MIXFP4_ERR_SHAPE;
   if (rows > 0 && (ldw < k || (ldw % 8) != 0)) return MIXFP4_ERR_SHAPE;

@@ -27,7 +27,8 @@ HadamardParams hadamard_params(int b, const int8_t* signs);
 
 // Options of one quantize call beyond the format mode.
 struct QuantOptions {
-  int mode = 0;              // 0 MixFP4 selection, 1 E2M1 only (NVFP4), 2 E1M2 only (INT4)
+  int mode = 0;              // 0 MixFP4 selection, 1 E2M1 only (NVFP4), 2 E1M2 only (INT4),
+                             // 3 the 4/6 candidate set (E2M1 under max/6 or max/4)
   bool sr = false;           // stochastic rounding of the codes
   SrParams srp{};
   bool had = false;          // rotate first

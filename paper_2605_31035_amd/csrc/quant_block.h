@@ -138,7 +138,27 @@ __device__ __forceinline__ void exact_pair(const float (&xs)[16], const uint32_t
 
 // Format modes: MixFP4 selection (Algorithm 1), or one branch for every
 // block (E2M1 = NVFP4, E1M2 = INT4); T records the branch either way.
-constexpr int kSelect = 0, kForceE2M1 = 1, kForceE1M2 = 2;
+// kFourSix: the candidate set {E2M1 under max/6, E2M1 under max/4} (the 4/6
+// baseline the paper compares against), T = 0.
+constexpr int kSelect = 0, kForceE2M1 = 1, kForceE1M2 = 2, kFourSix = 3;
+
+// Exact contribution of elements J, J+1 to Err(max/6) - Err(max/4) in fp64,
+// both branches E2M1: (D_4 - D_6) (2|x| - D_6 - D_4), exact for the same
+// reasons as exact_pair.
+template <int J>
+__device__ __forceinline__ void exact_pair_ff(const float (&xs)[16], const uint32_t (&p6)[2],
+                                              const uint32_t (&p4)[2], float s6, float s4,
+                                              double& d) {
+  const f32x2 q6 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p6[J >> 3], 1.0f, (J & 7) >> 1);
+  const f32x2 q4 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(p4[J >> 3], 1.0f, (J & 7) >> 1);
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const double ax = (double)fabsf(xs[J + h]);
+    const double d6 = (double)(fabsf(h ? q6.y : q6.x) * s6);
+    const double d4 = (double)(fabsf(h ? q4.y : q4.x) * s4);
+    d += (d4 - d6) * ((2.0 * ax - d6) - d4);
+  }
+}
 
 // E1M2 codes of the 16 elements with saturation at 7 (a subnormal or
 // saturated s_I admits codes above 7; rare path): codes into pi, with kErr
@@ -188,6 +208,69 @@ __device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], float s, float 
   return make_uint2(o[0], o[1]);
 }
 
+// 4/6: both candidates are E2M1, under E4M3(bm/6) and E4M3(bm/4) (bm/4 is
+// exact in fp32); the squared errors are compared as in Algorithm 1's
+// selection (bounded fp32 estimate, exact fp64 sum inside the bound); /4 is
+// kept only where its error is strictly smaller.  T = 0.
+template <bool kSR, bool kTile>
+__device__ __forceinline__ void quantize_four_six(const float (&xs)[16], float bm,
+                                                  const float2* __restrict__ tab, uint2& out,
+                                                  uint32_t& scale_byte, uint4 rnd) {
+  constexpr float kR6 = 1.0f / 6.0f;
+  const float cand6 = fminf(div_rn(bm, 6.0f, kR6), 448.0f);
+  const float cand4 = fminf(bm * 0.25f, 448.0f);
+  const s16x2 sc = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(s16x2{0, 0}, cand6, cand4, 1.0f, false);
+  const uint32_t scw = __builtin_bit_cast(uint32_t, sc);
+  const uint32_t c6 = scw & 0x7Fu, c4 = (scw >> 8) & 0x7Fu;
+  const float2 e6 = tab[c6], e4 = tab[c4];
+  const float s6 = e6.x, r6 = e6.y, s4 = e4.x, r4 = e4.y;
+  uint32_t p6[2] = {0u, 0u}, p4[2] = {0u, 0u};
+  float a6[2] = {0.0f, 0.0f}, b6[2] = {0.0f, 0.0f}, a4[2] = {0.0f, 0.0f}, b4[2] = {0.0f, 0.0f};
+#define MIXFP4_PAIR(J)                    \
+  encode_f_pair<J>(xs, s6, r6, p6);       \
+  encode_f_pair<J>(xs, s4, r4, p4);       \
+  error_pair<J>(xs, p6, a6, b6);          \
+  error_pair<J>(xs, p4, a4, b4);
+  MIXFP4_PAIR(0) MIXFP4_PAIR(2) MIXFP4_PAIR(4) MIXFP4_PAIR(6)
+  MIXFP4_PAIR(8) MIXFP4_PAIR(10) MIXFP4_PAIR(12) MIXFP4_PAIR(14)
+#undef MIXFP4_PAIR
+  float a6s = a6[0] + a6[1], b6s = b6[0] + b6[1], a4s = a4[0] + a4[1], b4s = b4[0] + b4[1];
+  if constexpr (kTile) {
+    a6s = row16_sum(a6s);
+    b6s = row16_sum(b6s);
+    a4s = row16_sum(a4s);
+    b4s = row16_sum(b4s);
+  }
+  // Err6 - Err4 = (s6^2 b6 - s4^2 b4) + 2 (s4 a4 - s6 a6); same error bound
+  // as the MixFP4 selection (both cross sums have non-negative terms).
+  const float s62b = (s6 * s6) * b6s, s42b = (s4 * s4) * b4s;
+  const float t6 = s6 * a6s, t4 = s4 * a4s;
+  const float est = (s62b - s42b) + 2.0f * (t4 - t6);
+  const float tau = kTile ? 0x1p-18f * (t6 + t4) + 0x1p-21f * (s62b + s42b)
+                          : 0x1p-19f * (t6 + t4) + 0x1p-22f * (s62b + s42b);
+  bool use4;
+  if (c6 != 0u && c4 != 0u && fabsf(est) > tau) {
+    use4 = est > 0.0f;
+  } else {
+    double d = 0.0;
+    exact_pair_ff<0>(xs, p6, p4, s6, s4, d);
+    exact_pair_ff<2>(xs, p6, p4, s6, s4, d);
+    exact_pair_ff<4>(xs, p6, p4, s6, s4, d);
+    exact_pair_ff<6>(xs, p6, p4, s6, s4, d);
+    exact_pair_ff<8>(xs, p6, p4, s6, s4, d);
+    exact_pair_ff<10>(xs, p6, p4, s6, s4, d);
+    exact_pair_ff<12>(xs, p6, p4, s6, s4, d);
+    exact_pair_ff<14>(xs, p6, p4, s6, s4, d);
+    if constexpr (kTile) d = row16_sum(d);
+    use4 = d > 0.0;
+  }
+  if constexpr (kSR)
+    out = sr_codes(xs, use4 ? s4 : s6, use4 ? r4 : r6, false, rnd);
+  else
+    out = use4 ? make_uint2(p4[0], p4[1]) : make_uint2(p6[0], p6[1]);
+  scale_byte = use4 ? c4 : c6;
+}
+
 // Codes and scale byte of one block from x (Algorithm 1 after the tensor
 // scale).  With kSR the chosen branch's codes are written by stochastic
 // rounding with the draws in `rnd`; scales and the format choice stay those
@@ -205,6 +288,10 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
 #pragma unroll
   for (int j = 0; j < 16; ++j) bm = fmaxf(bm, fabsf(xs[j]));
   if constexpr (kTile) bm = row16_max(bm);
+  if constexpr (kMode == kFourSix) {
+    quantize_four_six<kSR, kTile>(xs, bm, tab, out, scale_byte, rnd);
+    return;
+  }
   // Candidate block scales E4M3(bm/6), E4M3(bm/7): the exactly rounded
   // quotients, clamped at 448 (saturation), through the gfx950 E4M3
   // converter (scale 1: nearest, ties to the even code; checked against the

@@ -501,6 +501,8 @@ hipError_t launch_small_opts(const uint16_t* x, int64_t rows, int64_t k, int64_t
 hipError_t launch_quantize_small(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
                                  uint8_t* codes, uint8_t* scales, float* tensor_scale,
                                  const QuantOptions& opt, hipStream_t stream) {
+  if (opt.mode == kFourSix)
+    return launch_small_opts<kFourSix>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
   if (opt.mode == kForceE2M1)
     return launch_small_opts<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
   if (opt.mode == kForceE1M2)
@@ -514,6 +516,8 @@ hipError_t launch_quantize(const uint16_t* x, int64_t rows, int64_t k, int64_t l
                            uint8_t* codes, uint8_t* scales, const float* tensor_scale,
                            const QuantOptions& opt, hipStream_t stream) {
   if (rows * (k / kBlock) == 0) return hipSuccess;
+  if (opt.mode == kFourSix)
+    return launch_mode_opts<kFourSix>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
   if (opt.mode == kForceE2M1)
     return launch_mode_opts<kForceE2M1>(x, rows, k, ldx, codes, scales, tensor_scale, opt, stream);
   if (opt.mode == kForceE1M2)

@@ -252,6 +252,8 @@ hipError_t launch_quantize_2d(const uint16_t* w, int64_t n, int64_t k, int64_t l
                               uint8_t* scales_t, const float* tensor_scale, int mode,
                               hipStream_t stream) {
   if (n == 0 || k == 0) return hipSuccess;
+  if (mode == 3)
+    return launch_2d_mode<3>(w, n, k, ldw, codes, scales, codes_t, scales_t, tensor_scale, stream);
   if (mode == 1)
     return launch_2d_mode<1>(w, n, k, ldw, codes, scales, codes_t, scales_t, tensor_scale, stream);
   if (mode == 2)
@@ -263,6 +265,8 @@ hipError_t launch_quantize_t(const uint16_t* x, int64_t rows, int64_t k, int64_t
                              uint8_t* codes_t, uint8_t* scales_t, const float* tensor_scale,
                              const QuantOptions& opt, hipStream_t stream) {
   if (rows == 0 || k == 0) return hipSuccess;
+  if (opt.mode == 3)
+    return launch_t_opts<3>(x, rows, k, ldx, codes_t, scales_t, tensor_scale, opt, stream);
   if (opt.mode == 1)
     return launch_t_opts<1>(x, rows, k, ldx, codes_t, scales_t, tensor_scale, opt, stream);
   if (opt.mode == 2)

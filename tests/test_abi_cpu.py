@@ -57,7 +57,9 @@ def test_quantize_rejects(lib):
     assert q(lib, flags=6) == 4          # both FORCE bits
     assert q(lib, flags=8) == 4          # STOCHASTIC needs mixfp4_quantize_ex
     assert q(lib, flags=16) == 4         # TRANSPOSE is a mixfp4_quantize_ex option
-    assert q(lib, flags=32) == 4         # unknown bit
+    assert q(lib, flags=64) == 4         # unknown bit
+    assert q(lib, flags=2 | 32) == 4     # two format modes
+    assert q(lib, flags=4 | 32) == 4
     assert q(lib, flags=0x80000002) == 4
     assert q(lib, k=24) == 2
     assert q(lib, k=-16) == 2
@@ -108,7 +110,8 @@ def qx(lib, x=A16, rows=4, k=256, ldx=256, codes=A16, scales=A16, ts=A16, flags=
 
 
 def test_quantize_ex_rejects(lib):
-    assert qx(lib, flags=32) == 4
+    assert qx(lib, flags=64) == 4
+    assert qx(lib, flags=2 | 32) == 4
     assert qx(lib, flags=6 | 8) == 4
     assert qx(lib, flags=16, rows=4) == 2                # transpose: rows % 16
     assert qx(lib, flags=16, rows=256, block=128) == 2   # transposed rotation: b <= 64
@@ -142,6 +145,7 @@ def test_quantize_2d_rejects(lib):
         return lib.mixfp4_quantize_2d(w, rows, k, ldw, codes, scales, ct, st, ts, flags, None)
     assert f(flags=8) == 4
     assert f(flags=6) == 4
+    assert f(flags=36) == 4
     assert f(rows=24) == 2
     assert f(k=40, ldw=40) == 2
     assert f(ldw=60) == 2

@@ -127,6 +127,21 @@ def test_forced_format_operands():
     _check(host(c), qa, qw)
 
 
+def test_four_six_operands():
+    """4/6 output is plain NVFP4 (T = 0): the GEMM decodes it like any
+    MixFP4 operand."""
+    import paper_2605_31035_amd as M
+    a = W.adversarial(73, 200, 512)
+    w = W.adversarial(74, 150, 512)
+    qa, qw = Q.quantize(a, mode="four_six"), Q.quantize(w, mode="four_six")
+    ga = M.mixfp4_quantize(dev_bf16(a), mode="four_six")
+    gw = M.mixfp4_quantize(dev_bf16(w), mode="four_six")
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(host(ga[0]), qa.codes)
+    np.testing.assert_array_equal(host(gw[1]), qw.scales)
+    _check(host(M.mixfp4_gemm(ga, gw)), qa, qw)
+
+
 def test_k_zero_writes_zeros():
     import paper_2605_31035_amd as M
     e = torch.empty((4, 0), dtype=torch.uint8, device="cuda")

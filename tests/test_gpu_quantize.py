@@ -96,11 +96,11 @@ def test_small_and_large_compute_paths(rows, k, pad):
     _assert_same(bits, ldx_pad=pad, label=f"compute path {rows}x{k}")
 
 
-@pytest.mark.parametrize("mode", ["e2m1", "e1m2"])
+@pytest.mark.parametrize("mode", ["e2m1", "e1m2", "four_six"])
 @pytest.mark.parametrize("rows,k,s32", [(3, 48, None), (64, 4096, None), (65, 4096, None),
                                         (257, 80, 0.37), (1000, 272, None)])
 def test_forced_format_modes(mode, rows, k, s32):
-    """E2M1-only (NVFP4) and E1M2-only (INT4) modes, small one-launch and
+    """E2M1-only (NVFP4), E1M2-only (INT4) and 4/6 modes, small one-launch and
     large paths, computed and given tensor scales: the oracle's bits."""
     import paper_2605_31035_amd as M
     bits = W.adversarial(rows + 3 * k, rows, k)
@@ -161,3 +161,30 @@ def test_workload_full_size(name, tensors):
         np.testing.assert_array_equal(host(scales.index_select(0, idx)), ref.scales)
         np.testing.assert_array_equal(host(codes.index_select(0, idx)), ref.codes)
         log(f"{name}.{tname} ok; E1M2 share {ref.t.mean():.3f}")
+
+
+def test_four_six_ties_and_full_size():
+    """4/6 on blocks where both candidates are exact (ties keep max/6), and
+    on the full 7B-class prefill activation (sampled rows)."""
+    import paper_2605_31035_amd as M
+    x = np.zeros((2, 32), np.float32)
+    x[0, 0] = 6.0
+    x[0, 16:18] = [3.0, -1.5]
+    x[1, :16] = np.arange(16) * 0.25
+    bits = W.f32_to_bf16_bits(x)
+    codes, scales, _ = M.mixfp4_quantize(dev_bf16(bits), dev_f32(1.0), mode="four_six")
+    torch.cuda.synchronize()
+    ref = Q.quantize(bits, s32=1.0, mode="four_six")
+    np.testing.assert_array_equal(host(scales), ref.scales)
+    np.testing.assert_array_equal(host(codes), ref.codes)
+    assert host(scales)[0, 0] == 0x38 and host(scales)[0, 1] == 0x30
+    a = W.get("prefill_7b", tensors=("A",)).tensors["A"]
+    log("four_six full size prefill A")
+    codes, scales, s = M.mixfp4_quantize(dev_bf16(a), mode="four_six")
+    torch.cuda.synchronize()
+    s32 = Q.tensor_scale(a)
+    assert host(s)[0] == s32
+    rows = np.unique(np.random.default_rng(3).integers(0, a.shape[0], 64))
+    ref = Q.quantize(a[rows], s32=s32, mode="four_six")
+    np.testing.assert_array_equal(host(scales)[rows], ref.scales)
+    np.testing.assert_array_equal(host(codes)[rows], ref.codes)

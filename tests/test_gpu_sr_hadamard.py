@@ -41,7 +41,8 @@ def _check_quant(got, ref, label):
 
 # ---------------------------------------------------------------- stochastic rounding
 
-@pytest.mark.parametrize("mode,omode", [("mixfp4", "select"), ("e2m1", "e2m1"), ("e1m2", "e1m2")])
+@pytest.mark.parametrize("mode,omode", [("mixfp4", "select"), ("e2m1", "e2m1"), ("e1m2", "e1m2"),
+                                        ("four_six", "four_six")])
 @pytest.mark.parametrize("rows,k,s32,pad", [(3, 48, None, 0), (64, 4096, None, 0),
                                             (65, 4096, None, 0), (257, 80, 0.37, 0),
                                             (33, 64, None, 8), (300, 1024, 1.5, 24)])

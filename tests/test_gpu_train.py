@@ -47,7 +47,8 @@ def _grad(seed, t, n, scale=1e-3):
 
 # ---------------------------------------------------------------- 2D weights
 
-@pytest.mark.parametrize("mode,omode", [("mixfp4", "select"), ("e2m1", "e2m1"), ("e1m2", "e1m2")])
+@pytest.mark.parametrize("mode,omode", [("mixfp4", "select"), ("e2m1", "e2m1"), ("e1m2", "e1m2"),
+                                        ("four_six", "four_six")])
 @pytest.mark.parametrize("n,k,s32,pad", [(16, 16, None, 0), (48, 64, None, 0), (80, 48, 0.001, 0),
                                          (256, 512, None, 8), (272, 1040, 0.01, 0)])
 def test_quantize_2d(mode, omode, n, k, s32, pad):
@@ -94,7 +95,8 @@ def _ref_t(bits, s32, omode, rounding, seed, offset, b, signs):
     return Q.quantize(xt, s32=s32, mode=omode, rounding=rounding, seed=seed, offset=offset)
 
 
-@pytest.mark.parametrize("mode,omode", [("mixfp4", "select"), ("e2m1", "e2m1")])
+@pytest.mark.parametrize("mode,omode", [("mixfp4", "select"), ("e2m1", "e2m1"),
+                                        ("four_six", "four_six")])
 @pytest.mark.parametrize("rounding", ["nearest", "stochastic"])
 @pytest.mark.parametrize("b", [0, 16, 32, 64])
 @pytest.mark.parametrize("rows,k,s32,pad", [(64, 64, None, 0), (320, 112, None, 8),
