@@ -53,8 +53,8 @@ AMAX_BYTES_PER_ELEM = 2                   # the tensor-scale pass re-reads X
 # what the same counters read for a 512 MiB elementwise copy: FETCH x 2.0,
 # WRITE x 1.0.  Valid only for the GEMM source it was measured on (first 16
 # hex digits of its SHA-256); reported as null otherwise.
-GEMM1_TRAFFIC = {"gemm_src_sha256_16": "ac921d68e3ae719a",
-                 "fetch_kib": 46818.8, "write_kib": 88064.0,
+GEMM1_TRAFFIC = {"gemm_src_sha256_16": "a55ee40661aa8400",
+                 "fetch_kib": 46819.5, "write_kib": 88064.0,
                  "fetch_scale": 2.0, "write_scale": 1.0}
 
 

@@ -539,13 +539,15 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   }
   // Tile choice (measured on MI355X): 256 x 256 with 8 waves is the most
   // efficient tile per compute unit (least LDS traffic and decode work per
-  // MFMA), so it is used whenever it fills at least one round of the 256
-  // compute units; the clock headroom of a partly idle last round makes up for
-  // much of its imbalance.  Below that, 128 x 256 (same wave tiles, half the
-  // rows) if it fills most of a round, else 128 x 128.
+  // MFMA), so it is used whenever it fills at least three quarters of a round
+  // of the 256 compute units (2048 x 6144 x 4096: 127 us on 192 such tiles,
+  // 177 us on 384 tiles of 128 x 256); the clock headroom of a partly idle
+  // last round makes up for part of its imbalance (splitting those tiles'
+  // K range in two measured no better).  Below that, 128 x 256 (same wave
+  // tiles, half the rows) if it fills most of a round, else 128 x 128.
   const int64_t tiles256 = ((m + 255) / 256) * ((n + 255) / 256);
   const int64_t tiles128x256 = ((m + 127) / 128) * ((n + 255) / 256);
-  if (tiles256 >= 256)
+  if (4 * tiles256 >= 3 * 256)
     return launch_tile<256, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
                                        c, stream);
   if (tiles128x256 >= 192)

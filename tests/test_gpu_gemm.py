@@ -96,11 +96,12 @@ def test_many_tiles_ragged(m, n, k):
     _check(c1, qa, qw)
 
 
-@pytest.mark.parametrize("m,n,k", [(2000, 3100, 512), (2000, 3100, 560)])
+@pytest.mark.parametrize("m,n,k", [(2000, 3100, 512), (2000, 3100, 560), (1500, 8000, 560)])
 def test_mid_size_ragged(m, n, k):
-    """Shapes with fewer 256x256 tiles than CUs but at least 192 of 128x256
-    (the 128x256 tile path), ragged in all three dimensions, fast and
-    masked-K paths; checked in full."""
+    """Shapes with fewer 256x256 tiles than CUs: 2000 x 3100 takes 128x256
+    tiles, 1500 x 8000 (192 tiles of 256x256, three quarters of a round)
+    takes 256x256 ones; ragged in all three dimensions, fast and masked-K
+    paths; checked in full."""
     a = W.adversarial(m + 11, m, k)
     w = W.adversarial(n + 13, n, k)
     qa, qw = Q.quantize(a), Q.quantize(w)
