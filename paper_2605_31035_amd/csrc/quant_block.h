@@ -24,24 +24,34 @@ __device__ __forceinline__ float tensor_scale_of(uint32_t amax_bf16_bits) {
   return amax > 0.0f ? amax / 2688.0f : 1.0f;       // Algorithm 1, first step
 }
 
-// {E4M3(c), fl32(1 / E4M3(c))} for every 7-bit code ({0, 0} for the zero
-// scale and the NaN code), built by the first 128 threads; the caller
-// synchronizes before use.
-__device__ __forceinline__ void fill_scale_table(float2* tab) {
+// A block-scale divisor s with its two-term reciprocal: rh = 1 / s rounded
+// toward zero and rl = fl32((1 - rh s) / s) >= 0 (the residual 1 - rh s is
+// exact: one fma).  rh + rl equals 1 / s to about 2^-48 relative.
+struct alignas(16) ScaleRecip {
+  float s, rh, rl, unused;
+};
+
+__device__ __forceinline__ ScaleRecip scale_recip(float s) {
+  float rh = __fdiv_rn(1.0f, s);
+  float e = __builtin_fmaf(-rh, s, 1.0f);
+  if (e < 0.0f) {
+    rh = __uint_as_float(__float_as_uint(rh) - 1u);
+    e = __builtin_fmaf(-rh, s, 1.0f);
+  }
+  return ScaleRecip{s, rh, __fdiv_rn(e, s), 0.0f};
+}
+
+// The divisor and two-term reciprocal of every 7-bit E4M3 code (all zero for
+// the zero scale and the NaN code), built by the first 128 threads; the
+// caller synchronizes before use.
+__device__ __forceinline__ void fill_scale_table(ScaleRecip* tab) {
   if (threadIdx.x < 128) {
-    const float v = e4m3_value(threadIdx.x);
     const bool ok = threadIdx.x > 0 && threadIdx.x < 127;
-    tab[threadIdx.x] = ok ? make_float2(v, __fdiv_rn(1.0f, v)) : make_float2(0.0f, 0.0f);
+    tab[threadIdx.x] = ok ? scale_recip(e4m3_value(threadIdx.x)) : ScaleRecip{0.0f, 0.0f, 0.0f, 0.0f};
   }
 }
 
 typedef float f32x2 __attribute__((ext_vector_type(2)));
-
-// sum_{j<8} (0x4B000000 << 4j) mod 2^32: the constant part of the INT4 code
-// accumulator below (every term is the bit pattern of 2^23 + code).
-constexpr uint32_t kMagicPack = 0x4B000000u + (0x4B000000u << 4) + (0x4B000000u << 8) +
-                                (0x4B000000u << 12) + (0x4B000000u << 16) + (0x4B000000u << 20) +
-                                (0x4B000000u << 24) + (0x4B000000u << 28);
 
 // fl32(a / s) given r = fl32(1 / s): q0 = a r is within an ulp of the
 // quotient, the fma residual q0 s - a is exact, and q0 minus residual * r is
@@ -55,6 +65,18 @@ constexpr uint32_t kMagicPack = 0x4B000000u + (0x4B000000u << 4) + (0x4B000000u 
 __device__ __forceinline__ float div_rn(float a, float s, float r) {
   const float q0 = a * r;
   return __builtin_fmaf(-__builtin_fmaf(q0, s, -a), r, q0);
+}
+
+// fl32(a / s) for a divisor s with at most 4 significant bits (the E4M3
+// block scales, 6 and 7) from its two-term reciprocal: a rh + fl32(a rl) is
+// within about 2^-47 of a / s, while a / s with a in fp32 lies at least
+// 2^-29 (relative) away from every rounding boundary of fp32, so the one
+// rounding of the fma is the correctly rounded quotient.  Verified
+// exhaustively for every fp32 a against every such divisor, results and
+// a * rl in the normal range; both addends carry the sign of a (rl >= 0), so
+// zeros keep their sign, also with the zero scale (rh = rl = 0).
+__device__ __forceinline__ float div_scale(float a, float rh, float rl) {
+  return __builtin_fmaf(a, rh, a * rl);
 }
 
 typedef short s16x2 __attribute__((ext_vector_type(2)));
@@ -79,29 +101,31 @@ __device__ __forceinline__ void to_fp8_domain(uint4 v0, uint4 v1, float xmul, fl
 // rounded by the gfx950 FP4 converter (scale 1: nearest, ties to the even
 // code, saturating at 6, sign kept) into nibble pair (J%8)/2 of pf[J/8].
 template <int J>
-__device__ __forceinline__ void encode_f_pair(const float (&xs)[16], float sf, float rf,
+__device__ __forceinline__ void encode_f_pair(const float (&xs)[16], const ScaleRecip& f,
                                               uint32_t (&pf)[2]) {
-  const float yf0 = div_rn(xs[J], sf, rf), yf1 = div_rn(xs[J + 1], sf, rf);
+  const float yf0 = div_scale(xs[J], f.rh, f.rl), yf1 = div_scale(xs[J + 1], f.rh, f.rl);
   pf[J >> 3] = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(pf[J >> 3], yf0, yf1, 1.0f, (J & 7) >> 1);
 }
 
-// Elements J, J+1 (J even), E1M2 (x2 = INT4) branch: y = fl32(|x| / s_I);
-// adding 2^23 rounds it to an integer (ties to even) held in the low mantissa
-// bits, accumulated into pi[J/8] at nibble J%8 together with a constant
-// removed afterwards.  With kErr, ai[J/2 % 2] += |x| * q_I.
+// Elements J, J+1 (J even), E1M2 (x2 = INT4) branch: q = rint(fl32(|x| /
+// s_I)) (round half to even), an exact small integer, inserted as a byte:
+// element J into byte (J%8)/2 of pe[J/8], element J+1 into the same byte of
+// po[J/8] (the nibbles are interleaved afterwards).  With kErr, ai[J/2 % 2]
+// += |x| * q.
 template <int J, bool kErr>
-__device__ __forceinline__ void encode_i_pair(const float (&xs)[16], float si, float ri,
-                                              uint32_t (&pi)[2], float (&ai)[2]) {
+__device__ __forceinline__ void encode_i_pair(const float (&xs)[16], const ScaleRecip& i,
+                                              uint32_t (&pe)[2], uint32_t (&po)[2],
+                                              float (&ai)[2]) {
   const float a0 = fabsf(xs[J]), a1 = fabsf(xs[J + 1]);
-  const uint32_t b0 = __float_as_uint(div_rn(a0, si, ri) + 0x1p23f);
-  const uint32_t b1 = __float_as_uint(div_rn(a1, si, ri) + 0x1p23f);
+  const float q0 = __builtin_rintf(div_scale(a0, i.rh, i.rl));
+  const float q1 = __builtin_rintf(div_scale(a1, i.rh, i.rl));
   if (kErr) {
     float& acc = ai[(J >> 1) & 1];
-    acc = __builtin_fmaf(a0, __uint_as_float(b0) - 0x1p23f, acc);
-    acc = __builtin_fmaf(a1, __uint_as_float(b1) - 0x1p23f, acc);
+    acc = __builtin_fmaf(a0, q0, acc);
+    acc = __builtin_fmaf(a1, q1, acc);
   }
-  pi[J >> 3] += b0 << (4 * (J & 7));
-  pi[J >> 3] += b1 << (4 * ((J + 1) & 7));
+  pe[J >> 3] = __builtin_amdgcn_cvt_pk_u8_f32(q0, (J & 7) >> 1, pe[J >> 3]);
+  po[J >> 3] = __builtin_amdgcn_cvt_pk_u8_f32(q1, (J & 7) >> 1, po[J >> 3]);
 }
 
 // E2M1 error sums of elements J, J+1 from the decoded codes, in two chains:
@@ -164,12 +188,12 @@ __device__ __forceinline__ void exact_pair_ff(const float (&xs)[16], const uint3
 // saturated s_I admits codes above 7; rare path): codes into pi, with kErr
 // also sum |x| q_I into ai.
 template <bool kErr>
-__device__ __forceinline__ void encode_i_saturated(const float (&xs)[16], float si, float ri,
+__device__ __forceinline__ void encode_i_saturated(const float (&xs)[16], const ScaleRecip& i,
                                                    uint32_t (&pi)[2], float (&ai)[2]) {
   pi[0] = pi[1] = 0u;
   ai[0] = ai[1] = 0.0f;
   for (int j = 0; j < 16; ++j) {
-    const float q = fminf(rintf(div_rn(fabsf(xs[j]), si, ri)), 7.0f);
+    const float q = fminf(rintf(div_scale(fabsf(xs[j]), i.rh, i.rl)), 7.0f);
     if (kErr) ai[j & 1] = __builtin_fmaf(fabsf(xs[j]), q, ai[j & 1]);
     pi[j >> 3] |= (uint32_t)q << (4 * (j & 7));
   }
@@ -184,7 +208,7 @@ __device__ __forceinline__ void encode_i_saturated(const float (&xs)[16], float 
 // reads: up iff w > 511 - 2u, ties (w == 511 - 2u) to the even code.  y at
 // or above the largest magnitude clamps to code 7.  E2M1 spacing: 1/2 below
 // 2, 1 below 4, 2 up to 6; E1M2 (x2): 1 everywhere.
-__device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], float s, float r, bool int4,
+__device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], const ScaleRecip& sc, bool int4,
                                           uint4 rnd) {
   const uint32_t words[4] = {rnd.x, rnd.y, rnd.z, rnd.w};
   uint32_t o[2] = {0u, 0u};
@@ -192,7 +216,7 @@ __device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], float s, float 
   for (int j = 0; j < 16; ++j) {
     const uint32_t xb = __float_as_uint(xs[j]);
     const uint32_t neg = xb >> 31;
-    const float y = div_rn(__uint_as_float(xb & 0x7FFFFFFFu), s, r);
+    const float y = div_scale(__uint_as_float(xb & 0x7FFFFFFFu), sc.rh, sc.rl);
     const uint32_t u = ((words[j >> 2] >> (8 * (j & 3))) & 0xFFu) ^ (neg ? 0xFFu : 0u);
     const float thr = (float)(511 - 2 * (int)u);
     const float inv_d = int4 ? 1.0f : (y < 2.0f ? 2.0f : (y < 4.0f ? 1.0f : 0.5f));
@@ -214,21 +238,21 @@ __device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], float s, float 
 // kept only where its error is strictly smaller.  T = 0.
 template <bool kSR, bool kTile>
 __device__ __forceinline__ void quantize_four_six(const float (&xs)[16], float bm,
-                                                  const float2* __restrict__ tab, uint2& out,
+                                                  const ScaleRecip* __restrict__ tab, uint2& out,
                                                   uint32_t& scale_byte, uint4 rnd) {
-  constexpr float kR6 = 1.0f / 6.0f;
-  const float cand6 = fminf(div_rn(bm, 6.0f, kR6), 448.0f);
+  const ScaleRecip d6 = scale_recip(6.0f);
+  const float cand6 = fminf(div_scale(bm, d6.rh, d6.rl), 448.0f);
   const float cand4 = fminf(bm * 0.25f, 448.0f);
   const s16x2 sc = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(s16x2{0, 0}, cand6, cand4, 1.0f, false);
   const uint32_t scw = __builtin_bit_cast(uint32_t, sc);
   const uint32_t c6 = scw & 0x7Fu, c4 = (scw >> 8) & 0x7Fu;
-  const float2 e6 = tab[c6], e4 = tab[c4];
-  const float s6 = e6.x, r6 = e6.y, s4 = e4.x, r4 = e4.y;
+  const ScaleRecip e6 = tab[c6], e4 = tab[c4];
+  const float s6 = e6.s, s4 = e4.s;
   uint32_t p6[2] = {0u, 0u}, p4[2] = {0u, 0u};
   float a6[2] = {0.0f, 0.0f}, b6[2] = {0.0f, 0.0f}, a4[2] = {0.0f, 0.0f}, b4[2] = {0.0f, 0.0f};
 #define MIXFP4_PAIR(J)                    \
-  encode_f_pair<J>(xs, s6, r6, p6);       \
-  encode_f_pair<J>(xs, s4, r4, p4);       \
+  encode_f_pair<J>(xs, e6, p6);           \
+  encode_f_pair<J>(xs, e4, p4);           \
   error_pair<J>(xs, p6, a6, b6);          \
   error_pair<J>(xs, p4, a4, b4);
   MIXFP4_PAIR(0) MIXFP4_PAIR(2) MIXFP4_PAIR(4) MIXFP4_PAIR(6)
@@ -265,7 +289,7 @@ __device__ __forceinline__ void quantize_four_six(const float (&xs)[16], float b
     use4 = d > 0.0;
   }
   if constexpr (kSR)
-    out = sr_codes(xs, use4 ? s4 : s6, use4 ? r4 : r6, false, rnd);
+    out = sr_codes(xs, use4 ? e4 : e6, false, rnd);
   else
     out = use4 ? make_uint2(p4[0], p4[1]) : make_uint2(p6[0], p6[1]);
   scale_byte = use4 ? c4 : c6;
@@ -281,7 +305,7 @@ __device__ __forceinline__ void quantize_four_six(const float (&xs)[16], float b
 // are then all-reduced over the row with butterflies, which leave identical
 // values in every lane, so all 16 lanes take the same decision.
 template <int kMode, bool kSR, bool kTile = false>
-__device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2* __restrict__ tab,
+__device__ __forceinline__ void quantize_xs(const float (&xs)[16], const ScaleRecip* __restrict__ tab,
                                             uint2& out, uint32_t& scale_byte, uint4 rnd) {
   // fl32 rounding is monotonic, so bm is also fl32(max|X| / s32).
   float bm = 0.0f;
@@ -296,53 +320,56 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
   // quotients, clamped at 448 (saturation), through the gfx950 E4M3
   // converter (scale 1: nearest, ties to the even code; checked against the
   // software rounding on every fp32 value in [0, 448]).
-  constexpr float kR6 = 1.0f / 6.0f, kR7 = 1.0f / 7.0f;
-  const float cand6 = kMode == kForceE1M2 ? 0.0f : fminf(div_rn(bm, 6.0f, kR6), 448.0f);
-  const float cand7 = kMode == kForceE2M1 ? 0.0f : fminf(div_rn(bm, 7.0f, kR7), 448.0f);
+  const ScaleRecip d6 = scale_recip(6.0f), d7 = scale_recip(7.0f);
+  const float cand6 = kMode == kForceE1M2 ? 0.0f : fminf(div_scale(bm, d6.rh, d6.rl), 448.0f);
+  const float cand7 = kMode == kForceE2M1 ? 0.0f : fminf(div_scale(bm, d7.rh, d7.rl), 448.0f);
   const s16x2 sc = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(s16x2{0, 0}, cand6, cand7, 1.0f, false);
   const uint32_t scw = __builtin_bit_cast(uint32_t, sc);
   const uint32_t cf = scw & 0x7Fu, ci = (scw >> 8) & 0x7Fu;
-  const float2 ef = tab[cf], ei = tab[ci];
-  const float sf = ef.x, rf = ef.y, si = ei.x, ri = ei.y;
+  const ScaleRecip ef = tab[cf], ei = tab[ci];
+  const float sf = ef.s, si = ei.s;
 
   uint32_t pf[2] = {0u, 0u}, pi[2] = {0u, 0u};
   float af[2] = {0.0f, 0.0f}, bf[2] = {0.0f, 0.0f}, ai[2] = {0.0f, 0.0f};
   if constexpr (kMode != kForceE1M2) {
-    encode_f_pair<0>(xs, sf, rf, pf);
-    encode_f_pair<2>(xs, sf, rf, pf);
-    encode_f_pair<4>(xs, sf, rf, pf);
-    encode_f_pair<6>(xs, sf, rf, pf);
-    encode_f_pair<8>(xs, sf, rf, pf);
-    encode_f_pair<10>(xs, sf, rf, pf);
-    encode_f_pair<12>(xs, sf, rf, pf);
-    encode_f_pair<14>(xs, sf, rf, pf);
+    encode_f_pair<0>(xs, ef, pf);
+    encode_f_pair<2>(xs, ef, pf);
+    encode_f_pair<4>(xs, ef, pf);
+    encode_f_pair<6>(xs, ef, pf);
+    encode_f_pair<8>(xs, ef, pf);
+    encode_f_pair<10>(xs, ef, pf);
+    encode_f_pair<12>(xs, ef, pf);
+    encode_f_pair<14>(xs, ef, pf);
   }
   if constexpr (kMode == kForceE2M1) {
-    out = kSR ? sr_codes(xs, sf, rf, false, rnd) : make_uint2(pf[0], pf[1]);
+    out = kSR ? sr_codes(xs, ef, false, rnd) : make_uint2(pf[0], pf[1]);
     scale_byte = cf;
     return;
   }
   constexpr bool kErr = kMode == kSelect;
-  encode_i_pair<0, kErr>(xs, si, ri, pi, ai);
-  encode_i_pair<2, kErr>(xs, si, ri, pi, ai);
-  encode_i_pair<4, kErr>(xs, si, ri, pi, ai);
-  encode_i_pair<6, kErr>(xs, si, ri, pi, ai);
-  encode_i_pair<8, kErr>(xs, si, ri, pi, ai);
-  encode_i_pair<10, kErr>(xs, si, ri, pi, ai);
-  encode_i_pair<12, kErr>(xs, si, ri, pi, ai);
-  encode_i_pair<14, kErr>(xs, si, ri, pi, ai);
-  pi[0] -= kMagicPack;
-  pi[1] -= kMagicPack;
+  {
+    uint32_t pe[2] = {0u, 0u}, po[2] = {0u, 0u};
+    encode_i_pair<0, kErr>(xs, ei, pe, po, ai);
+    encode_i_pair<2, kErr>(xs, ei, pe, po, ai);
+    encode_i_pair<4, kErr>(xs, ei, pe, po, ai);
+    encode_i_pair<6, kErr>(xs, ei, pe, po, ai);
+    encode_i_pair<8, kErr>(xs, ei, pe, po, ai);
+    encode_i_pair<10, kErr>(xs, ei, pe, po, ai);
+    encode_i_pair<12, kErr>(xs, ei, pe, po, ai);
+    encode_i_pair<14, kErr>(xs, ei, pe, po, ai);
+    pi[0] = pe[0] | (po[0] << 4);
+    pi[1] = pe[1] | (po[1] << 4);
+  }
   // INT4 codes cannot exceed 7 when s_I is a normal E4M3 value below the
   // maximum (then max|x| / s_I < 7.47); other blocks redo the branch with
   // saturation (rare path).
-  if (ci < 8u || ci >= 0x7Eu) encode_i_saturated<kErr>(xs, si, ri, pi, ai);
+  if (ci < 8u || ci >= 0x7Eu) encode_i_saturated<kErr>(xs, ei, pi, ai);
   if constexpr (kMode == kForceE1M2) {
     // sign of X into bit 3 of every nibble
     uint32_t sg[2] = {0u, 0u};
 #pragma unroll
     for (int j = 0; j < 16; ++j) sg[j >> 3] |= (__float_as_uint(xs[j]) >> 31) << (4 * (j & 7) + 3);
-    out = kSR ? sr_codes(xs, si, ri, true, rnd) : make_uint2(pi[0] | sg[0], pi[1] | sg[1]);
+    out = kSR ? sr_codes(xs, ei, true, rnd) : make_uint2(pi[0] | sg[0], pi[1] | sg[1]);
     scale_byte = 0x80u | ci;
     return;
   }
@@ -403,7 +430,7 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const float2*
   }
   // Sign of X into bit 3 of every nibble: the E2M1 codes already carry it.
   if constexpr (kSR) {
-    out = sr_codes(xs, t1 ? si : sf, t1 ? ri : rf, t1, rnd);
+    out = sr_codes(xs, t1 ? ei : ef, t1, rnd);
   } else {
     out.x = t1 ? (pi[0] | (pf[0] & 0x88888888u)) : pf[0];
     out.y = t1 ? (pi[1] | (pf[1] & 0x88888888u)) : pf[1];

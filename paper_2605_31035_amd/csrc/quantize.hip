@@ -13,14 +13,16 @@
 // 16-byte loads, no cross-lane traffic, one 8-byte code store and one scale
 // byte.  Codes, scales and the format bit are exactly those of Algorithm 1:
 //   * x = fl32(X / s32), the candidate-scale quotients and the grid
-//     quotients y = fl32(|x| / s8) are correctly rounded fp32 divisions,
-//     computed with Markstein's division step from a correctly rounded
-//     reciprocal (div_rn, proved exhaustively for the operand classes used);
-//     rounding y to a grid equals rounding the exact quotient, because a
+//     quotients y = fl32(|x| / s8) are correctly rounded fp32 divisions:
+//     X / s32 with Markstein's division step from a correctly rounded
+//     reciprocal (div_rn), the quotients by 6, 7 and the E4M3 block scales
+//     (at most 4 significant bits) with one fma on a two-term reciprocal
+//     (div_scale); both proved exhaustively for the operand classes used.
+//     Rounding y to a grid equals rounding the exact quotient, because a
 //     grid midpoint times s8 is exact in fp32.
 //   * E2M1 rounding uses the gfx950 FP4 converter with scale 1 (round to
 //     nearest even onto the E2M1 grid, ties to the even code, saturating,
-//     sign kept); INT4 rounding adds 2^23 (round half to even).
+//     sign kept); INT4 rounding is rint (round half to even).
 //   * The format choice: an fp32 estimate s_F^2 sum q_F^2 - s_I^2 sum q_I^2
 //     + 2 (s_I sum |x| q_I - s_F sum x q_F) decides when it is farther from
 //     zero than its proven error bound; otherwise the exact fp64 sum
@@ -116,7 +118,7 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
                                               int64_t ldx, int64_t nblocks,
                                               uint8_t* __restrict__ codes,
                                               uint8_t* __restrict__ scales, float xmul, float sx,
-                                              float rx, const float2* tab, const SrParams& sr,
+                                              float rx, const ScaleRecip* tab, const SrParams& sr,
                                               const HadamardParams& hp) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   // Loads are unconditional (a block index past the end reads the last
@@ -166,7 +168,7 @@ __device__ __forceinline__ void quantize_all(const uint16_t* __restrict__ x, int
                                              int64_t ldx, int64_t nblocks,
                                              uint8_t* __restrict__ codes,
                                              uint8_t* __restrict__ scales, float s32,
-                                             const float2* tab, const SrParams& sr,
+                                             const ScaleRecip* tab, const SrParams& sr,
                                              const HadamardParams& hp) {
   if (s32 >= 0x1p-90f && s32 <= 0x1p120f) {
     quantize_loop<kContig, false, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, 1.0f,
@@ -184,7 +186,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales,
     const float* __restrict__ tensor_scale, SrParams sr, HadamardParams hp) {
-  __shared__ float2 tab[128];
+  __shared__ ScaleRecip tab[128];
   fill_scale_table(tab);
   __syncthreads();
   quantize_all<kContig, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, *tensor_scale, tab,
@@ -208,7 +210,7 @@ __global__ __launch_bounds__(kSmallThreads) void quantize_small_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, float* __restrict__ tensor_scale,
     SrParams sr) {
-  __shared__ float2 tab[128];
+  __shared__ ScaleRecip tab[128];
   __shared__ uint32_t wave_max[kSmallThreads / 64];
   fill_scale_table(tab);
   auto block_ptr = [&](int64_t g) -> const uint16_t* {

@@ -52,7 +52,7 @@ __global__ __launch_bounds__(kThreads2d) void quantize_2d_kernel(
     const uint16_t* __restrict__ w, int64_t n, int64_t k, int64_t ldw,
     uint8_t* __restrict__ codes, uint8_t* __restrict__ scales, uint8_t* __restrict__ codes_t,
     uint8_t* __restrict__ scales_t, const float* __restrict__ tensor_scale) {
-  __shared__ float2 tab[128];
+  __shared__ ScaleRecip tab[128];
   __shared__ uint8_t tr[kThreads2d / 64][4][16][16];
   fill_scale_table(tab);
   __syncthreads();
@@ -119,7 +119,7 @@ __global__ __launch_bounds__(kThreads2d) void quantize_t_kernel(
     uint8_t* __restrict__ codes_t, uint8_t* __restrict__ scales_t,
     const float* __restrict__ tensor_scale, SrParams sr, HadamardParams hp,
     uint32_t* __restrict__ partials) {
-  __shared__ float2 tab[128];
+  __shared__ ScaleRecip tab[128];
   __shared__ uint16_t xt[kTileC][kPitch];
   __shared__ uint32_t wave_max[kThreads2d / 64];
   if constexpr (!kAmax) fill_scale_table(tab);

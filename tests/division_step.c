@@ -10,6 +10,13 @@
  *       tensor scale s32; X is bf16).
  * (C) signed zeros: a = +-0 returns a zero of the same sign, also with the
  *     zero divisor the kernel encodes as s = 0, r = 0.
+ * (D) the two-term reciprocal step for the block-scale divisors: with rh =
+ *     1 / s rounded toward zero and rl = fl32(fma(-rh, s, 1) / s) >= 0 (the
+ *     residual 1 - rh s is exact), q = fma(a, rh, fl32(a * rl)).  Every fp32 a
+ *     in [1, 2) against every divisor in [1, 2) with at most 4 significant
+ *     bits, and signed zeros (rl >= 0 gives both addends the sign of a; also
+ *     with the zero scale, rh = rl = 0).  Here the scaling argument
+ *     additionally needs a * rl to stay normal.
  * Exit status 0 iff every case equals the IEEE quotient (C's a / s, correctly
  * rounded to nearest even).  Built with -mfma so fmaf is one fused operation.
  */
@@ -35,6 +42,23 @@ static int same_as_ieee(float a, float s) {
   volatile float r = 1.0f / s;
   volatile float want = a / s;
   return to_bits(step(a, s, r)) == to_bits(want);
+}
+
+static float step2(float a, float rh, float rl) {
+  volatile float t = a * rl;
+  return fmaf(a, rh, t);
+}
+
+/* rh = 1 / s rounded toward zero, rl = the remainder (1 - rh s) / s >= 0 */
+static void two_term_reciprocal(float s, float* rh, float* rl) {
+  volatile float h = 1.0f / s;
+  volatile float e = fmaf(-h, s, 1.0f);
+  if (e < 0.0f) {
+    h = from_bits(to_bits(h) - 1u);
+    e = fmaf(-h, s, 1.0f);
+  }
+  *rh = h;
+  *rl = e / s;
 }
 
 typedef struct { uint32_t lo, hi; long bad; } range_t;
@@ -80,8 +104,27 @@ int main(void) {
     const float a = dividends[i], q = step(a, 0.0f, 0.0f);
     if (q != 0.0f || signbit(q) != signbit(a)) bad_c++;
   }
+  long bad_d = 0;
+  for (uint32_t m = 0; m < 8; ++m) {
+    const float s = 1.0f + (float)m / 8.0f;
+    float rh, rl;
+    two_term_reciprocal(s, &rh, &rl);
+    if (rl < 0.0f || signbit(rl)) bad_d++;
+    for (uint32_t am = 0; am < (1u << 23); ++am) {
+      const float a = from_bits(0x3F800000u | am);
+      volatile float want = a / s;
+      if (to_bits(step2(a, rh, rl)) != to_bits(want)) bad_d++;
+    }
+    if (to_bits(step2(0.0f, rh, rl)) != 0u) bad_d++;
+    if (to_bits(step2(-0.0f, rh, rl)) != 0x80000000u) bad_d++;
+  }
+  for (unsigned i = 0; i < sizeof dividends / sizeof dividends[0]; ++i) {
+    const float a = dividends[i], q = step2(a, 0.0f, 0.0f);
+    if (q != 0.0f || signbit(q) != signbit(a)) bad_d++;
+  }
   printf("A: %ld of %ld mismatched\n", bad_a, 8L << 23);
   printf("B: %ld of %ld mismatched\n", bad_b, 128L << 23);
   printf("C: %ld signed-zero mismatches\n", bad_c);
-  return (bad_a || bad_b || bad_c) ? 1 : 0;
+  printf("D: %ld of %ld mismatched (two-term reciprocal)\n", bad_d, 8L << 23);
+  return (bad_a || bad_b || bad_c || bad_d) ? 1 : 0;
 }

@@ -1,7 +1,9 @@
-"""The quantizer divides in fp32 with one multiply and two fmas instead of a
-division (x = X / s32 and y = x / s_block).  tests/division_step.c proves on
-the CPU, exhaustively over the operand mantissas the kernel can see, that
-this gives the IEEE quotient bit for bit, and that zeros keep their sign."""
+"""The quantizer divides in fp32 without a divide instruction: x = X / s32
+with one multiply and two fmas on a correctly rounded reciprocal, and the
+quotients by the block scales (and by 6 and 7) with a multiply and one fma
+on a two-term reciprocal.  tests/division_step.c proves on the CPU,
+exhaustively over the operand mantissas the kernel can see, that both give
+the IEEE quotient bit for bit, and that zeros keep their sign."""
 import os
 import shutil
 import subprocess
@@ -22,3 +24,4 @@ def test_division_step_exhaustive():
     print(r.stdout)
     assert r.returncode == 0, r.stdout + r.stderr
     assert "A: 0 of" in r.stdout and "B: 0 of" in r.stdout and "C: 0 " in r.stdout
+    assert "D: 0 of" in r.stdout
