@@ -97,6 +97,24 @@ __device__ __forceinline__ void to_fp8_domain(uint4 v0, uint4 v1, float xmul, fl
   }
 }
 
+// x = fl32(X / s32) for the 16 elements of a block from the two-term
+// reciprocal of s32 (div_scale).  s32 has 24 significant bits, so this is
+// exact only for tensor scales that pass the per-launch check in
+// quantize_kernel: every one of the 128 bf16 mantissas divided this way
+// gives Markstein's (exact) quotient.  Scaling X by a power of two scales
+// both steps exactly while x and X * rl stay normal, which covers every x
+// at or above 2^-78; smaller elements receive zero codes with X's sign (kept:
+// rl >= 0) whatever their exact value, and contribute nothing to the errors.
+__device__ __forceinline__ void to_fp8_domain_two_term(uint4 v0, uint4 v1, float rh, float rl,
+                                                       float (&xs)[16]) {
+  const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    xs[2 * i] = div_scale(bf16_lo(w[i]), rh, rl);
+    xs[2 * i + 1] = div_scale(bf16_hi(w[i]), rh, rl);
+  }
+}
+
 // Elements J, J+1 (J even) of a block, E2M1 branch: y = fl32(x / s_F)
 // rounded by the gfx950 FP4 converter (scale 1: nearest, ties to the even
 // code, saturating at 6, sign kept) into nibble pair (J%8)/2 of pf[J/8].

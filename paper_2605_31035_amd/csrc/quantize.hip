@@ -103,22 +103,30 @@ __global__ void finalize_scale(uint32_t* p) {
   *reinterpret_cast<float*>(p) = tensor_scale_of(*p >> 16);
 }
 
+// The FP8 domain x = fl32(X / s32): kTwoTerm from the two-term reciprocal
+// {rh, rl} of s32 (tensor scales that passed the check below), otherwise
+// X * xmul (exact) divided by sx = s32 * xmul with Markstein's step on
+// rx = fl32(1 / sx).
+struct XDomain {
+  float xmul, sx, rx, rh, rl;
+};
+
 // Grid-stride walk over the blocks.  The next block of this thread is
 // loaded as soon as the current one has been turned into x, so its load
-// overlaps this block's arithmetic (measured: a second block in flight, or
-// more waves per SIMD, gains nothing; the kernel is bound by VALU issue).
+// overlaps this block's arithmetic (measured: two or three blocks in flight
+// per thread, at the lower occupancy their registers allow, are no faster).
 //
 // kSR: stochastic rounding with Philox draws per block (its global index).
 // kHad: each block is first rotated (block-diagonal Hadamard across the
 // L = b / 16 lanes holding one Hadamard block; the grid stride is a multiple
 // of 256, so a thread keeps its position in its Hadamard block and every
 // Hadamard block is processed by lanes of one wave in one iteration).
-template <bool kContig, bool kScaled, int kMode, bool kSR, bool kHad>
+template <bool kContig, bool kTwoTerm, int kMode, bool kSR, bool kHad>
 __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, int64_t nbk,
                                               int64_t ldx, int64_t nblocks,
                                               uint8_t* __restrict__ codes,
-                                              uint8_t* __restrict__ scales, float xmul, float sx,
-                                              float rx, const ScaleRecip* tab, const SrParams& sr,
+                                              uint8_t* __restrict__ scales, const XDomain& xd,
+                                              const ScaleRecip* tab, const SrParams& sr,
                                               const HadamardParams& hp) {
   const int64_t stride = (int64_t)gridDim.x * blockDim.x;
   // Loads are unconditional (a block index past the end reads the last
@@ -143,13 +151,12 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
   load(g, a0, a1);
   for (; g < nblocks; g += stride) {
     float xs[16];
-    if constexpr (kHad) {
-      uint4 r0 = a0, r1 = a1;
-      hadamard_rotate(r0, r1, sm, hp);
-      to_fp8_domain<kScaled>(r0, r1, xmul, sx, rx, xs);
-    } else {
-      to_fp8_domain<kScaled>(a0, a1, xmul, sx, rx, xs);
-    }
+    uint4 r0 = a0, r1 = a1;
+    if constexpr (kHad) hadamard_rotate(r0, r1, sm, hp);
+    if constexpr (kTwoTerm)
+      to_fp8_domain_two_term(r0, r1, xd.rh, xd.rl, xs);
+    else
+      to_fp8_domain<true>(r0, r1, xd.xmul, xd.sx, xd.rx, xs);
     load(g + stride, a0, a1);
     uint2 out;
     uint32_t sb;
@@ -162,25 +169,11 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
 // Quantize blocks [this thread's grid-stride share] with tensor scale s32.
 // The division steps stay in the normal range for every element that can get
 // a nonzero code when 2^-90 <= s32 <= 2^120; beyond that both X and s32 are
-// rescaled by 2^64 or 2^-64 first.
-template <bool kContig, int kMode, bool kSR, bool kHad>
-__device__ __forceinline__ void quantize_all(const uint16_t* __restrict__ x, int64_t nbk,
-                                             int64_t ldx, int64_t nblocks,
-                                             uint8_t* __restrict__ codes,
-                                             uint8_t* __restrict__ scales, float s32,
-                                             const ScaleRecip* tab, const SrParams& sr,
-                                             const HadamardParams& hp) {
-  if (s32 >= 0x1p-90f && s32 <= 0x1p120f) {
-    quantize_loop<kContig, false, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, 1.0f,
-                                                    s32, __fdiv_rn(1.0f, s32), tab, sr, hp);
-  } else {
-    const float xmul = s32 < 1.0f ? 0x1p64f : 0x1p-64f;
-    const float sx = s32 * xmul;
-    quantize_loop<kContig, true, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xmul, sx,
-                                                   __fdiv_rn(1.0f, sx), tab, sr, hp);
-  }
-}
-
+// rescaled by 2^64 or 2^-64 first.  Within that range, the two-term division
+// is used when it reproduces the exact quotient on all 128 bf16 mantissas
+// (checked by the first 128 threads of every workgroup, so every workgroup
+// takes the same, deterministic decision); the kernel's barrier publishes
+// the check and the scale table together.
 template <bool kContig, int kMode, bool kSR, bool kHad>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
@@ -188,9 +181,28 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const float* __restrict__ tensor_scale, SrParams sr, HadamardParams hp) {
   __shared__ ScaleRecip tab[128];
   fill_scale_table(tab);
-  __syncthreads();
-  quantize_all<kContig, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, *tensor_scale, tab,
-                                          sr, hp);
+  const float s32 = *tensor_scale;
+  const bool direct = s32 >= 0x1p-90f && s32 <= 0x1p120f;
+  XDomain xd;
+  xd.xmul = direct ? 1.0f : (s32 < 1.0f ? 0x1p64f : 0x1p-64f);
+  xd.sx = s32 * xd.xmul;
+  xd.rx = __fdiv_rn(1.0f, xd.sx);
+  const ScaleRecip r32 = scale_recip(s32);
+  xd.rh = r32.rh;
+  xd.rl = r32.rl;
+  int ok = 1;
+  if (direct && threadIdx.x < 128) {
+    // mantissa t at the exponent of s32, so that the quotient is near 1
+    const float xt = __uint_as_float((__float_as_uint(s32) & 0x7F800000u) | (threadIdx.x << 16));
+    ok = __float_as_uint(div_rn(xt, xd.sx, xd.rx)) == __float_as_uint(div_scale(xt, xd.rh, xd.rl));
+  }
+  const bool two_term = __syncthreads_and(ok) && direct;
+  if (two_term)
+    quantize_loop<kContig, true, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xd, tab,
+                                                   sr, hp);
+  else
+    quantize_loop<kContig, false, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xd, tab,
+                                                    sr, hp);
 }
 
 // Small tensors with the tensor scale computed (at most kSmallElems

@@ -17,8 +17,15 @@
  *     bits, and signed zeros (rl >= 0 gives both addends the sign of a; also
  *     with the zero scale, rh = rl = 0).  Here the scaling argument
  *     additionally needs a * rl to stay normal.
- * Exit status 0 iff every case equals the IEEE quotient (C's a / s, correctly
- * rounded to nearest even).  Built with -mfma so fmaf is one fused operation.
+ * (E) the same two-term step for the tensor scale (X / s32, X bf16): s32 has
+ *     24 significant bits and the step is not exact for every pair, so the
+ *     kernel checks the 128 bf16 mantissas against s32 at launch and falls
+ *     back to Markstein's step when one differs.  This part lists every fp32
+ *     s32 in [1, 2) with such a mantissa (and the mantissas), which the GPU
+ *     tests use to drive the fallback; it is a census, not a pass/fail check.
+ * Exit status 0 iff every case of (A)-(D) equals the IEEE quotient (C's a / s,
+ * correctly rounded to nearest even).  Built with -mfma so fmaf is one fused
+ * operation.
  */
 #include <math.h>
 #include <pthread.h>
@@ -62,6 +69,28 @@ static void two_term_reciprocal(float s, float* rh, float* rl) {
 }
 
 typedef struct { uint32_t lo, hi; long bad; } range_t;
+
+enum { kMaxCensus = 64 };
+typedef struct { uint32_t lo, hi; int n; uint32_t s[kMaxCensus], a[kMaxCensus]; } census_t;
+
+static void* part_e(void* p) {
+  census_t* j = (census_t*)p;
+  for (uint32_t sm = j->lo; sm < j->hi; ++sm) {
+    const float s = from_bits(0x3F800000u | sm);
+    float rh, rl;
+    two_term_reciprocal(s, &rh, &rl);
+    for (uint32_t am = 0; am < 128; ++am) {
+      const float a = from_bits(0x3F800000u | (am << 16));
+      volatile float want = a / s;
+      if (to_bits(step2(a, rh, rl)) != to_bits(want) && j->n < kMaxCensus) {
+        j->s[j->n] = to_bits(s);
+        j->a[j->n] = to_bits(a);
+        j->n++;
+      }
+    }
+  }
+  return NULL;
+}
 
 static void* part_b(void* p) {
   range_t* j = (range_t*)p;
@@ -126,5 +155,20 @@ int main(void) {
   printf("B: %ld of %ld mismatched\n", bad_b, 128L << 23);
   printf("C: %ld signed-zero mismatches\n", bad_c);
   printf("D: %ld of %ld mismatched (two-term reciprocal)\n", bad_d, 8L << 23);
+  census_t cj[kThreads];
+  for (int i = 0; i < kThreads; ++i) {
+    cj[i].lo = (1u << 23) / kThreads * (uint32_t)i;
+    cj[i].hi = (1u << 23) / kThreads * (uint32_t)(i + 1);
+    cj[i].n = 0;
+    pthread_create(&t[i], NULL, part_e, &cj[i]);
+  }
+  int n_e = 0;
+  for (int i = 0; i < kThreads; ++i) {
+    pthread_join(t[i], NULL);
+    n_e += cj[i].n;
+  }
+  printf("E: %d tensor-scale pairs take the fallback\n", n_e);
+  for (int i = 0; i < kThreads; ++i)
+    for (int k = 0; k < cj[i].n; ++k) printf("E s32 0x%08x X 0x%08x\n", cj[i].s[k], cj[i].a[k]);
   return (bad_a || bad_b || bad_c || bad_d) ? 1 : 0;
 }

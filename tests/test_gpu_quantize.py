@@ -85,6 +85,25 @@ def test_extreme_tensor_scales(exp, s32):
     _assert_same(bits, s32=given, label=f"2^{exp} data")
 
 
+@pytest.mark.parametrize("exp", [-20, 0, 7])
+def test_tensor_scale_fallback(exp):
+    """The tensor scales on which the two-term division misses the exact
+    quotient for one bf16 mantissa (census in test_division_step): the
+    launch-time check must route them to Markstein's step.  Each tensor holds
+    that mantissa at several exponents and both signs, among adversarial
+    blocks."""
+    from tests.test_division_step import FALLBACK_PAIRS
+    for s_bits, x_bits in FALLBACK_PAIRS:
+        s32 = np.float32(np.uint32(s_bits).view(np.float32) * np.float32(2.0 ** exp))
+        a = np.uint32(x_bits).view(np.float32) * np.float32(2.0 ** exp)
+        bits = W.adversarial(s_bits & 0xFFFF, 24, 64)
+        special = np.array([a * np.float32(2.0 ** j) * sg for j in range(-4, 4) for sg in (1, -1)],
+                           np.float32)
+        bits[:, 0] = W.f32_to_bf16_bits(special[np.arange(24) % 16])
+        bits[::3, 16:32] = W.f32_to_bf16_bits(special)
+        _assert_same(bits, s32=s32, label=f"fallback s32=0x{s_bits:08x}*2^{exp}")
+
+
 @pytest.mark.parametrize("rows,k,pad", [(64, 4096, 0), (65, 4096, 0), (1, 1 << 18, 0),
                                         (16, 8192, 0), (3, 48, 8), (100, 1024, 64)])
 def test_small_and_large_compute_paths(rows, k, pad):
