@@ -122,6 +122,20 @@ def cpu_baseline(wl, budget_s: float = 10.0, max_reps: int = 8) -> dict:
     }
 
 
+def spin_up(torch, fn, seconds: float = 0.2) -> None:
+    """Call fn back to back for about `seconds` before a timed region.  The
+    GPU lowers its clocks when idle (the workloads are generated on the host
+    between measurements) and takes tens of milliseconds of load to raise
+    them again; measured on MI355X, a 2^28-element quantize takes ~170 us
+    from idle and ~147 us at speed, and the prefill step 0.367 against
+    0.333 ms.  Untimed, like every warmup."""
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            fn()
+        torch.cuda.synchronize()
+
+
 def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
     """Quantize-only throughput on the standalone tensor Q [16384, 16384]
     (2^28 elements, seed 4 block mixture).  The kernel alone: tensor scale
@@ -142,9 +156,7 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
                          .astype(np.int8), device=dev)
 
     def time_calls(fn) -> float:
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
+        spin_up(torch, fn, 0.15)
         e = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)]
         e[0].record()
         for i in range(iters):
@@ -224,6 +236,12 @@ def measure_decode(M, torch, dev, iters: int = 50) -> dict:
           torch.empty(1, dtype=torch.float32, device=dev))
     out = torch.empty((r, qw[0].shape[0]), dtype=torch.float32, device=dev)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(iters)]
+
+    def decode_step():
+        M.mixfp4_quantize(xa, None, qa[0], qa[1], scale_out=qa[2])
+        M.mixfp4_gemm(qa, qw, out=out)
+
+    spin_up(torch, decode_step)
     for i in range(5 + iters):
         e = ev[i - 5] if i >= 5 else None
         if e:
@@ -309,9 +327,7 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
         M.mixfp4_gemm(qgt, qxt)
         mark(8)
 
-    for i in range(3):
-        step(it=i)
-    torch.cuda.synchronize()
+    spin_up(torch, step, 0.3)
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(iters)]
     t0 = time.perf_counter()
     for i in range(iters):
@@ -342,7 +358,9 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    # 300 prefill steps (~0.1 s): the clocks reach their loaded level (see
+    # spin_up); fewer warmup steps measure a partly idle GPU
+    ap.add_argument("--warmup", type=int, default=300)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-decode", action="store_true",
                     help="skip the extra decode-shape (m = 16) measurement")

@@ -345,9 +345,10 @@ __global__ __launch_bounds__(kThreads) void hadamard_kernel(const uint16_t* __re
 }
 
 // Workgroups of kThreads that the device keeps resident at once for
-// `kernel` (occupancy per CU x CU count); `cache` holds one value per device.
+// `kernel` (occupancy per CU x CU count), at most max_per_cu per CU when that
+// is positive; `cache` holds one value per device.
 template <typename Kernel>
-int64_t resident_groups(Kernel kernel, int64_t (&cache)[64]) {
+int64_t resident_groups(Kernel kernel, int64_t (&cache)[64], int max_per_cu = 0) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
   if (!cache[dev]) {
@@ -355,6 +356,7 @@ int64_t resident_groups(Kernel kernel, int64_t (&cache)[64]) {
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess ||
         per_cu <= 0)
       per_cu = 4;
+    if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cus <= 0)
       cus = 256;
@@ -468,14 +470,25 @@ hipError_t launch_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, 
                        hipStream_t stream) {
   const int64_t nbk = k / kBlock;
   const int64_t nblocks = rows * nbk;
-  // One wave of resident workgroups (occupancy x CUs) walks all blocks, so
-  // no partial second wave is left at the end; fewer if the tensor is small.
-  static int64_t cache_c[64], cache_s[64];
+  // A tensor that one round of resident workgroups covers gets one block per
+  // thread.  Larger ones are walked by a persistent grid, one wave of
+  // resident workgroups, so no partial second wave is left at the end, with
+  // at most kMaxPerCU workgroups per CU.  The single-format encodings do
+  // little arithmetic per byte and stream HBM better with fewer resident
+  // waves than their registers allow (measured on the 2^28 tensor: E2M1-only
+  // at 3 workgroups per CU takes 118 us against 137 us at 8; E1M2-only is
+  // best at 4).  For the other modes 4 to 8 measure the same; they take 6.
+  constexpr int kMaxPerCU = kMode == kForceE2M1 ? 3 : (kMode == kForceE1M2 ? 4 : 6);
+  static int64_t cache_c[64], cache_s[64], capped_c[64], capped_s[64];
   const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
+  const bool contig = ldx == k;
   const int64_t resident =
-      ldx == k ? resident_groups(quantize_kernel<true, kMode, kSR, kHad>, cache_c)
-               : resident_groups(quantize_kernel<false, kMode, kSR, kHad>, cache_s);
-  const int g = (int)(wanted < resident ? wanted : resident);
+      contig ? resident_groups(quantize_kernel<true, kMode, kSR, kHad>, cache_c)
+             : resident_groups(quantize_kernel<false, kMode, kSR, kHad>, cache_s);
+  const int64_t capped =
+      contig ? resident_groups(quantize_kernel<true, kMode, kSR, kHad>, capped_c, kMaxPerCU)
+             : resident_groups(quantize_kernel<false, kMode, kSR, kHad>, capped_s, kMaxPerCU);
+  const int g = (int)(wanted <= resident ? wanted : capped);
   if (ldx == k)
     quantize_kernel<true, kMode, kSR, kHad><<<g, kThreads, 0, stream>>>(
         x, nbk, ldx, nblocks, codes, scales, tensor_scale, opt.srp, opt.hp);
