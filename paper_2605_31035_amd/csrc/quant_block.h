@@ -229,22 +229,28 @@ __device__ __forceinline__ void encode_i_saturated(const float (&xs)[16], const 
 __device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], const ScaleRecip& sc, bool int4,
                                           uint4 rnd) {
   const uint32_t words[4] = {rnd.x, rnd.y, rnd.z, rnd.w};
+  // Branch-free lattice choice (a per-lane select, not control flow): E2M1
+  // spacing 2^(t-1) with t = clamp(exponent of y, 0, 2), so z = y 2^(1-t)
+  // exactly and the lattice point below y is code floor(z) + 2t; E1M2 (x2)
+  // spacing 1, z = y, code floor(z).
+  const int keep = int4 ? 0 : -1;                    // all ones on the E2M1 lattice
+  const float top = int4 ? 7.0f : 6.0f;
   uint32_t o[2] = {0u, 0u};
 #pragma unroll
   for (int j = 0; j < 16; ++j) {
     const uint32_t xb = __float_as_uint(xs[j]);
     const uint32_t neg = xb >> 31;
     const float y = div_scale(__uint_as_float(xb & 0x7FFFFFFFu), sc.rh, sc.rl);
-    const uint32_t u = ((words[j >> 2] >> (8 * (j & 3))) & 0xFFu) ^ (neg ? 0xFFu : 0u);
-    const float thr = (float)(511 - 2 * (int)u);
-    const float inv_d = int4 ? 1.0f : (y < 2.0f ? 2.0f : (y < 4.0f ? 1.0f : 0.5f));
-    const uint32_t base = int4 ? 0u : (y < 2.0f ? 0u : (y < 4.0f ? 2u : 4u));
-    const float z = y * inv_d;
+    const int e = (int)(__float_as_uint(y) >> 23) - 127;
+    const int t = min(max(e, 0), 2);
+    const float z = __builtin_ldexpf(y, (1 - t) & keep);
     const float lat = floorf(z);
     const float w = (z - lat) * 512.0f;
-    uint32_t code = (uint32_t)lat + base;
-    code += (w > thr || (w == thr && (code & 1u))) ? 1u : 0u;
-    code = y >= (int4 ? 7.0f : 6.0f) ? 7u : code;
+    const uint32_t u = ((words[j >> 2] >> (8 * (j & 3))) & 0xFFu) ^ (0xFFu & (0u - neg));
+    const float thr = (float)(511 - 2 * (int)u);
+    uint32_t code = (uint32_t)lat + (uint32_t)((2 * t) & keep);
+    code += ((uint32_t)(w > thr) | ((uint32_t)(w == thr) & code)) & 1u;
+    code = y >= top ? 7u : code;
     o[j >> 3] |= (code | (neg << 3)) << (4 * (j & 7));
   }
   return make_uint2(o[0], o[1]);
