@@ -11,10 +11,12 @@ timing starts.
 
 Prints ONE JSON line:
   value         GEMM FLOPs of the step / step time (TFLOP/s; the activation
-                quantizer is inside the step time)
+                quantizer is inside the step time), from K steps timed
+                wall-clock between device synchronizations
   roofline      the dominant kernel, the GEMM C1 = A W1^T, against the dense
-                fp16 MFMA peak (its operands are exact fp16 values): its FLOPs per launch over its mean launch time,
-                timed with HIP events on the stream it runs on
+                fp16 MFMA peak (its operands are exact fp16 values): its FLOPs
+                per launch over its mean launch time, timed with HIP events on
+                the stream it runs on during a second pass of the same K steps
   gemm2         the same for C2 = A W2^T
   quantize      the quantizer kernel on the standalone 2^28-element tensor
                 (seed 4 block mixture) against HBM, with the tensor scale given
@@ -156,14 +158,16 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
                          .astype(np.int8), device=dev)
 
     def time_calls(fn) -> float:
+        # `iters` back-to-back calls between two HIP events (an event between
+        # calls would add its own ~3.5 us to every span)
         spin_up(torch, fn, 0.15)
-        e = [torch.cuda.Event(enable_timing=True) for _ in range(iters + 1)]
-        e[0].record()
-        for i in range(iters):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
             fn()
-            e[i + 1].record()
+        e1.record()
         torch.cuda.synchronize()
-        return float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(iters)]))
+        return e0.elapsed_time(e1) / iters
 
     def timed(given: bool, mode: str = "mixfp4", **kw) -> float:
         return time_calls(lambda: M.mixfp4_quantize(xq, s32 if given else None, codes, scales,
@@ -264,6 +268,13 @@ def measure_decode(M, torch, dev, iters: int = 50) -> dict:
     b1.record()
     torch.cuda.synchronize()
     g_ms = b0.elapsed_time(b1) / iters
+    # the whole decode step (quantize A, then the GEMM), steps back to back
+    b0.record()
+    for _ in range(iters):
+        decode_step()
+    b1.record()
+    torch.cuda.synchronize()
+    st_ms = b0.elapsed_time(b1) / iters
     n = qw[0].shape[0]
     gemm_bytes = n * k / 2 + n * k / 16 + r * k / 2 + r * k / 16 + r * n * 4
     return {
@@ -275,9 +286,10 @@ def measure_decode(M, torch, dev, iters: int = 50) -> dict:
         "gemm_hbm_frac": round(gemm_bytes / (g_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
         "gemm_TFLOPs": round(2.0 * r * n * k / (g_ms * 1e-3) / 1e12, 2),
         "gemm_in_step_us": round(step_g_ms * 1e3, 2),
-        "step_us": round((q_ms + step_g_ms) * 1e3, 2),
-        "timing": "gemm_us: mean of back-to-back GEMM launches; step_us: quantize A then "
-                  "GEMM per step (includes the dispatch gap between the two kernels)",
+        "step_us": round(st_ms * 1e3, 2),
+        "timing": "gemm_us: back-to-back GEMM launches; step_us: back-to-back steps of quantize "
+                  "A then GEMM (dispatch gaps included); quantize_a_us and gemm_in_step_us: HIP "
+                  "event spans around each launch of a separate pass of steps",
     }
 
 
@@ -328,12 +340,16 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
         mark(8)
 
     spin_up(torch, step, 0.3)
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(iters)]
+    # step time without events, then the per-launch spans in a second pass
     t0 = time.perf_counter()
+    for i in range(iters):
+        step(None, i)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / iters
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(9)] for _ in range(iters)]
     for i in range(iters):
         step(ev[i], i)
     torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / iters
     spans = [float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev])) for j in range(8)]
     flops = 2.0 * tok * d_in * d_out
     out = {
@@ -425,14 +441,22 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
-    torch.cuda.synchronize()
+    # The value: K steps with nothing but the path on the stream.
     t0 = time.perf_counter()
     for i in range(args.steps):
-        step(marks[i])
+        step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     ms_step = (t1 - t0) * 1e3 / args.steps
+    # The per-kernel spans (roofline, gemm2, quantize_step): the same K steps
+    # again, right after, with HIP events on the launching stream around every
+    # launch.  Each event record adds ~3.5 us of GPU time to a step (measured:
+    # 312 us per step without events, 326 us with four), which is why the
+    # value's pass has none; an event does not change the kernel it brackets.
+    marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(marks[i])
+    torch.cuda.synchronize()
     span = lambda a, b: float(np.mean([m[a].elapsed_time(m[b]) for m in marks]))  # noqa: E731
     q_ms, g1_ms, g2_ms = span(0, 1), span(1, 2), span(2, 3)
 
