@@ -35,6 +35,28 @@ struct QuantOptions {
   HadamardParams hp{};
 };
 
+// Workgroups of `threads` threads that the device keeps resident at once for
+// `kernel` (occupancy per CU x CU count), at most max_per_cu per CU when that
+// is positive; `cache` holds one value per device.
+template <typename Kernel>
+int64_t resident_groups(Kernel kernel, int64_t (&cache)[64], int max_per_cu = 0,
+                        int threads = 256) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
+  if (!cache[dev]) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
+        per_cu <= 0)
+      per_cu = 4;
+    if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus <= 0)
+      cus = 256;
+    cache[dev] = (int64_t)per_cu * cus;
+  }
+  return cache[dev];
+}
+
 // Launchers: shapes are validated by the ABI layer before these are called.
 // Tensor scale s32 = max|X| / 2688 (1.0 for all-zero X) into *tensor_scale.
 // `scratch` (may be NULL) is device memory of `scratch_bytes` that the call

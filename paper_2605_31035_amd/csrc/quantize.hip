@@ -344,27 +344,6 @@ __global__ __launch_bounds__(kThreads) void hadamard_kernel(const uint16_t* __re
   }
 }
 
-// Workgroups of kThreads that the device keeps resident at once for
-// `kernel` (occupancy per CU x CU count), at most max_per_cu per CU when that
-// is positive; `cache` holds one value per device.
-template <typename Kernel>
-int64_t resident_groups(Kernel kernel, int64_t (&cache)[64], int max_per_cu = 0) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
-  if (!cache[dev]) {
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kThreads, 0) != hipSuccess ||
-        per_cu <= 0)
-      per_cu = 4;
-    if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus <= 0)
-      cus = 256;
-    cache[dev] = (int64_t)per_cu * cus;
-  }
-  return cache[dev];
-}
-
 int grid_for(int64_t work, int per_thread) {
   int64_t g = (work + (int64_t)kThreads * per_thread - 1) / ((int64_t)kThreads * per_thread);
   if (g < 1) g = 1;

@@ -86,6 +86,33 @@ def test_quantize_2d_full_size():
     np.testing.assert_array_equal(host(ct), ref.codes_t)
 
 
+def test_quantize_2d_many_super_blocks():
+    """W [8448, 8192]: 66 x 64 = 4224 super-blocks of 128 x 128 elements, more
+    than the 4096 workgroups of the launch, so the workgroups that take the
+    last 256 rows do so in a second super-block.  Tiles are independent for a
+    given s32, so the oracle quantizes three 256-row bands (first, middle,
+    last) and both layouts are compared there."""
+    import paper_2605_31035_amd as M
+    n, k = 8448, 8192
+    rng = np.random.default_rng(23)
+    x = rng.standard_normal((n, k), dtype=np.float32)
+    x *= np.float32(0.02)
+    bits = W.f32_to_bf16_bits(x)
+    del x
+    s32 = np.float32(0.1 / 2688)   # a few elements saturate at 6 * 448 * s32
+    log(f"2d {n}x{k} s32={s32} sampled bands")
+    (c, s, _), (ct, st, _) = M.mixfp4_quantize_2d(dev_bf16(bits), dev_f32(s32))
+    torch.cuda.synchronize()
+    c, s, ct, st = host(c), host(s), host(ct), host(st)
+    for r0 in (0, 4096, n - 256):
+        ref = Q.quantize_2d(bits[r0:r0 + 256], s32=s32)
+        label = f"band rows {r0}..{r0 + 256}"
+        np.testing.assert_array_equal(s[r0:r0 + 256], ref.scales, err_msg=label)
+        np.testing.assert_array_equal(c[r0:r0 + 256], ref.codes, err_msg=label)
+        np.testing.assert_array_equal(st[:, r0 // 16:(r0 + 256) // 16], ref.scales_t, err_msg=label)
+        np.testing.assert_array_equal(ct[:, r0 // 2:(r0 + 256) // 2], ref.codes_t, err_msg=label)
+
+
 # ---------------------------------------------------------------- transposed quantization
 
 def _ref_t(bits, s32, omode, rounding, seed, offset, b, signs):
