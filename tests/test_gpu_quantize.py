@@ -105,7 +105,8 @@ def test_tensor_scale_fallback(exp):
 
 
 @pytest.mark.parametrize("rows,k,pad", [(64, 4096, 0), (65, 4096, 0), (1, 1 << 18, 0),
-                                        (16, 8192, 0), (3, 48, 8), (100, 1024, 64)])
+                                        (16, 8192, 0), (3, 48, 8), (100, 1024, 64),
+                                        (2049, 8192, 0)])
 def test_small_and_large_compute_paths(rows, k, pad):
     """Tensors of at most 2^18 elements get their tensor scale and codes in one
     launch (every workgroup reduces max|X| itself); larger ones take the
@@ -113,6 +114,40 @@ def test_small_and_large_compute_paths(rows, k, pad):
     rows included, must give the oracle's bits."""
     bits = W.adversarial(rows * 7 + k, rows, k)
     _assert_same(bits, ldx_pad=pad, label=f"compute path {rows}x{k}")
+
+
+@pytest.mark.parametrize("mode,omode", [("mixfp4", "select"), ("e2m1", "e2m1"),
+                                        ("e1m2", "e1m2"), ("four_six", "four_six")])
+@pytest.mark.parametrize("rounding", ["nearest", "stochastic"])
+@pytest.mark.parametrize("rows,k,pad", [(65, 4096, 0), (601, 1008, 24), (4096, 4096, 0)])
+def test_compute_mode_matrix(mode, omode, rounding, rows, k, pad):
+    """The amax / reduce / quantize sequence (tensor scale computed, above the
+    one-launch size): every format mode and both roundings, ragged block
+    counts and strided rows; 4096 x 4096 has more blocks than resident
+    threads, so each thread takes several (checked on sampled rows there, in
+    full elsewhere)."""
+    import paper_2605_31035_amd as M
+    bits = W.adversarial(rows + 5 * k, rows, k)
+    label = f"compute {mode} {rounding} {rows}x{k} pad={pad}"
+    log(label)
+    x = dev_bf16(bits)
+    if pad:
+        big = torch.zeros((rows, k + pad), dtype=torch.bfloat16, device="cuda")
+        big[:, :k] = x
+        x = big[:, :k]
+    seed = 0x5EED0F05ED
+    codes, scales, s = M.mixfp4_quantize(x, mode=mode, rounding=rounding, seed=seed, offset=3)
+    torch.cuda.synchronize()
+    s_ref = Q.tensor_scale(bits)
+    assert host(s)[0] == s_ref, label
+    sel = np.arange(rows) if rows * k <= (1 << 20) else _sampled_rows(np.random.default_rng(1), rows)
+    # the selected rows with the full tensor's s32, numbered as in the full
+    # tensor (stochastic rounding draws by block index)
+    ref = Q.quantize(bits[sel], s32=s_ref, mode=omode, rounding=rounding, seed=seed, offset=3,
+                     row_index=sel)
+    idx = torch.from_numpy(sel).to("cuda")
+    np.testing.assert_array_equal(host(scales.index_select(0, idx)), ref.scales, err_msg=label)
+    np.testing.assert_array_equal(host(codes.index_select(0, idx)), ref.codes, err_msg=label)
 
 
 @pytest.mark.parametrize("mode", ["e2m1", "e1m2", "four_six"])
