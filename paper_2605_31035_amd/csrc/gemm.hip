@@ -336,52 +336,55 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // ---------------------------------------------------------------------------
 // Decode-shape GEMM (m <= 16): HBM-bound, W is read once.
 //
-// A workgroup owns 64 columns of C and splits K over its kW waves (4, or 2
-// when k is not a multiple of 1024); each wave walks its K range in steps of
-// 256 with no barrier and no LDS until the end.  Lane (nn, g) = (lane % 16,
-// lane / 16) owns W rows nn + 16 c (c < 4, one per 16-column MFMA group) and
-// the quarter [64 g, 64 g + 64) of every step: per row 32 code bytes and 4
-// scale bytes, loaded one step ahead.  It decodes them straight into the B
-// operands of v_mfma_f32_16x16x32_f16, and decodes its own A operand -- A
-// row nn, the same 64 elements -- once per step for all four column groups
-// (A's decode is a quarter of W's).  MFMA i of a 32-element group takes
-// elements 8 i + j in K slot (g, j); A and W use the same order.  The waves'
-// partial sums are added through LDS in a fixed order at the end.
+// A workgroup owns 16 kCG columns of C (kCG = 4, 2 or 1 MFMA column groups)
+// and splits K over its kW waves (4, or 2 when k is not a multiple of 1024);
+// each wave walks its K range in steps of 256 with no barrier and no LDS
+// until the end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
+// nn + 16 c (c < kCG, one per 16-column group) and the quarter
+// [64 g, 64 g + 64) of every step: per row 32 code bytes and 4 scale bytes,
+// loaded one step ahead.  It decodes them straight into the B operands of
+// v_mfma_f32_16x16x32_f16, and decodes its own A operand -- A row nn, the
+// same 64 elements -- once per step for all its column groups.  MFMA i of a
+// 32-element group takes elements 8 i + j in K slot (g, j); A and W use the
+// same order.  The waves' partial sums are added through LDS in a fixed
+// order at the end, so every column's sum is formed in the same order
+// whatever kCG is.
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kSkinnyRows = 16;
-constexpr int kSkinnyCols = 64;                    // columns of C per workgroup
 constexpr int kSkinnyStep = 256;                   // K per wave step
 constexpr int kSkinnyVec = kSkinnyStep / 128;      // 16-byte code loads per row per lane per step
 constexpr int kSkinnySw = kSkinnyStep / 256;       // scale dwords per row per lane per step
 
+template <int kCG>
 struct WPack {
-  uint4 c[4][kSkinnyVec];       // 4 rows x 64 codes
-  uint32_t s[4][kSkinnySw];     // their scale bytes
+  uint4 c[kCG][kSkinnyVec];     // kCG rows x 64 codes
+  uint32_t s[kCG][kSkinnySw];   // their scale bytes
 };
 struct APack {
   uint4 c[kSkinnyVec];
   uint32_t s[kSkinnySw];
 };
 
-template <int kW>
+template <int kW, int kCG>
 __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c) {
-  __shared__ f32x4 red[kW - 1][4][64];
+  constexpr int kCols = 16 * kCG;
+  __shared__ f32x4 red[kW - 1][kCG][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nn = lane & 15, g = lane >> 4;
   const int64_t code_pitch = k / 2, scale_pitch = k / kBlock;
   const int64_t kq = k / kW;                        // this wave's K range
   const int64_t steps = kq / kSkinnyStep;
   const int64_t kbase = wave * kq;
-  const int64_t col0 = (int64_t)blockIdx.x * kSkinnyCols;
-  const uint8_t* wc[4];
-  const uint8_t* ws[4];
+  const int64_t col0 = (int64_t)blockIdx.x * kCols;
+  const uint8_t* wc[kCG];
+  const uint8_t* ws[kCG];
 #pragma unroll
-  for (int cg = 0; cg < 4; ++cg) {
+  for (int cg = 0; cg < kCG; ++cg) {
     int64_t r = col0 + 16 * cg + nn;
     r = r < n ? r : n - 1;                          // clamped rows feed masked-out columns
     wc[cg] = w_codes + r * code_pitch + kbase / 2 + (kSkinnyStep / 8) * g;
@@ -390,15 +393,15 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
   const int64_t arow = nn < m ? nn : m - 1;
   const uint8_t* ac = a_codes + arow * code_pitch + kbase / 2 + (kSkinnyStep / 8) * g;
   const uint8_t* as = a_scales + arow * scale_pitch + kbase / 16 + (kSkinnyStep / 64) * g;
-  auto load_w = [&](WPack& p, int64_t st) {
+  auto load_w = [&](WPack<kCG>& p, int64_t st) {
     st = st < steps ? st : steps - 1;
 #pragma unroll
-    for (int cg = 0; cg < 4; ++cg)
+    for (int cg = 0; cg < kCG; ++cg)
 #pragma unroll
       for (int v = 0; v < kSkinnyVec; ++v)
         p.c[cg][v] = *reinterpret_cast<const uint4*>(wc[cg] + (kSkinnyStep / 2) * st + 16 * v);
 #pragma unroll
-    for (int cg = 0; cg < 4; ++cg)
+    for (int cg = 0; cg < kCG; ++cg)
 #pragma unroll
       for (int v = 0; v < kSkinnySw; ++v)
         p.s[cg][v] = *reinterpret_cast<const uint32_t*>(ws[cg] + (kSkinnyStep / 16) * st + 4 * v);
@@ -412,10 +415,10 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
     for (int v = 0; v < kSkinnySw; ++v)
       p.s[v] = *reinterpret_cast<const uint32_t*>(as + (kSkinnyStep / 16) * st + 4 * v);
   };
-  f32x4 acc[4];
+  f32x4 acc[kCG];
 #pragma unroll
-  for (int cg = 0; cg < 4; ++cg) acc[cg] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
-  auto compute = [&](const APack& pa, const WPack& pw) {
+  for (int cg = 0; cg < kCG; ++cg) acc[cg] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+  auto compute = [&](const APack& pa, const WPack<kCG>& pw) {
 #pragma unroll
     for (int v = 0; v < kSkinnyVec; ++v) {
       // 16-byte word v holds 32 elements = blocks 2v, 2v + 1 (scale bytes 2v, 2v + 1)
@@ -426,7 +429,7 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
 #pragma unroll
       for (int i = 0; i < 4; ++i) fa[i] = __builtin_bit_cast(f16x8, decode8(ca[i], i < 2 ? da0 : da1));
 #pragma unroll
-      for (int cg = 0; cg < 4; ++cg) {
+      for (int cg = 0; cg < kCG; ++cg) {
         const uint32_t sw = pw.s[cg][v >> 1] >> (16 * (v & 1));
         const BlockDec d0 = block_dec(sw & 0xFFu), d1 = block_dec((sw >> 8) & 0xFFu);
         const uint32_t cw[4] = {pw.c[cg][v].x, pw.c[cg][v].y, pw.c[cg][v].z, pw.c[cg][v].w};
@@ -442,7 +445,7 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
   // step s + 1 into the other one (free since step s - 1).  The pair-unrolled
   // loop keeps the pack indices static, so no pack is copied while its loads
   // are in flight.
-  WPack wp[2];
+  WPack<kCG> wp[2];
   APack ap[2];
   load_a(ap[0], 0);
   load_w(wp[0], 0);
@@ -465,13 +468,13 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
 
   if (wave > 0) {
 #pragma unroll
-    for (int cg = 0; cg < 4; ++cg) red[wave - 1][cg][lane] = acc[cg];
+    for (int cg = 0; cg < kCG; ++cg) red[wave - 1][cg][lane] = acc[cg];
   }
   __syncthreads();
   if (wave == 0) {
     const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
 #pragma unroll
-    for (int cg = 0; cg < 4; ++cg) {
+    for (int cg = 0; cg < kCG; ++cg) {
       f32x4 t = acc[cg];
 #pragma unroll
       for (int w = 0; w < kW - 1; ++w) t += red[w][cg][lane];
@@ -510,6 +513,20 @@ hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   return hipGetLastError();
 }
 
+template <int kCG>
+hipError_t launch_skinny(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
+                         const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
+                         int64_t m, int64_t n, int64_t k, float* c, hipStream_t stream) {
+  const unsigned groups = (unsigned)((n + 16 * kCG - 1) / (16 * kCG));
+  if (k % (4 * kSkinnyStep) == 0)
+    gemm_skinny_kernel<4, kCG><<<groups, 256, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
+                                                           w_scales, w_ts, m, n, k, c);
+  else
+    gemm_skinny_kernel<2, kCG><<<groups, 128, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
+                                                           w_scales, w_ts, m, n, k, c);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
@@ -527,15 +544,14 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   // 4-byte words
   const bool skinny_aligned = ((reinterpret_cast<uintptr_t>(w_scales) |
                                 reinterpret_cast<uintptr_t>(a_scales)) & 3u) == 0;
-  if (m <= kSkinnyRows && skinny_aligned && k % (4 * kSkinnyStep) == 0) {
-    gemm_skinny_kernel<4><<<(unsigned)((n + kSkinnyCols - 1) / kSkinnyCols), 256, 0, stream>>>(
-        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
-    return hipGetLastError();
-  }
   if (m <= kSkinnyRows && skinny_aligned && k % (2 * kSkinnyStep) == 0) {
-    gemm_skinny_kernel<2><<<(unsigned)((n + kSkinnyCols - 1) / kSkinnyCols), 128, 0, stream>>>(
-        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
-    return hipGetLastError();
+    // 64, 32 or 16 columns per workgroup, so that narrow W still spreads over
+    // the CUs (measured, m = 16: n = 4096 takes 5.3 us with 16 columns against
+    // 11.7 us with 64, n = 8192 7.6 against 11.8 us with 32; from n = 10240 on
+    // 64 columns is fastest, 35 us on n = 28672, k = 8192)
+    if (n >= 10240) return launch_skinny<4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    if (n >= 6144) return launch_skinny<2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    return launch_skinny<1>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
   }
   // Tile choice (measured on MI355X): 256 x 256 with 8 waves is the most
   // efficient tile per compute unit (least LDS traffic and decode work per
