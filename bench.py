@@ -49,14 +49,15 @@ PEAK_HBM_GBPS = 8000.0             # MI355X HBM3E
 QUANT_BYTES_PER_ELEM = 2 + 0.5 + 1 / 16   # read bf16, write codes + scales
 AMAX_BYTES_PER_ELEM = 2                   # the tensor-scale pass re-reads X
 
-# HBM traffic of one launch of the dominant GEMM kernel (C1 = A W1^T, 256x256
-# tiles), from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then
-# WRITE_SIZE, KiB per dispatch; summary and commands in profiles/), scaled by
-# what the same counters read for a 512 MiB elementwise copy: FETCH x 2.0,
-# WRITE x 1.0.  Valid only for the GEMM source it was measured on (first 16
-# hex digits of its SHA-256); reported as null otherwise.
-GEMM1_TRAFFIC = {"gemm_src_sha256_16": "a55ee40661aa8400",
-                 "fetch_kib": 46819.5, "write_kib": 88064.0,
+# HBM traffic of one call of the dominant GEMM (C1 = A W1^T: 256x256 tiles over
+# the first 8192 columns, then 128x256 tiles over the rest, two launches),
+# from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE,
+# KiB per dispatch, the two launches added; summary and commands in
+# profiles/), scaled by what the same counters read for a 512 MiB elementwise
+# copy: FETCH x 2.0, WRITE x 1.0.  Valid only for the GEMM source it was
+# measured on (first 16 hex digits of its SHA-256); reported as null otherwise.
+GEMM1_TRAFFIC = {"gemm_src_sha256_16": "1de3f537ac98d877",
+                 "fetch_kib": 27811.3 + 18544.5, "write_kib": 65536.0 + 22528.0,
                  "fetch_scale": 2.0, "write_scale": 1.0}
 
 
@@ -479,7 +480,9 @@ def main():
                                "W1[11008,4096], W2[4096,4096] N(0,0.02) quantized before timing",
                    "seed": 1, "gemm_flops_per_step": fl1 + fl2,
                    "quantized_elements_per_step": ra * ka},
-        "roofline": {"bound": "mfma", "kernel": "gemm_kernel 256x256 tiles (C1 = A W1^T)",
+        "roofline": {"bound": "mfma", "kernel": "gemm_kernel, C1 = A W1^T: 256x256 tiles over "
+                               "columns 0-8191, then 128x256 tiles over 8192-11007 "
+                               "(two launches, timed together)",
                      "achieved": round(tf1, 2), "peak": PEAK_F16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(tf1 / PEAK_F16_TFLOPS, 4), "traffic": gemm1_traffic_bytes(),
                      "algorithmic_bytes": ra * ka * QUANT_BYTES_PER_ELEM - ra * ka * 2

@@ -180,7 +180,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
-    int64_t n, int64_t k, float* __restrict__ c) {
+    int64_t n, int64_t k, float* __restrict__ c, int64_t ldc) {
   using T = Tile<BM, BN, WM, WN>;
   constexpr int R = T::kRowsPerThread;
   // Two separate buffers (not one indexed array) so the compiler can see that
@@ -328,7 +328,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
         const int64_t row = m0 + wm + i * 32 + 8 * (q >> 2) + 4 * half + (q & 3);
-        if (row < m && col < n) c[row * n + col] = acc[i][j][q] * scale;
+        if (row < m && col < n) c[row * ldc + col] = acc[i][j][q] * scale;
       }
     }
 }
@@ -499,17 +499,18 @@ __global__ void fill_zero(float* c, int64_t count) {
 template <int BM, int BN, int WM, int WN>
 hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
                        const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
-                       int64_t m, int64_t n, int64_t k, float* c, hipStream_t stream) {
+                       int64_t m, int64_t n, int64_t k, float* c, int64_t ldc,
+                       hipStream_t stream) {
   const unsigned tiles = (unsigned)(((m + BM - 1) / BM) * ((n + BN - 1) / BN));
   constexpr int threads = 64 * WM * WN;
   const bool fast = k % 64 == 0 && ((reinterpret_cast<uintptr_t>(a_scales) |
                                      reinterpret_cast<uintptr_t>(w_scales)) & 3u) == 0;
   if (fast)
     gemm_kernel<BM, BN, WM, WN, true, false><<<tiles, threads, 0, stream>>>(
-        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, ldc);
   else
     gemm_kernel<BM, BN, WM, WN, false, false><<<tiles, threads, 0, stream>>>(
-        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, ldc);
   return hipGetLastError();
 }
 
@@ -557,20 +558,37 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   // efficient tile per compute unit (least LDS traffic and decode work per
   // MFMA), so it is used whenever it fills at least three quarters of a round
   // of the 256 compute units (2048 x 6144 x 4096: 127 us on 192 such tiles,
-  // 177 us on 384 tiles of 128 x 256); the clock headroom of a partly idle
-  // last round makes up for part of its imbalance (splitting those tiles'
-  // K range in two measured no better).  Below that, 128 x 256 (same wave
-  // tiles, half the rows) if it fills most of a round, else 128 x 128.
-  const int64_t tiles256 = ((m + 255) / 256) * ((n + 255) / 256);
-  const int64_t tiles128x256 = ((m + 127) / 128) * ((n + 255) / 256);
-  if (4 * tiles256 >= 3 * 256)
+  // 177 us on 384 tiles of 128 x 256).  A short last round goes to 128 x 256
+  // tiles in a second launch (2048 x 11008 x 4096: 207 us against 216 us).
+  // Below that, 128 x 256 (same wave tiles, half the rows) if it fills most
+  // of a round, else 128 x 128.
+  const int64_t tm = (m + 255) / 256, tn = (n + 255) / 256;
+  const int64_t tiles256 = tm * tn;
+  const int64_t tiles128x256 = ((m + 127) / 128) * tn;
+  if (4 * tiles256 >= 3 * 256) {
+    // A short last round of 256 x 256 tiles keeps only a few CUs busy for a
+    // whole tile time.  Its columns go to a second launch of 128 x 256 tiles
+    // (half the work per CU) when those fit in one round: every output still
+    // sums its K range in the same order, so C is bit-identical.
+    const int64_t nt1 = (tiles256 / 256) * 256 / tm;    // 256-column tiles in whole rounds
+    const int64_t rest = 2 * tm * (tn - nt1);           // 128 x 256 tiles left
+    if (nt1 > 0 && nt1 < tn && rest <= 256) {
+      const int64_t n1 = 256 * nt1;
+      const hipError_t e = launch_tile<256, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales,
+                                                       w_ts, m, n1, k, c, n, stream);
+      if (e != hipSuccess) return e;
+      return launch_tile<128, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes + n1 * (k / 2),
+                                         w_scales + n1 * (k / kBlock), w_ts, m, n - n1, k,
+                                         c + n1, n, stream);
+    }
     return launch_tile<256, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
-                                       c, stream);
+                                       c, n, stream);
+  }
   if (tiles128x256 >= 192)
     return launch_tile<128, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
-                                       c, stream);
+                                       c, n, stream);
   return launch_tile<128, 128, 2, 2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
-                                     c, stream);
+                                     c, n, stream);
 }
 
 }  // namespace mixfp4
