@@ -99,6 +99,34 @@ def test_many_tiles_ragged(m, n, k):
     _check(c1, qa, qw)
 
 
+@pytest.mark.parametrize("m,n,k,cuts", [(2048, 11008, 512, (8192,)), (3072, 11008, 256, (8192, 8448)),
+                                        (16, 12288, 1024, (4096, 10240)), (300, 9000, 512, (16, 4112))])
+def test_column_slices_bit_identical(m, n, k, cuts):
+    """Every output sums its K range in the same order whatever the tile
+    shape, the number of launches (a short last round of 256 x 256 tiles goes
+    to a second launch of 128 x 256 tiles) or the decode-shape width, so C
+    restricted to a column range equals the GEMM of that range of W rows, bit
+    for bit.  The full product is also checked against the oracle on sampled
+    rows and columns, the cut columns included."""
+    import paper_2605_31035_amd as M
+    qa = Q.quantize(W.adversarial(m + 1, m, k))
+    qw = Q.quantize(W.adversarial(n + 2, n, k))
+    log(f"gemm column slices m={m} n={n} k={k} cuts={cuts}")
+    a = (dev_u8(qa.codes), dev_u8(qa.scales), dev_f32(qa.s32))
+    wc, ws, wt = dev_u8(qw.codes), dev_u8(qw.scales), dev_f32(qw.s32)
+    full = M.mixfp4_gemm(a, (wc, ws, wt))
+    edges = (0,) + tuple(cuts) + (n,)
+    for lo, hi in zip(edges[:-1], edges[1:]):
+        part = M.mixfp4_gemm(a, (wc[lo:hi], ws[lo:hi], wt))
+        torch.cuda.synchronize()
+        assert torch.equal(part, full[:, lo:hi]), f"columns {lo}..{hi}"
+    rng = np.random.default_rng(m + n)
+    rows = np.unique(np.concatenate([[0, m - 1], rng.integers(0, m, 40)]))
+    cols = np.unique(np.concatenate([[0, n - 1], np.array(cuts), np.array(cuts) - 1,
+                                     rng.integers(0, n, 200)]))
+    _check(host(full), qa, qw, rows=rows, cols=cols)
+
+
 @pytest.mark.parametrize("m,n,k", [(2000, 3100, 512), (2000, 3100, 560), (1500, 8000, 560)])
 def test_mid_size_ragged(m, n, k):
     """Shapes with fewer 256x256 tiles than CUs: 2000 x 3100 takes 128x256
