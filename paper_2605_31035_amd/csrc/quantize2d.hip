@@ -85,8 +85,9 @@ __global__ __launch_bounds__(kThreads2d) void quantize_2d_kernel(
 // in registers across its 16 lanes (one DPP row), so lane i holds row i of
 // the W^T tile.  A W^T row of the super-block collects one 8-byte code chunk
 // and one scale byte from each of its kSR tile rows, so those rows are
-// staged in LDS (the chunk slot XOR-swizzled by the row, which spreads the
-// 16 lanes of a tile over the banks) and written out after the last
+// staged in LDS (the chunk slot XOR-swizzled by the row, so that the 16
+// lanes of a tile, one row each, write kSR different slots rather than the
+// same one) and written out after the last
 // iteration as runs of 8 kSR code bytes and kSR scale bytes.  Stored one
 // chunk per lane, the W^T rows cost a separate memory transaction for every
 // 8 bytes of codes and every scale byte.
