@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+
 namespace mixfp4 {
 
 // Block size along the reduction dimension (App. B.1, V = 16).
@@ -37,24 +39,28 @@ struct QuantOptions {
 
 // Workgroups of `threads` threads that the device keeps resident at once for
 // `kernel` (occupancy per CU x CU count), at most max_per_cu per CU when that
-// is positive; `cache` holds one value per device.
+// is positive.  `cache` holds one value per device (0 = not yet known);
+// concurrent first calls may both query the runtime, and store the same value.
+using ResidentCache = std::atomic<int64_t>[64];
+
 template <typename Kernel>
-int64_t resident_groups(Kernel kernel, int64_t (&cache)[64], int max_per_cu = 0,
+int64_t resident_groups(Kernel kernel, ResidentCache& cache, int max_per_cu = 0,
                         int threads = 256) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 1024;
-  if (!cache[dev]) {
-    int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
-        per_cu <= 0)
-      per_cu = 4;
-    if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-        cus <= 0)
-      cus = 256;
-    cache[dev] = (int64_t)per_cu * cus;
-  }
-  return cache[dev];
+  const int64_t known = cache[dev].load(std::memory_order_relaxed);
+  if (known) return known;
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
+      per_cu <= 0)
+    per_cu = 4;
+  if (max_per_cu > 0 && per_cu > max_per_cu) per_cu = max_per_cu;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  const int64_t v = (int64_t)per_cu * cus;
+  cache[dev].store(v, std::memory_order_relaxed);
+  return v;
 }
 
 // Launchers: shapes are validated by the ABI layer before these are called.

@@ -409,7 +409,7 @@ hipError_t launch_tensor_scale_rotated(const uint16_t* x, int64_t rows, int64_t 
                                        int64_t scratch_bytes, float* tensor_scale,
                                        hipStream_t stream) {
   const int64_t nbk = k / kBlock, nblocks = rows * nbk;
-  static int64_t cache_c[64], cache_s[64];
+  static ResidentCache cache_c, cache_s;
   const int64_t resident = ldx == k ? resident_groups(amax_rotated_kernel<true>, cache_c)
                                     : resident_groups(amax_rotated_kernel<false>, cache_s);
   const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
@@ -458,7 +458,7 @@ hipError_t launch_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, 
   // at 3 workgroups per CU takes 118 us against 137 us at 8; E1M2-only is
   // best at 4).  For the other modes 4 to 8 measure the same; they take 6.
   constexpr int kMaxPerCU = kMode == kForceE2M1 ? 3 : (kMode == kForceE1M2 ? 4 : 6);
-  static int64_t cache_c[64], cache_s[64], capped_c[64], capped_s[64];
+  static ResidentCache cache_c, cache_s, capped_c, capped_s;
   const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
   const bool contig = ldx == k;
   const int64_t resident =
@@ -535,7 +535,7 @@ hipError_t launch_hadamard(const uint16_t* x, int64_t rows, int64_t k, int64_t l
                            const HadamardParams& hp, uint16_t* y, hipStream_t stream) {
   const int64_t nbk = k / kBlock, nblocks = rows * nbk;
   if (nblocks == 0) return hipSuccess;
-  static int64_t cache_c[64], cache_s[64];
+  static ResidentCache cache_c, cache_s;
   const int64_t resident = ldx == k ? resident_groups(hadamard_kernel<true>, cache_c)
                                     : resident_groups(hadamard_kernel<false>, cache_s);
   const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
