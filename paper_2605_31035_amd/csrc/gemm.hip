@@ -336,7 +336,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // ---------------------------------------------------------------------------
 // Decode-shape GEMM (m <= 16): HBM-bound, W is read once.
 //
-// A workgroup owns 16 kCG columns of C (kCG = 4, 2 or 1 MFMA column groups)
+// A workgroup owns 16 kCG columns of C (kCG = 1 to 4 MFMA column groups)
 // and splits K over its kW waves (4, or 2 when k is not a multiple of 1024);
 // each wave walks its K range in steps of 256 with no barrier and no LDS
 // until the end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
@@ -546,13 +546,19 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   const bool skinny_aligned = ((reinterpret_cast<uintptr_t>(w_scales) |
                                 reinterpret_cast<uintptr_t>(a_scales)) & 3u) == 0;
   if (m <= kSkinnyRows && skinny_aligned && k % (2 * kSkinnyStep) == 0) {
-    // 64, 32 or 16 columns per workgroup, so that narrow W still spreads over
-    // the CUs (measured, m = 16: n = 4096 takes 5.3 us with 16 columns against
-    // 11.7 us with 64, n = 8192 7.6 against 11.8 us with 32; from n = 10240 on
-    // 64 columns is fastest, 35 us on n = 28672, k = 8192)
-    if (n >= 10240) return launch_skinny<4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
-    if (n >= 6144) return launch_skinny<2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
-    return launch_skinny<1>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    // The narrowest workgroups (16, 32, 48 or 64 columns) that need at most
+    // one workgroup per CU, so that narrow W still spreads over every CU
+    // without leaving some CUs two; wider W takes 64 columns (best per column,
+    // one A decode for four column groups).  Measured, m = 16, k = 4096:
+    // n = 4096 5.3 us with 16 columns against 11.7 with 64; n = 8192 7.5
+    // against 11.8 with 32; n = 11008 9.7 against 11.6 with 48; n = 14336
+    // 12.0 with 64 against 16.8 with 48 (299 workgroups); 16 x 28672 x 8192
+    // 35.0 us with 64.
+    const int64_t cus = 256;
+    if (n <= 16 * cus) return launch_skinny<1>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    if (n <= 32 * cus) return launch_skinny<2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    if (n <= 48 * cus) return launch_skinny<3>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    return launch_skinny<4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
   }
   // Tile choice (measured on MI355X): 256 x 256 with 8 waves is the most
   // efficient tile per compute unit (least LDS traffic and decode work per

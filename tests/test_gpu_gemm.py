@@ -71,11 +71,12 @@ def test_ragged_shapes(m, n, k):
 
 @pytest.mark.parametrize("m,n,k", [(1, 1, 512), (5, 127, 1024), (16, 129, 512), (9, 1000, 2048),
                                    (16, 256, 8192), (3, 300, 1536), (16, 6150, 1024),
-                                   (2, 7000, 1536), (16, 10250, 2048), (7, 10256, 512)])
+                                   (2, 7000, 1536), (16, 10250, 2048), (7, 10256, 512),
+                                   (16, 12300, 1024)])
 def test_decode_shapes(m, n, k):
     """m <= 16 with k % 512 == 0 takes the decode-shape kernel (K split over 4
     waves when k % 1024 == 0, else over 2; odd and single step counts), with
-    16, 32 or 64 columns per workgroup (n below 6144, below 10240, above),
+    16, 32, 48 or 64 columns per workgroup (n up to 4096, 8192, 12288, above),
     ragged last column groups included."""
     a = W.adversarial(7 * m + k, m, k)
     w = W.adversarial(11 * n + k, n, k)
