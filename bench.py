@@ -56,8 +56,8 @@ AMAX_BYTES_PER_ELEM = 2                   # the tensor-scale pass re-reads X
 # profiles/), scaled by what the same counters read for a 512 MiB elementwise
 # copy: FETCH x 2.0, WRITE x 1.0.  Valid only for the GEMM source it was
 # measured on (first 16 hex digits of its SHA-256); reported as null otherwise.
-GEMM1_TRAFFIC = {"gemm_src_sha256_16": "1de3f537ac98d877",
-                 "fetch_kib": 27811.3 + 18544.5, "write_kib": 65536.0 + 22528.0,
+GEMM1_TRAFFIC = {"gemm_src_sha256_16": "db85dd2f329cd1d2",
+                 "fetch_kib": 27811.0 + 18545.5, "write_kib": 65536.0 + 22528.0,
                  "fetch_scale": 2.0, "write_scale": 1.0}
 
 
