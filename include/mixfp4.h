@@ -205,8 +205,11 @@ int mixfp4_dequantize(const uint8_t *codes, const uint8_t *scales,
  * mixfp4_gemm - C[m, n] = sum_k A[m, k] * W[n, k] for two MixFP4 operands
  * (C = A W^T, both quantized along the reduction dimension K, App. B.1).
  * Each element is decoded through the unified E2M2 value set (Sec. 3.3,
- * App. B.5) to an exact bf16 value E4M3 * v, the products accumulate in fp32
- * on the matrix cores, and the epilogue multiplies by s32_A * s32_W.
+ * App. B.5) to the 16-bit value E4M3 * v, the products accumulate in fp32 on
+ * the matrix cores, and the epilogue multiplies by s32_A * s32_W.  The
+ * decoded value has at most 7 significant bits (4 of the E4M3 scale, 3 of v)
+ * and lies in [2^-10, 3136], so it is exact in fp16 and in bf16 alike; the
+ * kernels feed fp16 operands to the fp16 matrix instructions.
  * Accuracy: |C - C_exact| <= 1e-5 * sum_k |A_hat * W_hat| + 1e-6, where
  * A_hat, W_hat are the exactly dequantized operands.
  *

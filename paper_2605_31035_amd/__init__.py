@@ -48,6 +48,35 @@ def _ptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
+def _require(t, name: str, dtype, shape=None, numel=None):
+    """Check a caller-supplied tensor before its address reaches the library:
+    the C ABI takes bare pointers with no pitches, so a wrong dtype, shape or
+    layout would make a kernel read or write the wrong bytes.  Shape, dtype
+    and contiguity are checked before the device, so every mistake is named."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if numel is not None and t.numel() != numel:
+        raise ValueError(f"{name} must have {numel} element(s), got {t.numel()}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _same_device(device, *named):
+    """Every tensor on the same CUDA device as the first."""
+    for name, t in named:
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be a CUDA tensor")
+        if t.device != device:
+            raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
 def _check(status: int):
     if status != 0:
         msg = lib.mixfp4_status_string(status).decode()
@@ -80,7 +109,7 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
         raise ValueError(f"mode must be one of {sorted(_MODES)}")
     if rounding not in ("nearest", "stochastic"):
         raise ValueError("rounding must be 'nearest' or 'stochastic'")
-    if x.dtype != torch.bfloat16 or x.dim() != 2 or not x.is_cuda:
+    if x.dtype != torch.bfloat16 or x.dim() != 2:
         raise ValueError("x must be a 2-D bfloat16 CUDA tensor")
     if x.stride(1) != 1:
         raise ValueError("x must have unit stride along K")
@@ -91,12 +120,17 @@ def mixfp4_quantize(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
         codes = torch.empty((orows, ok // 2), dtype=torch.uint8, device=dev)
     if scales is None:
         scales = torch.empty((orows, ok // 16), dtype=torch.uint8, device=dev)
+    _require(codes, "codes", torch.uint8, (orows, ok // 2))
+    _require(scales, "scales", torch.uint8, (orows, ok // 16))
     if tensor_scale is None:
         ts = scale_out if scale_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
         flags = SCALE_COMPUTE
     else:
         ts = tensor_scale
         flags = SCALE_GIVEN
+    _require(ts, "tensor_scale" if tensor_scale is not None else "scale_out", torch.float32,
+             numel=1)
+    _same_device(dev, ("x", x), ("codes", codes), ("scales", scales), ("tensor scale", ts))
     flags |= _MODES[mode]
     ldx = x.stride(0) if rows > 0 else k
     if rounding == "nearest" and hadamard_block == 0 and not transpose:
@@ -150,6 +184,8 @@ def mixfp4_quantize_2d(w: torch.Tensor, tensor_scale: torch.Tensor | None = None
         flags = SCALE_COMPUTE
     else:
         ts, flags = tensor_scale, SCALE_GIVEN
+    _require(ts, "tensor scale", torch.float32, numel=1)
+    _same_device(dev, ("tensor scale", ts))
     st = lib.mixfp4_quantize_2d(_ptr(w), n, k, w.stride(0) if n > 0 else k, _ptr(codes),
                                 _ptr(scales), _ptr(codes_t), _ptr(scales_t), _ptr(ts),
                                 flags | _MODES[mode], _stream(dev))
@@ -168,6 +204,8 @@ def mixfp4_hadamard(x: torch.Tensor, block: int, signs: torch.Tensor | None = No
     rows, k = x.shape
     if out is None:
         out = torch.empty((rows, k), dtype=torch.bfloat16, device=x.device)
+    _require(out, "out", torch.bfloat16, (rows, k))
+    _same_device(x.device, ("out", out))
     sg = _signs_arg(signs, block)
     st = lib.mixfp4_hadamard(_ptr(x), rows, k, x.stride(0) if rows > 0 else k, block, _ptr(sg),
                              _ptr(out), _stream(x.device))
@@ -179,8 +217,18 @@ def mixfp4_dequantize(codes: torch.Tensor, scales: torch.Tensor,
                       tensor_scale: torch.Tensor | None = None) -> torch.Tensor:
     """Decode MixFP4 to fp32 [rows, k]; ``tensor_scale`` None decodes in the
     FP8 domain (s32 = 1)."""
+    if not isinstance(codes, torch.Tensor) or codes.dim() != 2:
+        raise ValueError("codes must be a 2-D uint8 tensor [rows, k/2]")
     rows, half = codes.shape
     k = half * 2
+    _require(codes, "codes", torch.uint8, (rows, half))
+    _require(scales, "scales", torch.uint8, (rows, k // 16))
+    if k % 16:
+        raise ValueError("k = 2 * codes.shape[1] must be a multiple of 16")
+    if tensor_scale is not None:
+        _require(tensor_scale, "tensor_scale", torch.float32, numel=1)
+    _same_device(codes.device, ("codes", codes), ("scales", scales),
+                 ("tensor_scale", tensor_scale))
     out = torch.empty((rows, k), dtype=torch.float32, device=codes.device)
     st = lib.mixfp4_dequantize(_ptr(codes), _ptr(scales), _ptr(tensor_scale), rows, k,
                                _ptr(out), _stream(codes.device))
@@ -193,11 +241,26 @@ def mixfp4_gemm(a, w, out: torch.Tensor | None = None) -> torch.Tensor:
     (s32 may be None for 1.0).  Returns fp32 [m, n]."""
     ac, asc, ats = a
     wc, wsc, wts = w
+    for name, t in (("A codes", ac), ("W codes", wc)):
+        if not isinstance(t, torch.Tensor) or t.dim() != 2:
+            raise ValueError(f"{name} must be a 2-D uint8 tensor [rows, k/2]")
     m, n, k = ac.shape[0], wc.shape[0], ac.shape[1] * 2
     if wc.shape[1] * 2 != k:
         raise ValueError("A and W disagree on K")
+    if k % 16:
+        raise ValueError("k = 2 * codes.shape[1] must be a multiple of 16")
+    _require(ac, "A codes", torch.uint8, (m, k // 2))
+    _require(asc, "A scales", torch.uint8, (m, k // 16))
+    _require(wc, "W codes", torch.uint8, (n, k // 2))
+    _require(wsc, "W scales", torch.uint8, (n, k // 16))
+    for name, t in (("A tensor scale", ats), ("W tensor scale", wts)):
+        if t is not None:
+            _require(t, name, torch.float32, numel=1)
     if out is None:
         out = torch.empty((m, n), dtype=torch.float32, device=ac.device)
+    _require(out, "out", torch.float32, (m, n))
+    _same_device(ac.device, ("A codes", ac), ("A scales", asc), ("A tensor scale", ats),
+                 ("W codes", wc), ("W scales", wsc), ("W tensor scale", wts), ("out", out))
     st = lib.mixfp4_gemm(_ptr(ac), _ptr(asc), _ptr(ats), _ptr(wc), _ptr(wsc), _ptr(wts),
                          m, n, k, _ptr(out), _stream(ac.device))
     _check(st)

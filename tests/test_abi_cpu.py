@@ -154,3 +154,77 @@ def test_quantize_2d_rejects(lib):
     assert f(codes=P(0)) == 1
     assert f(ct=P(0x10008)) == 3
     assert f(rows=0, flags=1) == 0
+
+
+# --- the Python binding rejects mis-shaped tensors before any launch --------
+# (CPU tensors: every check below fires before the device check, and a
+# correctly shaped CPU argument is rejected for its device, so no call reaches
+# the library.)
+
+def _gemm_args(m=32, n=48, k=64):
+    import torch
+    u8 = torch.uint8
+    a = (torch.zeros((m, k // 2), dtype=u8), torch.zeros((m, k // 16), dtype=u8),
+         torch.ones(1, dtype=torch.float32))
+    w = (torch.zeros((n, k // 2), dtype=u8), torch.zeros((n, k // 16), dtype=u8),
+         torch.ones(1, dtype=torch.float32))
+    return a, w, torch.zeros((m, n), dtype=torch.float32)
+
+
+def test_binding_gemm_rejects_bad_tensors():
+    import torch
+
+    import paper_2605_31035_amd as M
+    a, w, out = _gemm_args()
+    cases = [
+        ((a, w, out[:, :40]), "out must have shape"),                       # short out
+        ((a, w, out.t().contiguous().t()), "contiguous"),                   # strided out
+        ((a, w, out.double()), "float32"),                                  # wrong dtype
+        (((a[0], a[1][:, :3], a[2]), w, out), "A scales must have shape"),  # scales too narrow
+        (((a[0][:, :16], a[1], a[2]), w, None), "disagree on K"),           # K-sliced codes
+        (((a[0][:, ::2], a[1][:, :2], a[2]), (w[0][:, :16], w[1][:, :2], w[2]), None),
+         "contiguous"),                                                     # strided codes
+        ((a, (w[0], w[1].to(torch.int8), w[2]), out), "uint8"),
+        (((a[0], a[1], torch.ones(2)), w, out), "1 element"),
+        ((a, w, out), "CUDA tensor"),                                       # all fine but CPU
+    ]
+    for (aa, ww, oo), msg in cases:
+        with pytest.raises(ValueError, match=msg):
+            M.mixfp4_gemm(aa, ww, out=oo)
+
+
+def test_binding_dequantize_rejects_bad_tensors():
+    import torch
+
+    import paper_2605_31035_amd as M
+    codes = torch.zeros((4, 32), dtype=torch.uint8)
+    scales = torch.zeros((4, 4), dtype=torch.uint8)
+    with pytest.raises(ValueError, match="scales must have shape"):
+        M.mixfp4_dequantize(codes, scales[:, :3])
+    with pytest.raises(ValueError, match="contiguous"):
+        M.mixfp4_dequantize(torch.zeros((4, 64), dtype=torch.uint8)[:, ::2], scales)
+    with pytest.raises(ValueError, match="multiple of 16"):
+        M.mixfp4_dequantize(torch.zeros((4, 4), dtype=torch.uint8), scales[:, :0])
+    with pytest.raises(ValueError, match="1 element"):
+        M.mixfp4_dequantize(codes, scales, torch.ones(3))
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        M.mixfp4_dequantize(codes, scales)
+
+
+def test_binding_quantize_rejects_bad_outputs():
+    import torch
+
+    import paper_2605_31035_amd as M
+    x = torch.zeros((8, 64), dtype=torch.bfloat16)
+    good_c = torch.zeros((8, 32), dtype=torch.uint8)
+    good_s = torch.zeros((8, 4), dtype=torch.uint8)
+    with pytest.raises(ValueError, match="codes must have shape"):
+        M.mixfp4_quantize(x, codes=good_c[:, :16].contiguous(), scales=good_s)
+    with pytest.raises(ValueError, match="scales must have shape"):
+        M.mixfp4_quantize(x, codes=good_c, scales=good_s[:4])
+    with pytest.raises(ValueError, match="scale_out must have 1 element"):
+        M.mixfp4_quantize(x, codes=good_c, scales=good_s, scale_out=torch.ones(2))
+    with pytest.raises(ValueError, match="codes must have shape"):
+        M.mixfp4_quantize(x, codes=good_c, scales=good_s, transpose=True)
+    with pytest.raises(ValueError, match="CUDA tensor"):
+        M.mixfp4_quantize(x, codes=good_c, scales=good_s)

@@ -295,3 +295,28 @@ def test_catches_four_six_wrong_divisor(monkeypatch):
 
     monkeypatch.setattr(Q, "_algorithm1_blocks", mutated)
     assert not _four_six_pins_pass()
+
+
+# --- dequantize (App. B.2-B.3): one rounding of s32 * s8 * v -----------------
+
+def test_unmutated_dequantize_pins_pass():
+    from tests.test_oracle_dequantize import dequantize_pins_pass
+    assert dequantize_pins_pass()
+
+
+def test_catches_dequantize_double_rounding(monkeypatch):
+    """s32 * s8 rounded to fp32 first, then times v (two roundings)."""
+    from tests.test_oracle_dequantize import dequantize_pins_pass
+
+    def twice(codes, scales, s32=None):
+        nib = Q.unpack_nibbles(codes)
+        sc = np.asarray(scales, dtype=np.uint8)
+        t = np.repeat((sc >> 7).astype(np.int64), Q.BLOCK, axis=1)
+        s8 = np.repeat(F.e4m3_decode(sc & 0x7F), Q.BLOCK, axis=1)
+        mag = (nib & 7).astype(np.int64)
+        v = np.where(t == 1, F.I_GRID[mag], F.F_GRID[mag]) * np.where(nib & 8, -1.0, 1.0)
+        s = np.float32(1.0 if s32 is None else s32)
+        return (np.float32(s) * s8.astype(np.float32)).astype(np.float32) * v.astype(np.float32)
+
+    monkeypatch.setattr(Q, "dequantize", twice)
+    assert not dequantize_pins_pass()
