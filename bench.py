@@ -1,34 +1,40 @@
 #!/usr/bin/env python3
 """Throughput of the MixFP4 hot path on one MI355X.
 
-One step = one pass of the prefill path over the 7B-class workload (seed 1):
-compute the tensor scale of and quantize the activations A [2048, 4096]
-(Student-t nu=4 with 8 outlier channels x50), then C1 = A W1^T [2048, 11008]
-and C2 = A W2^T [2048, 4096] in fp32 on the matrix cores.  The weights W1
-[11008, 4096] and W2 [4096, 4096] (N(0, 0.02)) are quantized once before
-timing, as weights are quantized offline.  Inputs are resident in HBM before
-timing starts.
+One step = one pass of the whole path over the large prefill workload (seed
+4): compute the tensor scale of and quantize the activations A [16384, 8192]
+(block mixture: 90% of 16-blocks N(0, 0.1), 10% Laplace(0, 1) with one x40
+spike), then C = A W^T [16384, 8192] in fp32 on the matrix cores.  The weight
+W [8192, 8192] (N(0, 0.02)) is quantized once before timing, as weights are
+quantized offline.  Inputs are resident in HBM before timing starts.
 
 Prints ONE JSON line:
   value         GEMM FLOPs of the step / step time (TFLOP/s; the activation
                 quantizer is inside the step time), from K steps timed
-                wall-clock between device synchronizations
-  roofline      the dominant kernel, the GEMM C1 = A W1^T, against the dense
-                fp16 MFMA peak (its operands are exact fp16 values): its FLOPs
-                per launch over its mean launch time, timed with HIP events on
-                the stream it runs on during a second pass of the same K steps
-  gemm2         the same for C2 = A W2^T
+                wall-clock between device synchronizations, after W warmup
+                steps and a time-based spin-up to loaded clocks
+  roofline      the dominant kernel, the GEMM C = A W^T of the step, against
+                the dense fp16 MFMA peak (its operands are exact fp16 values):
+                its FLOPs per launch over its mean launch time, timed with HIP
+                events on the stream it runs on during a second pass of the
+                same K steps
   quantize      the quantizer kernel on the standalone 2^28-element tensor
                 (seed 4 block mixture) against HBM, with the tensor scale given
                 (algorithmic 2.5625 B / element), plus the end-to-end time with
-                the tensor scale computed on the device
+                the tensor scale computed on the device, and the other
+                encodings / roundings / rotation on the same tensor
   quantize_step the activation quantizer inside the step
-  decode_shape  the memory-bound m = 16 GEMM (seed 3) against HBM
+  prefill_7b    the 7B-class prefill step (seed 1): quantize A [2048, 4096],
+                C1 = A W1^T [2048, 11008], C2 = A W2^T [2048, 4096]
+  rotated       the rotated-operand step (seed 2): quantize A [4096, 4096],
+                C = A W^T [4096, 14336]
+  decode_shape  the memory-bound m = 16 step (seed 3) against HBM
   train_step    one training step of a 7B-class linear layer (FPROP, DGRAD,
                 WGRAD with 2D weight blocks, stochastic rounding and the
                 16-row Hadamard rotation of the WGRAD inputs; seed 5)
-  cpu_baseline  the CPU oracle on a bounded sample of the same step
+  cpu_baseline  the CPU oracle on a bounded sample of the headline step
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+                       [--only large,quantize,prefill_7b,rotated,decode,train]
 """
 from __future__ import annotations
 
@@ -49,23 +55,23 @@ PEAK_HBM_GBPS = 8000.0             # MI355X HBM3E
 QUANT_BYTES_PER_ELEM = 2 + 0.5 + 1 / 16   # read bf16, write codes + scales
 AMAX_BYTES_PER_ELEM = 2                   # the tensor-scale pass re-reads X
 
-# HBM traffic of one call of the dominant GEMM (C1 = A W1^T: 256x256 tiles over
-# the first 8192 columns, then 128x256 tiles over the rest, two launches),
-# from two rocprofv3 --pmc runs of this script (FETCH_SIZE, then WRITE_SIZE,
-# KiB per dispatch, the two launches added; summary and commands in
+# HBM traffic of one launch of the dominant GEMM (C = A W^T of the large
+# workload, 16384 x 8192 x 8192), from two rocprofv3 --pmc runs of this script
+# (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch; summary and commands in
 # profiles/), scaled by what the same counters read for a 512 MiB elementwise
-# copy: FETCH x 2.0, WRITE x 1.0.  Valid only for the GEMM source it was
-# measured on (first 16 hex digits of its SHA-256); reported as null otherwise.
-GEMM1_TRAFFIC = {"gemm_src_sha256_16": "db85dd2f329cd1d2",
-                 "fetch_kib": 27811.0 + 18545.5, "write_kib": 65536.0 + 22528.0,
-                 "fetch_scale": 2.0, "write_scale": 1.0}
+# copy (--calibrate-copy).  Valid only for the GEMM source it was measured on
+# (first 16 hex digits of its SHA-256); reported as null otherwise, and null
+# until it has been measured.
+GEMM_TRAFFIC = None
 
 
-def gemm1_traffic_bytes():
+def gemm_traffic_bytes():
     import hashlib
+    t = GEMM_TRAFFIC
+    if t is None:
+        return None
     with open(os.path.join(ROOT, "paper_2605_31035_amd", "csrc", "gemm.hip"), "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()[:16]
-    t = GEMM1_TRAFFIC
     if sha != t["gemm_src_sha256_16"]:
         return None
     return round((t["fetch_kib"] * t["fetch_scale"] + t["write_kib"] * t["write_scale"]) * 1024)
@@ -82,24 +88,45 @@ def _oracle_quantize_rows(args):
     return q.codes, q.scales
 
 
-def cpu_baseline(wl, budget_s: float = 10.0, max_reps: int = 8) -> dict:
-    """The CPU oracle on the same step: quantize A (row chunks in a process
-    pool, one process per core; the tensor scale is the oracle's own max over
-    the full tensor) and both GEMMs as the oracle defines them (fp64 matmul of
-    exactly dequantized operands plus the bound matmul, multithreaded BLAS).
-    The weights are quantized by the oracle once, outside the timed sample, as
-    in the GPU step.  Whole steps repeat until `budget_s` has elapsed."""
+def _blas_threads() -> int | None:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i["num_threads"] for i in threadpool_info() if i.get("user_api") == "blas"]
+        return max(n) if n else None
+    except Exception:
+        return None
+
+
+# The sample of the headline step that the oracle runs: the first SAMPLE_ROWS
+# rows of A against the first SAMPLE_COLS rows of W (all of K), with the
+# tensor scales of the full tensors, as in the GPU step.
+SAMPLE_ROWS, SAMPLE_COLS = 512, 2048
+
+
+def cpu_baseline(wl, budget_s: float = 12.0, max_reps: int = 8) -> dict:
+    """The CPU oracle on a bounded sample of the headline step: the oracle
+    quantize of A's first SAMPLE_ROWS rows (row chunks in a process pool; the
+    tensor scale is the oracle's max over all of A) and the oracle GEMM of
+    those rows against W's first SAMPLE_COLS rows (fp64 matmul of exactly
+    dequantized operands plus its bound matmul, multithreaded BLAS).  W's
+    sample is quantized by the oracle once, outside the timed sample, as W is
+    in the GPU step.  Samples repeat until `budget_s` has elapsed; the rate is
+    the sample's GEMM FLOPs over its time.  The pool takes every core of this
+    process's affinity mask up to 16, the CPU share one GPU of the box has."""
     from concurrent.futures import ProcessPoolExecutor
 
     from oracle import gemm as G
     from oracle import quant as Q
 
-    cores = max(1, min(16, len(os.sched_getaffinity(0))))
-    step_flops = sum(2.0 * wl.tensors[a].shape[0] * wl.tensors[w].shape[0] * wl.tensors[a].shape[1]
-                     for a, w in wl.gemms)
+    affinity = len(os.sched_getaffinity(0))
+    cores = max(1, min(16, affinity))
+    a_bits, w_bits = wl.tensors["A"], wl.tensors["W"]
+    sa, sw = Q.tensor_scale(a_bits), Q.tensor_scale(w_bits)
+    a_s, w_s = a_bits[:SAMPLE_ROWS], w_bits[:SAMPLE_COLS]
+    k = a_bits.shape[1]
+    flops = 2.0 * a_s.shape[0] * w_s.shape[0] * k
 
-    def quantize(ex, bits):
-        s32 = Q.tensor_scale(bits)
+    def quantize(ex, bits, s32):
         parts = list(ex.map(_oracle_quantize_rows,
                             [(c, s32) for c in np.array_split(bits, 4 * cores)]))
         return Q.Quantized(codes=np.concatenate([p[0] for p in parts]),
@@ -108,20 +135,22 @@ def cpu_baseline(wl, budget_s: float = 10.0, max_reps: int = 8) -> dict:
 
     times = []
     with ProcessPoolExecutor(cores) as ex:
-        weights = {w: quantize(ex, wl.tensors[w]) for _, w in wl.gemms}
+        qw = quantize(ex, w_s, sw)
         while len(times) < max_reps and sum(times) < budget_s:
             t0 = time.perf_counter()
-            qa = quantize(ex, wl.tensors["A"])
-            for _, w in wl.gemms:
-                G.gemm(*G.operands(qa, weights[w]))
+            qa = quantize(ex, a_s, sa)
+            G.gemm(*G.operands(qa, qw))
             times.append(time.perf_counter() - t0)
     t = float(np.mean(times))
+    blas = _blas_threads()
     return {
-        "value": step_flops / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
-        "sample": (f"{len(times)} full step(s) of the same workload: oracle quantize of A "
-                   f"({cores} processes) + oracle fp64 GEMMs C1, C2 with their bound matmuls "
-                   f"(BLAS threads), weights quantized by the oracle beforehand; "
-                   f"{t:.2f} s per step"),
+        "value": flops / t / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+        "blas_threads": blas, "affinity_cores": affinity,
+        "sample": (f"{len(times)} sample(s) of the headline step: oracle quantize of "
+                   f"A[:{SAMPLE_ROWS}] of [16384,8192] ({cores} processes, s32 of all of A) + "
+                   f"oracle fp64 GEMM of those rows against W[:{SAMPLE_COLS}] with its bound "
+                   f"matmul ({blas} BLAS threads); W's rows quantized by the oracle "
+                   f"beforehand; {t:.2f} s per sample of {flops / 1e9:.1f} GFLOP"),
     }
 
 
@@ -371,20 +400,102 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
     return out
 
 
+def gemm_bytes(m: int, n: int, k: int) -> float:
+    """Algorithmic HBM bytes of one GEMM call: packed A and W (codes and scale
+    bytes, 0.5625 B / element) and the fp32 C."""
+    return (m + n) * k * (0.5 + 1 / 16) + 4.0 * m * n
+
+
+def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -> dict:
+    """One prefill step of a workload: quantize A (tensor scale computed on the
+    device), then every GEMM of the workload against weights quantized before
+    timing.  The step time comes from `steps` steps with nothing else on the
+    stream, timed wall-clock between device synchronizations, after `warmup`
+    untimed steps and `spin_s` seconds of untimed steps that bring the clocks
+    to their loaded level.  The per-launch spans come from a second pass of the
+    same steps with HIP events recorded on the launching stream around each
+    launch (an event adds ~3.5 us of GPU time between launches, so the step
+    time is taken without them)."""
+    x = {n: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
+         for n, b in wl.tensors.items()}
+    wnames = [w for _, w in wl.gemms]
+    qw = {w: M.mixfp4_quantize(x[w]) for w in wnames}
+    for w in wnames:
+        del x[w]
+    ra, ka = x["A"].shape
+    qa = (torch.empty((ra, ka // 2), dtype=torch.uint8, device=dev),
+          torch.empty((ra, ka // 16), dtype=torch.uint8, device=dev),
+          torch.empty(1, dtype=torch.float32, device=dev))
+    outs = {w: torch.empty((ra, qw[w][0].shape[0]), dtype=torch.float32, device=dev)
+            for w in wnames}
+    torch.cuda.synchronize()
+
+    def step(e=None):
+        if e is not None:
+            e[0].record()
+        M.mixfp4_quantize(x["A"], None, qa[0], qa[1], scale_out=qa[2])
+        for i, w in enumerate(wnames):
+            if e is not None:
+                e[i + 1].record()
+            M.mixfp4_gemm(qa, qw[w], out=outs[w])
+        if e is not None:
+            e[len(wnames) + 1].record()
+
+    for _ in range(warmup):
+        step()
+    spin_up(torch, step, spin_s)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    ms_step = (time.perf_counter() - t0) * 1e3 / steps
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(len(wnames) + 2)]
+             for _ in range(steps)]
+    for i in range(steps):
+        step(marks[i])
+    torch.cuda.synchronize()
+    span = lambda a, b: float(np.mean([m[a].elapsed_time(m[b]) for m in marks]))  # noqa: E731
+    q_ms = span(0, 1)
+    gemms = {}
+    total_flops = 0.0
+    for i, w in enumerate(wnames):
+        n = qw[w][0].shape[0]
+        fl = 2.0 * ra * n * ka
+        total_flops += fl
+        g_ms = span(i + 1, i + 2)
+        tf = fl / (g_ms * 1e-3) / 1e12
+        gemms[w] = {"shape": [ra, n, ka], "flops": fl, "us_per_launch": round(g_ms * 1e3, 2),
+                    "achieved": round(tf, 2), "unit": "TFLOP/s",
+                    "frac": round(tf / PEAK_F16_TFLOPS, 4),
+                    "algorithmic_bytes": gemm_bytes(ra, n, ka)}
+    out = {"ms_per_step": round(ms_step, 4), "steps": steps, "warmup": warmup,
+           "spin_up_s": spin_s,
+           "step_TFLOPs": round(total_flops / (ms_step * 1e-3) / 1e12, 3),
+           "gemm_flops_per_step": total_flops,
+           "quantize_a": {"what": f"A[{ra},{ka}] with the tensor scale computed on the device "
+                                  "(amax pass + reduction + quantize kernel)",
+                          "us": round(q_ms * 1e3, 2),
+                          "GBps": round(ra * ka * QUANT_BYTES_PER_ELEM / (q_ms * 1e-3) / 1e9, 1),
+                          "bytes_per_elem": QUANT_BYTES_PER_ELEM},
+           "gemms": gemms}
+    del x, qw, qa, outs
+    torch.cuda.empty_cache()
+    return out
+
+
+SECTIONS = ("large", "quantize", "prefill_7b", "rotated", "decode", "train")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    # 300 prefill steps (~0.1 s): the clocks reach their loaded level (see
-    # spin_up); fewer warmup steps measure a partly idle GPU
-    ap.add_argument("--warmup", type=int, default=300)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--spin-up", type=float, default=0.5,
+                    help="seconds of untimed steps before the timed ones (loaded clocks)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-decode", action="store_true",
-                    help="skip the extra decode-shape (m = 16) measurement")
-    ap.add_argument("--no-quantize-only", action="store_true",
-                    help="skip the quantize-only measurement on the 2^28-element tensor")
-    ap.add_argument("--no-train", action="store_true",
-                    help="skip the training-step (FPROP/DGRAD/WGRAD) measurement")
+    ap.add_argument("--only", default=",".join(SECTIONS),
+                    help="comma-separated sections to run (profiling runs isolate one)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one elementwise copy of 512 MiB (read + write of known "
                          "size) so hardware byte counters can be scaled")
@@ -393,113 +504,86 @@ def main():
         print("bench.py measures one GPU only: the MixFP4 path here runs on a single MI355X "
               "(--gpus 1).", file=sys.stderr)
         sys.exit(2)
+    only = set(args.only.split(","))
+    unknown = only - set(SECTIONS)
+    if unknown:
+        print(f"unknown sections {sorted(unknown)}; choose from {SECTIONS}", file=sys.stderr)
+        sys.exit(2)
 
     import workloads as W
-    log("generating prefill_7b workload (seed 1)")
-    wl = W.prefill_7b()
-    cpu = None if args.no_cpu_baseline else cpu_baseline(wl)
-    if cpu:
-        log(f"cpu baseline: {cpu['value']:.4g} TFLOP/s ({cpu['sample']})")
+    wl5 = None
+    cpu = None
+    if "large" in only:
+        log("generating the large workload (seed 4): A[16384,8192], W[8192,8192]")
+        wl5 = W.large(tensors=("A", "W"))
+        if not args.no_cpu_baseline:
+            cpu = cpu_baseline(wl5)
+            log(f"cpu baseline: {cpu['value']:.4g} TFLOP/s ({cpu['sample']})")
 
     import torch
 
     import paper_2605_31035_amd as M
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    x = {n: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
-         for n, b in wl.tensors.items()}
-    (g1a, g1w), (g2a, g2w) = wl.gemms
-    # weights: quantized once, before timing
-    qw = {w: M.mixfp4_quantize(x[w]) for _, w in wl.gemms}
-    ra, ka = x["A"].shape
-    qa = (torch.empty((ra, ka // 2), dtype=torch.uint8, device=dev),
-          torch.empty((ra, ka // 16), dtype=torch.uint8, device=dev),
-          torch.empty(1, dtype=torch.float32, device=dev))
-    c1 = torch.empty((ra, x[g1w].shape[0]), dtype=torch.float32, device=dev)
-    c2 = torch.empty((ra, x[g2w].shape[0]), dtype=torch.float32, device=dev)
     if args.calibrate_copy:
         src = torch.ones(128 << 20, dtype=torch.float32, device=dev)
         dst = torch.empty_like(src)
         torch.mul(src, 1.0, out=dst)
+        torch.cuda.synchronize()
         del src, dst
-    torch.cuda.synchronize()
 
-    ev = lambda: torch.cuda.Event(enable_timing=True)  # noqa: E731
-
-    def step(e=None):
-        if e is not None:
-            e[0].record()
-        M.mixfp4_quantize(x["A"], None, qa[0], qa[1], scale_out=qa[2])
-        if e is not None:
-            e[1].record()
-        M.mixfp4_gemm(qa, qw[g1w], out=c1)
-        if e is not None:
-            e[2].record()
-        M.mixfp4_gemm(qa, qw[g2w], out=c2)
-        if e is not None:
-            e[3].record()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    # The value: K steps with nothing but the path on the stream.
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_step = (t1 - t0) * 1e3 / args.steps
-    # The per-kernel spans (roofline, gemm2, quantize_step): the same K steps
-    # again, right after, with HIP events on the launching stream around every
-    # launch.  Each event record adds ~3.5 us of GPU time to a step (measured:
-    # 312 us per step without events, 326 us with four), which is why the
-    # value's pass has none; an event does not change the kernel it brackets.
-    marks = [[ev() for _ in range(4)] for _ in range(args.steps)]
-    for i in range(args.steps):
-        step(marks[i])
-    torch.cuda.synchronize()
-    span = lambda a, b: float(np.mean([m[a].elapsed_time(m[b]) for m in marks]))  # noqa: E731
-    q_ms, g1_ms, g2_ms = span(0, 1), span(1, 2), span(2, 3)
-
-    fl1 = 2.0 * ra * x[g1w].shape[0] * ka
-    fl2 = 2.0 * ra * x[g2w].shape[0] * ka
-    tf1 = fl1 / (g1_ms * 1e-3) / 1e12
-    tf2 = fl2 / (g2_ms * 1e-3) / 1e12
-    qa_gbps = ra * ka * QUANT_BYTES_PER_ELEM / (q_ms * 1e-3) / 1e9
-    out = {
-        "metric": METRIC,
-        "value": round((fl1 + fl2) / (ms_step * 1e-3) / 1e12, 3),
-        "unit": "TFLOP/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-        "ms_per_step": round(ms_step, 4),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "fp16", "data": "synthetic",
-        "config": {"workload": "prefill_7b: quantize A[2048,4096] (Student-t nu=4, 8 outlier "
-                               "channels x50, tensor scale computed on the device), then "
-                               "C1=A W1^T [2048,11008] and C2=A W2^T [2048,4096] fp32; "
-                               "W1[11008,4096], W2[4096,4096] N(0,0.02) quantized before timing",
-                   "seed": 1, "gemm_flops_per_step": fl1 + fl2,
-                   "quantized_elements_per_step": ra * ka},
-        "roofline": {"bound": "mfma", "kernel": "gemm_kernel, C1 = A W1^T: 256x256 tiles over "
-                               "columns 0-8191, then 128x256 tiles over 8192-11007 "
-                               "(two launches, timed together)",
-                     "achieved": round(tf1, 2), "peak": PEAK_F16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(tf1 / PEAK_F16_TFLOPS, 4), "traffic": gemm1_traffic_bytes(),
-                     "algorithmic_bytes": ra * ka * QUANT_BYTES_PER_ELEM - ra * ka * 2
-                     + x[g1w].shape[0] * ka * (QUANT_BYTES_PER_ELEM - 2) + 4.0 * ra * x[g1w].shape[0],
-                     "flops_per_launch": fl1, "us_per_launch": round(g1_ms * 1e3, 2)},
-        "gemm2": {"kernel": "gemm_kernel 128x256 tiles (C2 = A W2^T)",
-                  "achieved": round(tf2, 2), "unit": "TFLOP/s",
-                  "frac": round(tf2 / PEAK_F16_TFLOPS, 4), "us_per_launch": round(g2_ms * 1e3, 2)},
-        "quantize_step": {"what": "A[2048,4096] with the tensor scale computed on the device "
-                                  "(amax pass + reduction + quantize kernel)",
-                          "us": round(q_ms * 1e3, 2), "GBps": round(qa_gbps, 1),
-                          "bytes_per_elem": QUANT_BYTES_PER_ELEM},
-        "quantize": None if args.no_quantize_only else measure_quantize(M, torch, dev),
-        "decode_shape": None if args.no_decode else measure_decode(M, torch, dev),
-        "train_step": None if args.no_train else measure_train(M, torch, dev),
-        "cpu_baseline": cpu,
-    }
+    out = {"metric": METRIC, "value": None, "unit": "TFLOP/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": None,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "fp16", "data": "synthetic"}
+    if wl5 is not None:
+        log("large step: quantize A[16384,8192] + GEMM 16384x8192x8192")
+        r = measure_prefill(M, torch, dev, wl5, args.steps, args.warmup, args.spin_up)
+        del wl5
+        g = r["gemms"]["W"]
+        out["value"] = r["step_TFLOPs"]
+        out["ms_per_step"] = r["ms_per_step"]
+        out["config"] = {
+            "workload": "large (seed 4): quantize A[16384,8192] (block mixture: 90% of "
+                        "16-blocks N(0,0.1), 10% Laplace(0,1) with one x40 spike; tensor scale "
+                        "computed on the device), then C = A W^T [16384,8192] fp32; "
+                        "W[8192,8192] N(0,0.02) quantized before timing",
+            "seed": 4, "gemm_flops_per_step": r["gemm_flops_per_step"],
+            "quantized_elements_per_step": 16384 * 8192, "spin_up_s": args.spin_up,
+            "timing": "value: K steps back to back, wall clock between device "
+                      "synchronizations, after W warmup steps and spin_up_s seconds of "
+                      "untimed steps (loaded clocks)"}
+        out["roofline"] = {"bound": "mfma",
+                           "kernel": "gemm_kernel, C = A W^T 16384x8192x8192, 256x256 tiles "
+                                     "(2048 tiles: 8 whole rounds of 256 CUs, one launch)",
+                           "achieved": g["achieved"], "peak": PEAK_F16_TFLOPS,
+                           "unit": "TFLOP/s", "frac": g["frac"],
+                           "traffic": gemm_traffic_bytes(),
+                           "algorithmic_bytes": g["algorithmic_bytes"],
+                           "flops_per_launch": g["flops"],
+                           "us_per_launch": g["us_per_launch"]}
+        out["quantize_step"] = r["quantize_a"]
+    if "quantize" in only:
+        out["quantize"] = measure_quantize(M, torch, dev)
+    if "prefill_7b" in only:
+        log("generating prefill_7b workload (seed 1)")
+        r = measure_prefill(M, torch, dev, W.prefill_7b(), args.steps, min(args.warmup, 20), 0.3)
+        r["workload"] = ("prefill_7b (seed 1): quantize A[2048,4096] (Student-t nu=4, 8 outlier "
+                         "channels x50), C1 = A W1^T [2048,11008], C2 = A W2^T [2048,4096]; "
+                         "W1, W2 N(0,0.02) quantized before timing")
+        out["prefill_7b"] = r
+    if "rotated" in only:
+        log("generating rotated workload (seed 2)")
+        r = measure_prefill(M, torch, dev, W.rotated(), args.steps, min(args.warmup, 20), 0.3)
+        r["workload"] = ("rotated (seed 2): quantize A[4096,4096] (Student-t nu=3 times "
+                         "blockdiag(H128/sqrt(128)) along K), C = A W^T [4096,14336]; W rotated "
+                         "the same way, quantized before timing")
+        out["rotated"] = r
+    if "decode" in only:
+        out["decode_shape"] = measure_decode(M, torch, dev)
+    if "train" in only:
+        out["train_step"] = measure_train(M, torch, dev)
+    out["cpu_baseline"] = cpu
     print(json.dumps(out), flush=True)
 
 
