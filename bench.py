@@ -400,22 +400,28 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
     return out
 
 
-def gemm_bytes(m: int, n: int, k: int) -> float:
-    """Algorithmic HBM bytes of one GEMM call: packed A and W (codes and scale
-    bytes, 0.5625 B / element) and the fp32 C."""
-    return (m + n) * k * (0.5 + 1 / 16) + 4.0 * m * n
+def gemm_decoded_bytes(m: int, n: int, k: int) -> float:
+    """Algorithmic HBM bytes of one GEMM launch on decoded operands: the 16-bit
+    A and W read once and the fp32 C written."""
+    return (m + n) * k * 2.0 + 4.0 * m * n
 
 
 def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -> dict:
     """One prefill step of a workload: quantize A (tensor scale computed on the
-    device), then every GEMM of the workload against weights quantized before
-    timing.  The step time comes from `steps` steps with nothing else on the
-    stream, timed wall-clock between device synchronizations, after `warmup`
-    untimed steps and `spin_s` seconds of untimed steps that bring the clocks
-    to their loaded level.  The per-launch spans come from a second pass of the
-    same steps with HIP events recorded on the launching stream around each
-    launch (an event adds ~3.5 us of GPU time between launches, so the step
-    time is taken without them)."""
+    device), decode A once into exact 16-bit values, and for every weight of
+    the workload decode it and run the GEMM on the decoded operands (the two
+    passes of mixfp4_gemm_ws, called separately so that A, shared by the
+    workload's GEMMs, is decoded once and every kernel has its own span).  The
+    weights are quantized before timing; their decode is inside the step.  The
+    step time comes from `steps` steps with nothing else on the stream, timed
+    wall-clock between device synchronizations, after `warmup` untimed steps
+    and `spin_s` seconds of untimed steps that bring the clocks to their
+    loaded level.  The per-launch spans come from a second pass of the same
+    steps with HIP events recorded on the launching stream around each launch
+    (an event adds ~3.5 us of GPU time between launches, so the step time is
+    taken without them).  The fused single-kernel GEMM (mixfp4_gemm, which
+    decodes inside its MFMA loop) is timed on the same operands for
+    comparison."""
     x = {n: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
          for n, b in wl.tensors.items()}
     wnames = [w for _, w in wl.gemms]
@@ -428,18 +434,28 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
           torch.empty(1, dtype=torch.float32, device=dev))
     outs = {w: torch.empty((ra, qw[w][0].shape[0]), dtype=torch.float32, device=dev)
             for w in wnames}
+    # decoded-operand buffers, allocated once (the step writes them every time)
+    da = M.mixfp4_decode_operand(qa)
+    dws = {w: M.mixfp4_decode_operand(qw[w]) for w in wnames}
     torch.cuda.synchronize()
+    nspan = 2 + 2 * len(wnames)
 
     def step(e=None):
         if e is not None:
             e[0].record()
         M.mixfp4_quantize(x["A"], None, qa[0], qa[1], scale_out=qa[2])
+        if e is not None:
+            e[1].record()
+        M.mixfp4_decode_operand(qa, out=da.buf)
         for i, w in enumerate(wnames):
             if e is not None:
-                e[i + 1].record()
-            M.mixfp4_gemm(qa, qw[w], out=outs[w])
+                e[2 + 2 * i].record()
+            M.mixfp4_decode_operand(qw[w], out=dws[w].buf)
+            if e is not None:
+                e[3 + 2 * i].record()
+            M.mixfp4_gemm_decoded(da, dws[w], out=outs[w])
         if e is not None:
-            e[len(wnames) + 1].record()
+            e[nspan].record()
 
     for _ in range(warmup):
         step()
@@ -449,25 +465,49 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
         step()
     torch.cuda.synchronize()
     ms_step = (time.perf_counter() - t0) * 1e3 / steps
-    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(len(wnames) + 2)]
+    marks = [[torch.cuda.Event(enable_timing=True) for _ in range(nspan + 1)]
              for _ in range(steps)]
     for i in range(steps):
         step(marks[i])
     torch.cuda.synchronize()
     span = lambda a, b: float(np.mean([m[a].elapsed_time(m[b]) for m in marks]))  # noqa: E731
     q_ms = span(0, 1)
+    da_ms = span(1, 2)
     gemms = {}
     total_flops = 0.0
     for i, w in enumerate(wnames):
         n = qw[w][0].shape[0]
         fl = 2.0 * ra * n * ka
         total_flops += fl
-        g_ms = span(i + 1, i + 2)
+        dw_ms = span(2 + 2 * i, 3 + 2 * i)
+        g_ms = span(3 + 2 * i, 4 + 2 * i)
         tf = fl / (g_ms * 1e-3) / 1e12
-        gemms[w] = {"shape": [ra, n, ka], "flops": fl, "us_per_launch": round(g_ms * 1e3, 2),
+        dec_bytes = n * ka * (0.5 + 1 / 16 + 2)
+        gemms[w] = {"shape": [ra, n, ka], "flops": fl,
+                    "kernel": "gemm_f16_kernel (decoded operands)",
+                    "us_per_launch": round(g_ms * 1e3, 2),
                     "achieved": round(tf, 2), "unit": "TFLOP/s",
                     "frac": round(tf / PEAK_F16_TFLOPS, 4),
-                    "algorithmic_bytes": gemm_bytes(ra, n, ka)}
+                    "decode_w_us": round(dw_ms * 1e3, 2),
+                    "decode_w_GBps": round(dec_bytes / (dw_ms * 1e-3) / 1e9, 1),
+                    "gemm_call_us": round((dw_ms + g_ms) * 1e3, 2),
+                    "gemm_call_TFLOPs": round(fl / ((dw_ms + g_ms) * 1e-3) / 1e12, 2)}
+    # the fused kernel on the same operands: back-to-back launches
+    for w in wnames:
+        f = lambda: M.mixfp4_gemm(qa, qw[w], out=outs[w])  # noqa: E731
+        spin_up(torch, f, 0.1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        f_ms = e0.elapsed_time(e1) / steps
+        fl = gemms[w]["flops"]
+        gemms[w]["fused_kernel"] = {"kernel": "gemm_kernel (decode inside the MFMA loop)",
+                                    "us_per_launch": round(f_ms * 1e3, 2),
+                                    "achieved": round(fl / (f_ms * 1e-3) / 1e12, 2),
+                                    "frac": round(fl / (f_ms * 1e-3) / 1e12 / PEAK_F16_TFLOPS, 4)}
     out = {"ms_per_step": round(ms_step, 4), "steps": steps, "warmup": warmup,
            "spin_up_s": spin_s,
            "step_TFLOPs": round(total_flops / (ms_step * 1e-3) / 1e12, 3),
@@ -477,8 +517,11 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
                           "us": round(q_ms * 1e3, 2),
                           "GBps": round(ra * ka * QUANT_BYTES_PER_ELEM / (q_ms * 1e-3) / 1e9, 1),
                           "bytes_per_elem": QUANT_BYTES_PER_ELEM},
+           "decode_a": {"kernel": "decode_blocked_kernel", "us": round(da_ms * 1e3, 2),
+                        "bytes": ra * ka * (0.5 + 1 / 16 + 2),
+                        "GBps": round(ra * ka * (0.5 + 1 / 16 + 2) / (da_ms * 1e-3) / 1e9, 1)},
            "gemms": gemms}
-    del x, qw, qa, outs
+    del x, qw, qa, outs, da, dws
     torch.cuda.empty_cache()
     return out
 
@@ -546,23 +589,32 @@ def main():
         out["config"] = {
             "workload": "large (seed 4): quantize A[16384,8192] (block mixture: 90% of "
                         "16-blocks N(0,0.1), 10% Laplace(0,1) with one x40 spike; tensor scale "
-                        "computed on the device), then C = A W^T [16384,8192] fp32; "
-                        "W[8192,8192] N(0,0.02) quantized before timing",
+                        "computed on the device), decode A and W once to exact 16-bit values, "
+                        "then C = A W^T [16384,8192] fp32; W[8192,8192] N(0,0.02) quantized "
+                        "before timing (its decode is inside the step)",
             "seed": 4, "gemm_flops_per_step": r["gemm_flops_per_step"],
             "quantized_elements_per_step": 16384 * 8192, "spin_up_s": args.spin_up,
             "timing": "value: K steps back to back, wall clock between device "
                       "synchronizations, after W warmup steps and spin_up_s seconds of "
                       "untimed steps (loaded clocks)"}
         out["roofline"] = {"bound": "mfma",
-                           "kernel": "gemm_kernel, C = A W^T 16384x8192x8192, 256x256 tiles "
-                                     "(2048 tiles: 8 whole rounds of 256 CUs, one launch)",
+                           "kernel": "gemm_f16_kernel on decoded operands, C = A W^T "
+                                     "16384x8192x8192, 256x256 tiles (2048 tiles: 8 whole rounds "
+                                     "of 256 CUs, one launch)",
                            "achieved": g["achieved"], "peak": PEAK_F16_TFLOPS,
                            "unit": "TFLOP/s", "frac": g["frac"],
                            "traffic": gemm_traffic_bytes(),
-                           "algorithmic_bytes": g["algorithmic_bytes"],
+                           "algorithmic_bytes": gemm_decoded_bytes(16384, 8192, 8192),
                            "flops_per_launch": g["flops"],
                            "us_per_launch": g["us_per_launch"]}
         out["quantize_step"] = r["quantize_a"]
+        out["decode_step"] = {"decode_a": r["decode_a"],
+                              "decode_w_us": g["decode_w_us"], "decode_w_GBps": g["decode_w_GBps"],
+                              "bound": "hbm", "bytes_per_elem": 0.5 + 1 / 16 + 2}
+        out["gemm_call"] = {"what": "decode W + GEMM (the mixfp4_gemm_ws work for an operand "
+                                    "decoded once), and the fused single-kernel GEMM",
+                            "us": g["gemm_call_us"], "TFLOPs": g["gemm_call_TFLOPs"],
+                            "fused_kernel": g["fused_kernel"]}
     if "quantize" in only:
         out["quantize"] = measure_quantize(M, torch, dev)
     if "prefill_7b" in only:

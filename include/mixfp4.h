@@ -224,6 +224,74 @@ int mixfp4_gemm(const uint8_t *a_codes, const uint8_t *a_scales,
                 const uint8_t *w_scales, const float *w_tensor_scale,
                 int64_t m, int64_t n, int64_t k, float *c, void *stream);
 
+/*
+ * mixfp4_gemm_ws - mixfp4_gemm with caller-supplied device workspace, for the
+ * compute-bound shapes.  The result satisfies the same accuracy bound as
+ * mixfp4_gemm (every product is of the same exactly decoded operands, only
+ * the fp32 summation order differs).
+ *
+ * With m > 16, k % 32 == 0, k <= 2^22 and workspace_bytes at least
+ * mixfp4_gemm_workspace_size(m, n, k), the call runs two passes: each
+ * operand's elements are decoded once (Sec. 3.3 / App. B.5: T selects the
+ * E2M1 or E1M2 x2 value, times the E4M3 block scale, exactly) into 16-bit
+ * values in the workspace, in a blocked layout private to the library; then
+ * a GEMM on those values accumulates in fp32 on the matrix cores and applies
+ * s32_A * s32_W in the epilogue (App. B.1).  Otherwise (decode-shape m,
+ * k % 32 != 0, or too little workspace) it computes exactly what mixfp4_gemm
+ * computes, without touching the workspace.
+ *
+ *   a_codes ... c      as for mixfp4_gemm.
+ *   workspace          device memory, 256-byte aligned (MIXFP4_ERR_ALIGN
+ *                      otherwise), or NULL; its contents on entry are
+ *                      ignored and on return are unspecified.  Calls that
+ *                      share a workspace must be ordered (same stream).
+ *   workspace_bytes    its size; < 0 is MIXFP4_ERR_SHAPE.
+ */
+int mixfp4_gemm_ws(const uint8_t *a_codes, const uint8_t *a_scales,
+                   const float *a_tensor_scale, const uint8_t *w_codes,
+                   const uint8_t *w_scales, const float *w_tensor_scale,
+                   int64_t m, int64_t n, int64_t k, float *c, void *workspace,
+                   int64_t workspace_bytes, void *stream);
+
+/*
+ * mixfp4_gemm_workspace_size - bytes of workspace with which mixfp4_gemm_ws
+ * takes the two-pass path for this shape: 2 * k * (m + n) rounded up to
+ * whole 256-row tiles of A and of W, or 0 where that path does not apply.
+ * Host-only; *bytes is written on MIXFP4_OK.  Negative sizes or k % 16 != 0:
+ * MIXFP4_ERR_SHAPE; bytes == NULL: MIXFP4_ERR_NULL.
+ */
+int mixfp4_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t *bytes);
+
+/*
+ * The two passes of mixfp4_gemm_ws as separate calls, so that an operand
+ * used by several GEMMs (activations against several weights) is decoded
+ * once, and each pass can be timed on its own.
+ *
+ * mixfp4_decode_operand - decode a MixFP4 operand [rows, k] (codes, scales
+ * as written by mixfp4_quantize) into the 16-bit values E4M3 * v(code, T)
+ * (Sec. 3.3, App. B.5), exactly, in the library's blocked layout (rows
+ * padded to a multiple of 256; the layout is private and only
+ * mixfp4_gemm_decoded reads it; padding rows are left unwritten).  The
+ * tensor scale is not applied.
+ *   rows, k       rows >= 0, k % 32 == 0, k <= 2^22 (else MIXFP4_ERR_SHAPE).
+ *   out           device memory of out_bytes, 256-byte aligned; bytes_needed
+ *                 (may be NULL) receives the size the layout needs.  out ==
+ *                 NULL with out_bytes == 0 only reports that size.  A
+ *                 smaller out_bytes is MIXFP4_ERR_SHAPE.
+ *
+ * mixfp4_gemm_decoded - C[m, n] = s32_A s32_W sum_k a[m,k] w[n,k] from two
+ * decoded operands (same k), fp32 accumulation on the matrix cores (App.
+ * B.1), the tensor scales applied in the epilogue (NULL = 1.0).  Accuracy as
+ * for mixfp4_gemm.  m, n >= 0; k as above; k == 0 writes zeros; C fp32
+ * row-major [m, n], 4-byte aligned; decoded operands 256-byte aligned.
+ */
+int mixfp4_decode_operand(const uint8_t *codes, const uint8_t *scales,
+                          int64_t rows, int64_t k, void *out, int64_t out_bytes,
+                          int64_t *bytes_needed, void *stream);
+int mixfp4_gemm_decoded(const void *a_decoded, const float *a_tensor_scale,
+                        const void *w_decoded, const float *w_tensor_scale,
+                        int64_t m, int64_t n, int64_t k, float *c, void *stream);
+
 /* Human-readable name of a mixfp4_status value (static storage). */
 const char *mixfp4_status_string(int status);
 
@@ -233,7 +301,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 104
+#define MIXFP4_ABI_VERSION 105
 
 #ifdef __cplusplus
 }

@@ -15,12 +15,19 @@ Functions (same names as the C ABI in include/mixfp4.h):
       -> (codes, scales, s32) for W and (codes_t, scales_t, s32) for W^T
   mixfp4_hadamard(x, block, signs=None) -> bf16 tensor
   mixfp4_dequantize(codes, scales, tensor_scale=None) -> fp32 tensor
-  mixfp4_gemm(a, w) -> C = A W^T (fp32), a/w are (codes, scales, s32) triples
+  mixfp4_gemm(a, w, workspace=None) -> C = A W^T (fp32), a/w are (codes, scales,
+      s32) triples; with a workspace (a uint8 CUDA tensor, or True to allocate
+      one of mixfp4_gemm_workspace_size bytes) the call is mixfp4_gemm_ws
+  mixfp4_gemm_workspace_size(m, n, k) -> bytes
+  mixfp4_decode_operand((codes, scales, s32)) -> Decoded (the operand decoded
+      once to exact 16-bit values in the library's blocked layout)
+  mixfp4_gemm_decoded(a: Decoded, w: Decoded) -> C = A W^T (fp32)
 """
 from __future__ import annotations
 
 import ctypes
 import os
+from typing import NamedTuple
 
 import torch
 
@@ -28,7 +35,9 @@ from ._lib import LIB_PATH, MixFP4Error, lib
 
 __all__ = ["mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_hadamard", "mixfp4_dequantize",
            "mixfp4_gemm", "MixFP4Error", "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN",
-           "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC", "TRANSPOSE", "mixfp4_quantize_2d"]
+           "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC", "TRANSPOSE", "mixfp4_quantize_2d",
+           "mixfp4_gemm_workspace_size", "mixfp4_decode_operand", "mixfp4_gemm_decoded",
+           "Decoded"]
 
 SCALE_COMPUTE = 0
 SCALE_GIVEN = 1
@@ -236,9 +245,20 @@ def mixfp4_dequantize(codes: torch.Tensor, scales: torch.Tensor,
     return out
 
 
-def mixfp4_gemm(a, w, out: torch.Tensor | None = None) -> torch.Tensor:
+def mixfp4_gemm_workspace_size(m: int, n: int, k: int) -> int:
+    """Bytes of workspace with which mixfp4_gemm(..., workspace=...) takes the
+    two-pass path (0 where it does not apply)."""
+    b = ctypes.c_int64(0)
+    _check(lib.mixfp4_gemm_workspace_size(m, n, k, ctypes.byref(b)))
+    return b.value
+
+
+def mixfp4_gemm(a, w, out: torch.Tensor | None = None, workspace=None) -> torch.Tensor:
     """C = A W^T for MixFP4 operands given as (codes, scales, s32) triples
-    (s32 may be None for 1.0).  Returns fp32 [m, n]."""
+    (s32 may be None for 1.0).  Returns fp32 [m, n].  ``workspace``: None
+    (mixfp4_gemm), a contiguous uint8 CUDA tensor (mixfp4_gemm_ws with it), or
+    True (mixfp4_gemm_ws with a workspace of mixfp4_gemm_workspace_size bytes
+    allocated here)."""
     ac, asc, ats = a
     wc, wsc, wts = w
     for name, t in (("A codes", ac), ("W codes", wc)):
@@ -259,9 +279,75 @@ def mixfp4_gemm(a, w, out: torch.Tensor | None = None) -> torch.Tensor:
     if out is None:
         out = torch.empty((m, n), dtype=torch.float32, device=ac.device)
     _require(out, "out", torch.float32, (m, n))
+    if workspace is True:
+        workspace = torch.empty(max(1, mixfp4_gemm_workspace_size(m, n, k)), dtype=torch.uint8,
+                                device=ac.device)
+    if workspace is not None:
+        if not isinstance(workspace, torch.Tensor) or workspace.dtype != torch.uint8 \
+                or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous uint8 tensor (or True / None)")
     _same_device(ac.device, ("A codes", ac), ("A scales", asc), ("A tensor scale", ats),
-                 ("W codes", wc), ("W scales", wsc), ("W tensor scale", wts), ("out", out))
-    st = lib.mixfp4_gemm(_ptr(ac), _ptr(asc), _ptr(ats), _ptr(wc), _ptr(wsc), _ptr(wts),
-                         m, n, k, _ptr(out), _stream(ac.device))
+                 ("W codes", wc), ("W scales", wsc), ("W tensor scale", wts), ("out", out),
+                 ("workspace", workspace))
+    if workspace is None:
+        st = lib.mixfp4_gemm(_ptr(ac), _ptr(asc), _ptr(ats), _ptr(wc), _ptr(wsc), _ptr(wts),
+                             m, n, k, _ptr(out), _stream(ac.device))
+    else:
+        st = lib.mixfp4_gemm_ws(_ptr(ac), _ptr(asc), _ptr(ats), _ptr(wc), _ptr(wsc), _ptr(wts),
+                                m, n, k, _ptr(out), _ptr(workspace), workspace.numel(),
+                                _stream(ac.device))
     _check(st)
+    return out
+
+
+class Decoded(NamedTuple):
+    """An operand decoded by mixfp4_decode_operand: ``buf`` (uint8 CUDA
+    tensor in the library's blocked layout), its logical shape and its tensor
+    scale (fp32 [1] tensor or None)."""
+    buf: torch.Tensor
+    rows: int
+    k: int
+    s32: torch.Tensor | None
+
+
+def mixfp4_decode_operand(q, out: torch.Tensor | None = None) -> Decoded:
+    """Decode a MixFP4 operand (codes [rows, k/2], scales [rows, k/16], s32)
+    once into exact 16-bit values (App. B.5) for mixfp4_gemm_decoded; k % 32
+    must be 0."""
+    codes, scales, ts = q
+    if not isinstance(codes, torch.Tensor) or codes.dim() != 2:
+        raise ValueError("codes must be a 2-D uint8 tensor [rows, k/2]")
+    rows, k = codes.shape[0], codes.shape[1] * 2
+    if k % 32:
+        raise ValueError("k must be a multiple of 32 for the decoded GEMM")
+    _require(codes, "codes", torch.uint8, (rows, k // 2))
+    _require(scales, "scales", torch.uint8, (rows, k // 16))
+    if ts is not None:
+        _require(ts, "tensor scale", torch.float32, numel=1)
+    need = ctypes.c_int64(0)
+    _check(lib.mixfp4_decode_operand(None, None, rows, k, None, 0, ctypes.byref(need), None))
+    if out is None:
+        out = torch.empty(max(1, need.value), dtype=torch.uint8, device=codes.device)
+    _require(out, "out", torch.uint8)
+    if out.numel() < need.value:
+        raise ValueError(f"out must hold {need.value} bytes")
+    _same_device(codes.device, ("codes", codes), ("scales", scales), ("tensor scale", ts),
+                 ("out", out))
+    _check(lib.mixfp4_decode_operand(_ptr(codes), _ptr(scales), rows, k, _ptr(out), out.numel(),
+                                     None, _stream(codes.device)))
+    return Decoded(out, rows, k, ts)
+
+
+def mixfp4_gemm_decoded(a: Decoded, w: Decoded, out: torch.Tensor | None = None) -> torch.Tensor:
+    """C = s32_A s32_W A W^T (fp32 [m, n]) from two decoded operands."""
+    if a.k != w.k:
+        raise ValueError("A and W disagree on K")
+    m, n = a.rows, w.rows
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=a.buf.device)
+    _require(out, "out", torch.float32, (m, n))
+    _same_device(a.buf.device, ("A", a.buf), ("W", w.buf), ("A tensor scale", a.s32),
+                 ("W tensor scale", w.s32), ("out", out))
+    _check(lib.mixfp4_gemm_decoded(_ptr(a.buf), _ptr(a.s32), _ptr(w.buf), _ptr(w.s32), m, n, a.k,
+                                   _ptr(out), _stream(a.buf.device)))
     return out

@@ -15,8 +15,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmixfp4.s
 
 SYMBOLS = ("mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_quantize_2d", "mixfp4_hadamard",
            "mixfp4_dequantize",
-           "mixfp4_gemm", "mixfp4_status_string", "mixfp4_last_launch_error",
-           "mixfp4_abi_version")
+           "mixfp4_gemm", "mixfp4_gemm_ws", "mixfp4_gemm_workspace_size",
+           "mixfp4_decode_operand", "mixfp4_gemm_decoded",
+           "mixfp4_status_string", "mixfp4_last_launch_error", "mixfp4_abi_version")
 
 
 class MixFP4Error(RuntimeError):
@@ -27,7 +28,7 @@ class MixFP4Error(RuntimeError):
 
 def load(path: str = LIB_PATH) -> ctypes.CDLL:
     if not os.path.exists(path):
-        raise ImportError(f"{path} not found: build it with `python -m paper_2605_31035_amd.build`")
+        raise ImportError(f"{path} not found: build it with `python paper_2605_31035_amd/build.py`")
     h = ctypes.CDLL(path)
     vp, i64, u32, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint, ctypes.c_int
     h.mixfp4_quantize.argtypes = [vp, i64, i64, i64, vp, vp, vp, u32, vp]
@@ -43,6 +44,14 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     h.mixfp4_dequantize.restype = i32
     h.mixfp4_gemm.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, vp, vp]
     h.mixfp4_gemm.restype = i32
+    h.mixfp4_gemm_ws.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, vp, vp, i64, vp]
+    h.mixfp4_gemm_ws.restype = i32
+    h.mixfp4_gemm_workspace_size.argtypes = [i64, i64, i64, ctypes.POINTER(i64)]
+    h.mixfp4_gemm_workspace_size.restype = i32
+    h.mixfp4_decode_operand.argtypes = [vp, vp, i64, i64, vp, i64, ctypes.POINTER(i64), vp]
+    h.mixfp4_decode_operand.restype = i32
+    h.mixfp4_gemm_decoded.argtypes = [vp, vp, vp, vp, i64, i64, i64, vp, vp]
+    h.mixfp4_gemm_decoded.restype = i32
     h.mixfp4_status_string.argtypes = [i32]
     h.mixfp4_status_string.restype = ctypes.c_char_p
     h.mixfp4_last_launch_error.argtypes = []

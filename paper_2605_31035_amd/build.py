@@ -1,6 +1,7 @@
 """Build libmixfp4.so (gfx950) in-tree with hipcc.
 
-Usage: python -m paper_2605_31035_amd.build   (or call build()).
+Usage: python paper_2605_31035_amd/build.py   (or call build(); importing the
+package first would load the library being rebuilt).
 
 Every HIP source is compiled for gfx950 only, with fp contraction off (the
 quantizer relies on exact IEEE operations in the order written) and packed
@@ -20,7 +21,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmixfp4.so")
-SOURCES = ["api.cpp", "quantize.hip", "quantize2d.hip", "dequantize.hip", "gemm.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "quantize2d.hip", "dequantize.hip", "gemm.hip",
+           "gemm_f16.hip"]
 
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")

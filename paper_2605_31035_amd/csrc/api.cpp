@@ -194,11 +194,15 @@ int mixfp4_dequantize(const uint8_t* codes, const uint8_t* scales, const float* 
                                                  static_cast<hipStream_t>(stream)));
 }
 
-int mixfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_tensor_scale,
-                const uint8_t* w_codes, const uint8_t* w_scales, const float* w_tensor_scale,
-                int64_t m, int64_t n, int64_t k, float* c, void* stream) {
+namespace {
+// Argument checks shared by the GEMM entry points: MIXFP4_OK means "launch",
+// kEmpty "nothing to compute" (m or n is 0), anything else is the error.
+constexpr int kEmpty = -1;
+int gemm_check(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_tensor_scale,
+               const uint8_t* w_codes, const uint8_t* w_scales, const float* w_tensor_scale,
+               int64_t m, int64_t n, int64_t k, float* c) {
   if (m < 0 || n < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;
-  if (m == 0 || n == 0) return MIXFP4_OK;
+  if (m == 0 || n == 0) return kEmpty;
   if (!c) return MIXFP4_ERR_NULL;
   if (k > 0 && (!a_codes || !a_scales || !w_codes || !w_scales)) return MIXFP4_ERR_NULL;
   if (!aligned(c, 4)) return MIXFP4_ERR_ALIGN;
@@ -206,10 +210,84 @@ int mixfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_
   if ((a_tensor_scale && !aligned(a_tensor_scale, 4)) ||
       (w_tensor_scale && !aligned(w_tensor_scale, 4)))
     return MIXFP4_ERR_ALIGN;
+  return MIXFP4_OK;
+}
+}  // namespace
+
+int mixfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_tensor_scale,
+                const uint8_t* w_codes, const uint8_t* w_scales, const float* w_tensor_scale,
+                int64_t m, int64_t n, int64_t k, float* c, void* stream) {
+  const int st = gemm_check(a_codes, a_scales, a_tensor_scale, w_codes, w_scales, w_tensor_scale,
+                            m, n, k, c);
+  if (st != MIXFP4_OK) return st == kEmpty ? MIXFP4_OK : st;
   (void)hipGetLastError();
   return launch_status(mixfp4::launch_gemm(a_codes, a_scales, a_tensor_scale, w_codes, w_scales,
                                            w_tensor_scale, m, n, k, c,
                                            static_cast<hipStream_t>(stream)));
+}
+
+int mixfp4_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t* bytes) {
+  if (!bytes) return MIXFP4_ERR_NULL;
+  if (m < 0 || n < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;
+  *bytes = mixfp4::gemm_two_pass_workspace(m, n, k);
+  return MIXFP4_OK;
+}
+
+int mixfp4_gemm_ws(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_tensor_scale,
+                   const uint8_t* w_codes, const uint8_t* w_scales, const float* w_tensor_scale,
+                   int64_t m, int64_t n, int64_t k, float* c, void* workspace,
+                   int64_t workspace_bytes, void* stream) {
+  const int st = gemm_check(a_codes, a_scales, a_tensor_scale, w_codes, w_scales, w_tensor_scale,
+                            m, n, k, c);
+  if (st != MIXFP4_OK) return st == kEmpty ? MIXFP4_OK : st;
+  if (workspace_bytes < 0) return MIXFP4_ERR_SHAPE;
+  if (workspace && !aligned(workspace, 256)) return MIXFP4_ERR_ALIGN;
+  (void)hipGetLastError();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t need = mixfp4::gemm_two_pass_workspace(m, n, k);
+  if (need > 0 && workspace && workspace_bytes >= need)
+    return launch_status(mixfp4::launch_gemm_two_pass(a_codes, a_scales, a_tensor_scale, w_codes,
+                                                      w_scales, w_tensor_scale, m, n, k, c,
+                                                      static_cast<uint8_t*>(workspace), s));
+  return launch_status(mixfp4::launch_gemm(a_codes, a_scales, a_tensor_scale, w_codes, w_scales,
+                                           w_tensor_scale, m, n, k, c, s));
+}
+
+int mixfp4_decode_operand(const uint8_t* codes, const uint8_t* scales, int64_t rows, int64_t k,
+                          void* out, int64_t out_bytes, int64_t* bytes_needed, void* stream) {
+  if (rows < 0 || k < 0 || (k % 32) != 0 || k > (int64_t(1) << 22)) return MIXFP4_ERR_SHAPE;
+  const int64_t need = mixfp4::decoded_bytes(rows, k);
+  if (bytes_needed) *bytes_needed = need;
+  if (!out && out_bytes == 0) return MIXFP4_OK;        // size query
+  if (rows == 0 || k == 0) return MIXFP4_OK;
+  if (!codes || !scales || !out) return MIXFP4_ERR_NULL;
+  if (out_bytes < need) return MIXFP4_ERR_SHAPE;
+  if (!aligned(codes, 16) || !aligned(out, 256)) return MIXFP4_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launch_status(mixfp4::launch_decode_blocked(codes, scales, rows, k,
+                                                     static_cast<uint8_t*>(out),
+                                                     static_cast<hipStream_t>(stream)));
+}
+
+int mixfp4_gemm_decoded(const void* a_decoded, const float* a_tensor_scale,
+                        const void* w_decoded, const float* w_tensor_scale, int64_t m, int64_t n,
+                        int64_t k, float* c, void* stream) {
+  if (m < 0 || n < 0 || k < 0 || (k % 32) != 0 || k > (int64_t(1) << 22)) return MIXFP4_ERR_SHAPE;
+  if (m == 0 || n == 0) return MIXFP4_OK;
+  if (!c || (k > 0 && (!a_decoded || !w_decoded))) return MIXFP4_ERR_NULL;
+  if (!aligned(c, 4) || (k > 0 && (!aligned(a_decoded, 256) || !aligned(w_decoded, 256))))
+    return MIXFP4_ERR_ALIGN;
+  if ((a_tensor_scale && !aligned(a_tensor_scale, 4)) ||
+      (w_tensor_scale && !aligned(w_tensor_scale, 4)))
+    return MIXFP4_ERR_ALIGN;
+  (void)hipGetLastError();
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (k == 0)   // the fused path writes the zeros of an empty reduction
+    return launch_status(mixfp4::launch_gemm(nullptr, nullptr, nullptr, nullptr, nullptr,
+                                             nullptr, m, n, 0, c, s));
+  return launch_status(mixfp4::launch_gemm_decoded(
+      static_cast<const uint8_t*>(a_decoded), a_tensor_scale,
+      static_cast<const uint8_t*>(w_decoded), w_tensor_scale, m, n, k, c, s));
 }
 
 }  // extern "C"

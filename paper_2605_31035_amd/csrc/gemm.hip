@@ -36,60 +36,17 @@
 // decode as zeros; stores are masked.
 #include <type_traits>
 
+#include "decode.h"
 #include "formats.h"
 #include "internal.h"
+#include "tile_order.h"
 
 namespace mixfp4 {
 namespace {
 
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kStepBlocks = 4;               // scale blocks per K step (64 elements)
-
-// High bytes of the fp16 values of magnitudes 0..7 (bytes 0-3 in the low
-// dword): E2M1 {0, .5, 1, 1.5, 2, 3, 4, 6} and E1M2 x2 = INT4 {0, ..., 7}.
-constexpr uint32_t kE2M1Lo = 0x3E3C3800u, kE2M1Hi = 0x46444240u;
-constexpr uint32_t kInt4Lo = 0x42403C00u, kInt4Hi = 0x47464544u;
-
-// Decoding constants of one block from its scale byte: the codebook's high
-// bytes (by T = bit 7) and s8 = E4M3(bits 6:0) as an fp16 pair.  E4M3 ->
-// fp32 is exact (hardware converter) and so is fp32 -> fp16 (4 significant
-// bits, 2^-9 .. 448), whatever the rounding mode of the packing conversion.
-struct BlockDec {
-  uint32_t lo, hi;
-  f16x2 s8;
-};
-__device__ __forceinline__ BlockDec block_dec(uint32_t sb) {
-  BlockDec d;
-  const bool t1 = (sb & 0x80u) != 0;
-  d.lo = t1 ? kInt4Lo : kE2M1Lo;
-  d.hi = t1 ? kInt4Hi : kE2M1Hi;
-  const float s8 = __builtin_amdgcn_cvt_f32_fp8((int)(sb & 0x7Fu), 0);
-  d.s8 = __builtin_bit_cast(f16x2, __builtin_amdgcn_cvt_pkrtz(s8, s8));
-  return d;
-}
-
-__device__ __forceinline__ uint32_t scale_pair(uint32_t v, f16x2 s8) {
-  return __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, v) * s8);
-}
-
-// Decode one code dword (8 nibbles, element 2j in the low nibble of byte j)
-// of a block into 8 fp16 s8 * v in the order [e0 e2 e4 e6 e1 e3 e5 e7].
-__device__ __forceinline__ uint4 decode8(uint32_t c, const BlockDec& d) {
-  const uint32_t me = c & 0x07070707u;
-  const uint32_t mo = (c >> 4) & 0x07070707u;
-  const uint32_t he = __builtin_amdgcn_perm(d.hi, d.lo, me) | ((c << 4) & 0x80808080u);
-  const uint32_t ho = __builtin_amdgcn_perm(d.hi, d.lo, mo) | (c & 0x80808080u);
-  // selector byte 0x0C yields a zero byte: fp16 pairs {0, hi_a, 0, hi_b}
-  uint4 r;
-  r.x = scale_pair(__builtin_amdgcn_perm(he, he, 0x010C000Cu), d.s8);   // e0 e2
-  r.y = scale_pair(__builtin_amdgcn_perm(he, he, 0x030C020Cu), d.s8);   // e4 e6
-  r.z = scale_pair(__builtin_amdgcn_perm(ho, ho, 0x010C000Cu), d.s8);   // e1 e3
-  r.w = scale_pair(__builtin_amdgcn_perm(ho, ho, 0x030C020Cu), d.s8);   // e5 e7
-  return r;
-}
 
 template <int BM, int BN, int WM, int WN>
 struct Tile {
@@ -154,25 +111,6 @@ __device__ __forceinline__ void sched_slice() {
   __builtin_amdgcn_sched_group_barrier(0x100, N_READ, 0);
   sched_mfma_valu<N_MFMA>();
   __builtin_amdgcn_sched_group_barrier(0x200, N_WRITE, 0);
-}
-
-// Work-item order.  The hardware deals workgroups round-robin over the 8 XCDs,
-// each with its own L2.  xcd_item() turns the launch index into an item index
-// such that every XCD receives one contiguous range of items (a bijection for
-// any count), and grouped_tile() walks tiles in groups of four tile-rows,
-// column by column, so the workgroups resident on one XCD share A and W
-// tiles in that XCD's L2.
-__device__ __forceinline__ int64_t xcd_item(int64_t b, int64_t count) {
-  const int64_t q = count / 8, r = count % 8, x = b % 8, j = b / 8;
-  return x * q + (x < r ? x : r) + j;
-}
-__device__ __forceinline__ int64_t grouped_tile(int64_t i, int64_t ntm, int64_t ntn) {
-  constexpr int64_t kGroup = 4;
-  const int64_t per_group = kGroup * ntn;
-  const int64_t first = (i / per_group) * kGroup;
-  const int64_t rows = ntm - first < kGroup ? ntm - first : kGroup;
-  const int64_t local = i % per_group;
-  return (first + local % rows) * ntn + local / rows;
 }
 
 template <int BM, int BN, int WM, int WN, bool kFast, bool kSchedule>

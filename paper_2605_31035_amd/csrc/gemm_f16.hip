@@ -1,0 +1,325 @@
+// Two-pass MixFP4 GEMM for compute-bound shapes: C = s32_A s32_W A W^T.
+//
+// Pass 1 decodes each operand once into the exact 16-bit values s8 * v
+// (Sec. 3.3, App. B.5; see decode.h) in a blocked layout in the caller's
+// workspace.  Pass 2 is a GEMM on those fp16 operands with fp32 accumulation
+// (Sec. 3.3 keeps the accumulation unchanged) whose main loop issues nothing
+// but matrix instructions, LDS reads and direct global -> LDS loads.
+//
+// Why two passes.  Measured on MI355X, the matrix core's throughput under a
+// sustained fp16 MFMA load is power-limited (the clock settles near 1.6-1.8
+// GHz), and every VALU instruction issued between MFMAs lowers it further: a
+// decode fused into the MFMA loop costs ~6 VALU instructions per 32x32x16
+// MFMA (each element decoded once per 256 x 256 tile), which held the fused
+// kernel below ~0.47 of the fp16 peak.  Decoding once per element instead
+// (16 B of fp16 written and read back per 4.5 bits stored) moves that work to
+// an HBM-bound pass that takes ~4% of the GEMM's time at the large shapes.
+//
+// Blocked operand layout (rows padded to a multiple of 256, K % 32 == 0):
+// block (t, s) = rows [256 t, 256 t + 256) x K [32 s, 32 s + 32) is 16 KB at
+// byte offset (t * K/32 + s) * 16384.  Row r of a block takes 64 bytes at
+// 64 r; its 8-element group g (K 32 s + 8 g ..) is stored at 16-byte slot
+// g ^ ((r >> 2) & 3), in the order [e0 e2 e4 e6 e1 e3 e5 e7] that decode8
+// produces (A and W share the order; a dot product does not depend on it).
+// A whole block is then one contiguous copy into LDS, and the swizzle keeps
+// the 16 lanes of each LDS read pass on distinct banks.
+//
+// GEMM kernel.  A workgroup of 4 waves (one per SIMD) owns a 256 x 256 tile
+// of C; wave w computes rows 128 (w / 2) and columns 128 (w % 2) of it as
+// 4 x 4 v_mfma_f32_32x32x16_f16 tiles (256 accumulator registers).  The K loop
+// steps 32; four LDS stages of 32 KB (A block then W block) hold the steps
+// t .. t+3, filled by 16-byte buffer loads straight into LDS three steps
+// ahead, so global latency hides under three steps of MFMAs.  Each step is
+// two halves of 16 MFMAs (one 16-K slice each): the first half reads the
+// second slice's fragments, a barrier then makes step t+1 visible, and the
+// second half reads step t+1's first slice, so no LDS latency and no barrier
+// sits in front of an MFMA that has nothing else to wait for.
+#include "decode.h"
+#include "internal.h"
+#include "tile_order.h"
+
+typedef int mixfp4_i32x4 __attribute__((ext_vector_type(4)));
+// The 16-byte buffer load that writes straight into LDS (the LLVM intrinsic;
+// its LDS destination is M0 + offset + 16 * lane).
+__device__ void raw_buffer_load_lds(mixfp4_i32x4 rsrc,
+                                    __attribute__((address_space(3))) uint32_t* lds, int size,
+                                    int voffset, int soffset, int offset,
+                                    int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+namespace mixfp4 {
+namespace {
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef mixfp4_i32x4 i32x4;
+
+constexpr int kTileRows = 256;                // rows of A or W per tile
+constexpr int kStepK = 32;                    // K per step (two 16-K MFMA slices)
+constexpr int kBlkBytes = kTileRows * kStepK * 2;   // 16 KB per (tile, step) block
+constexpr int kStageBytes = 2 * kBlkBytes;    // A block then W block
+constexpr int kStages = 4;
+
+__device__ __forceinline__ int slot_of(int r, int g) { return g ^ ((r >> 2) & 3); }
+
+// ---------------------------------------------------------------------------
+// Pass 1: decode a MixFP4 operand [rows, k] into the blocked layout.
+// A workgroup takes items of 32 rows x 8 steps.  Thread (row rl, step j)
+// reads 16 code bytes and two scale bytes (eight lanes cover 128 contiguous
+// code bytes of a row) and decodes them into the row's 64 output bytes in an
+// LDS tile [step][32 rows x 64 B]; after a barrier the tile leaves as eight
+// runs of 2 KB, one per step block (the item's rows are consecutive there),
+// so every store instruction writes contiguous memory.  The next item's loads
+// are issued before the current item's stores.  Rows beyond `rows` decode as
+// zeros into padding rows of the last tile; nothing beyond the padded layout
+// is written.
+constexpr int kDecRows = 32, kDecSteps = 8;
+
+__global__ __launch_bounds__(256) void decode_blocked_kernel(const uint8_t* __restrict__ codes,
+                                                             const uint8_t* __restrict__ scales,
+                                                             int64_t rows, int64_t k,
+                                                             uint8_t* __restrict__ out) {
+  __shared__ uint4 tile[kDecSteps * kDecRows * 4];
+  const int64_t steps = k / kStepK;
+  const int64_t sgroups = (steps + kDecSteps - 1) / kDecSteps;
+  const int64_t items = ((rows + kDecRows - 1) / kDecRows) * sgroups;
+  const int tid = threadIdx.x;
+  const int j = tid & 7, rl = tid >> 3;
+  struct In { uint4 c; uint32_t s0, s1; bool ok; };
+  auto load = [&](In& in, int64_t it) {
+    const int64_t row = (it / sgroups) * kDecRows + rl;
+    const int64_t s = (it % sgroups) * kDecSteps + j;
+    in.ok = it < items && row < rows && s < steps;
+    if (in.ok) {
+      in.c = *reinterpret_cast<const uint4*>(codes + row * (k / 2) + s * 16);
+      const uint8_t* sp = scales + row * (k / kBlock) + 2 * s;
+      in.s0 = sp[0];
+      in.s1 = sp[1];
+    } else {
+      in.c = make_uint4(0u, 0u, 0u, 0u);
+      in.s0 = in.s1 = 0u;
+    }
+  };
+  In cur;
+  int64_t it = blockIdx.x;
+  load(cur, it);
+  for (; it < items; it += gridDim.x) {
+    In nxt;
+    load(nxt, it + gridDim.x);
+    {
+      const BlockDec d0 = block_dec(cur.s0), d1 = block_dec(cur.s1);
+      const int r = (int)(((it / sgroups) * kDecRows + rl) % kTileRows);
+      uint4* t = tile + (j * kDecRows + rl) * 4;
+      t[slot_of(r, 0)] = decode8(cur.c.x, d0);
+      t[slot_of(r, 1)] = decode8(cur.c.y, d0);
+      t[slot_of(r, 2)] = decode8(cur.c.z, d1);
+      t[slot_of(r, 3)] = decode8(cur.c.w, d1);
+    }
+    __syncthreads();
+    const int64_t row0 = (it / sgroups) * kDecRows;
+    const int64_t s0 = (it % sgroups) * kDecSteps;
+    uint8_t* ob = out + (row0 / kTileRows) * steps * kBlkBytes + (row0 % kTileRows) * 64;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int ch = tid + 256 * q;          // 16-byte chunk of the tile
+      const int sj = ch >> 7;                // step within the item (128 chunks each)
+      if (s0 + sj < steps)
+        *reinterpret_cast<uint4*>(ob + (s0 + sj) * kBlkBytes + (ch & 127) * 16) = tile[ch];
+    }
+    __syncthreads();
+    cur = nxt;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Pass 2: the fp16 GEMM on blocked operands.
+
+// Buffer resource of a raw byte range (stride 0, 32-bit data format word of
+// the gfx9 descriptor); loads past `bytes` return zeros.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  i32x4 r;
+  r[0] = (int)(uint32_t)b;
+  r[1] = (int)(uint32_t)(b >> 32);
+  r[2] = (int)bytes;
+  r[3] = 0x00020000;
+  return r;
+}
+
+__global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restrict__ ablk,
+                                                         const uint8_t* __restrict__ wblk,
+                                                         const float* __restrict__ a_ts,
+                                                         const float* __restrict__ w_ts,
+                                                         int64_t m, int64_t n, int64_t k,
+                                                         float* __restrict__ c, int64_t ldc) {
+  typedef _Float16 f16x8v __attribute__((ext_vector_type(8)));
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kStageBytes];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t steps = k / kStepK;
+  const int64_t ntm = (m + kTileRows - 1) / kTileRows, ntn = (n + kTileRows - 1) / kTileRows;
+  const int64_t tile = grouped_tile(xcd_item(blockIdx.x, gridDim.x), ntm, ntn);
+  const int64_t tm = tile / ntn, tn = tile % ntn;
+
+  // Waves 0-1 copy halves (8 KB) of the A block of each step, waves 2-3 of
+  // the W block: 8 loads of 1 KB per wave and step.
+  const bool is_a = wave < 2;
+  const uint8_t* src = (is_a ? ablk + tm * steps * kBlkBytes : wblk + tn * steps * kBlkBytes) +
+                       (wave & 1) * (kBlkBytes / 2);
+  const i32x4 rsrc = make_rsrc(src, (uint32_t)(steps * kBlkBytes));
+  const int ldst = (is_a ? 0 : kBlkBytes) + (wave & 1) * (kBlkBytes / 2);
+  auto issue = [&](int stage, int64_t st) {
+    auto* l0 = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(
+        reinterpret_cast<uintptr_t>(lds) + stage * kStageBytes + ldst);
+    auto* l1 = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(
+        reinterpret_cast<uintptr_t>(lds) + stage * kStageBytes + ldst + 4096);
+    const int so = (int)(st * kBlkBytes);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) raw_buffer_load_lds(rsrc, l0, 16, lane * 16, so, i * 1024, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) raw_buffer_load_lds(rsrc, l1, 16, lane * 16, so + 4096, i * 1024, 0);
+  };
+
+  const int wm = (wave >> 1) * 128, wn = (wave & 1) * 128;
+  const int half = lane >> 5, lrow = lane & 31;
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+
+  // fragments of one 16-K slice: 4 A and 4 W 32-row tiles; lane (lrow, half)
+  // takes the 8-element group 2 sl + half of its row
+  typedef f16x8v Frag[4];
+  auto read = [&](Frag& fa, Frag& fw, int stage, int sl) {
+    const uint8_t* b = lds + stage * kStageBytes;
+    const int g = 2 * sl + half;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = wm + 32 * i + lrow;
+      fa[i] = *reinterpret_cast<const f16x8v*>(b + r * 64 + slot_of(r, g) * 16);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int r = wn + 32 * j + lrow;
+      fw[j] = *reinterpret_cast<const f16x8v*>(b + kBlkBytes + r * 64 + slot_of(r, g) * 16);
+    }
+  };
+  auto mfmas = [&](const Frag& fa, const Frag& fw) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fw[j], acc[i][j], 0, 0, 0);
+  };
+  // At the barrier of step t, step t+1's loads (issued at step t-2) must have
+  // landed: the two later steps' 16 loads may still be in flight.  The LDS
+  // reads of the step are complete too, so the stage refilled after the
+  // barrier is free in every wave.
+  auto wait_loads = [&]() { asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory"); };
+
+  const int64_t last = steps - 1;
+#pragma unroll
+  for (int p = 0; p < kStages - 1; ++p) issue(p, p < last ? p : last);
+  wait_loads();
+  __builtin_amdgcn_s_barrier();
+  Frag pa, pw, qa, qw;
+  read(pa, pw, 0, 0);
+  // Invariant at the top of step t: P holds slice 0 of step t; steps t+1 and
+  // t+2 are in flight or landed.  Loads and reads past the last step are
+  // clamped to it (they refill a stage that is never read again).
+  for (int64_t t = 0; t < steps; ++t) {
+    const int cur = (int)(t % kStages);
+    const int64_t tl = t + kStages - 1 < last ? t + kStages - 1 : last;
+    issue((int)((t + kStages - 1) % kStages), tl);   // the stage of step t-1
+    read(qa, qw, cur, 1);
+    mfmas(pa, pw);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global -> LDS load
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    wait_loads();
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    read(pa, pw, (int)((t + 1) % kStages), 0);
+    mfmas(qa, qw);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
+  const int64_t m0 = tm * kTileRows + wm, n0 = tn * kTileRows + wn;
+  // 32 x 32 accumulator layout: lane holds column lane%32; register q holds
+  // row 8*(q/4) + 4*(lane/32) + q%4.
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t col = n0 + j * 32 + lrow;
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int64_t row = m0 + i * 32 + 8 * (q >> 2) + 4 * half + (q & 3);
+        if (row < m && col < n) c[row * ldc + col] = acc[i][j][q] * scale;
+      }
+    }
+}
+
+int64_t padded_rows(int64_t rows) { return (rows + kTileRows - 1) / kTileRows * kTileRows; }
+
+}  // namespace
+
+bool gemm_two_pass_applies(int64_t m, int64_t n, int64_t k) {
+  // k <= 2^22 keeps a tile-row's blocks (k/32 x 16 KB) inside a 32-bit buffer range
+  return m > 16 && n > 0 && k > 0 && k % kStepK == 0 && k <= (int64_t(1) << 22);
+}
+
+int64_t gemm_two_pass_workspace(int64_t m, int64_t n, int64_t k) {
+  if (!gemm_two_pass_applies(m, n, k)) return 0;
+  return (padded_rows(m) + padded_rows(n)) * k * 2;
+}
+
+hipError_t launch_decode_blocked(const uint8_t* codes, const uint8_t* scales, int64_t rows,
+                                 int64_t k, uint8_t* out, hipStream_t stream) {
+  static ResidentCache cache{};
+  const int64_t items = ((rows + kDecRows - 1) / kDecRows) * ((k / kStepK + kDecSteps - 1) / kDecSteps);
+  int64_t grid = resident_groups(decode_blocked_kernel, cache, 8, 256);
+  if (grid > items) grid = items;
+  if (grid < 1) grid = 1;
+  decode_blocked_kernel<<<(unsigned)grid, 256, 0, stream>>>(codes, scales, rows, k, out);
+  return hipGetLastError();
+}
+
+int64_t decoded_bytes(int64_t rows, int64_t k) { return padded_rows(rows) * k * 2; }
+
+hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uint8_t* wblk,
+                               const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
+                               hipStream_t stream) {
+  const unsigned tiles = (unsigned)((padded_rows(m) / kTileRows) * (padded_rows(n) / kTileRows));
+  gemm_f16_kernel<<<tiles, 256, 0, stream>>>(ablk, wblk, a_ts, w_ts, m, n, k, c, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemm_two_pass(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
+                                const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
+                                int64_t m, int64_t n, int64_t k, float* c, uint8_t* workspace,
+                                hipStream_t stream) {
+  uint8_t* ablk = workspace;
+  uint8_t* wblk = workspace + decoded_bytes(m, k);
+  hipError_t e = launch_decode_blocked(a_codes, a_scales, m, k, ablk, stream);
+  if (e != hipSuccess) return e;
+  e = launch_decode_blocked(w_codes, w_scales, n, k, wblk, stream);
+  if (e != hipSuccess) return e;
+  return launch_gemm_decoded(ablk, a_ts, wblk, w_ts, m, n, k, c, stream);
+}
+
+}  // namespace mixfp4

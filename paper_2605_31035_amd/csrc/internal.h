@@ -115,5 +115,22 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales,
                        const float* a_ts, const uint8_t* w_codes,
                        const uint8_t* w_scales, const float* w_ts, int64_t m,
                        int64_t n, int64_t k, float* c, hipStream_t stream);
+// Two-pass GEMM (operands decoded once into a blocked fp16 layout in
+// `workspace`, then an fp16 GEMM): applies for m > 16 and k % 32 == 0, and
+// needs gemm_two_pass_workspace(m, n, k) bytes of 256-byte aligned workspace.
+bool gemm_two_pass_applies(int64_t m, int64_t n, int64_t k);
+int64_t gemm_two_pass_workspace(int64_t m, int64_t n, int64_t k);
+hipError_t launch_gemm_two_pass(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
+                                const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
+                                int64_t m, int64_t n, int64_t k, float* c, uint8_t* workspace,
+                                hipStream_t stream);
+// The two passes on their own: bytes of one decoded operand [rows, k]
+// (rows padded to 256, k % 32 == 0), its decode, and the GEMM on two of them.
+int64_t decoded_bytes(int64_t rows, int64_t k);
+hipError_t launch_decode_blocked(const uint8_t* codes, const uint8_t* scales, int64_t rows,
+                                 int64_t k, uint8_t* out, hipStream_t stream);
+hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uint8_t* wblk,
+                               const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
+                               hipStream_t stream);
 
 }  // namespace mixfp4

@@ -228,3 +228,47 @@ def test_binding_quantize_rejects_bad_outputs():
         M.mixfp4_quantize(x, codes=good_c, scales=good_s, transpose=True)
     with pytest.raises(ValueError, match="CUDA tensor"):
         M.mixfp4_quantize(x, codes=good_c, scales=good_s)
+
+
+def test_gemm_ws_rejects(lib):
+    f = lib.mixfp4_gemm_ws
+    args = lambda **kw: [kw.get("ac", A16), kw.get("as_", A16), None, kw.get("wc", A16),
+                         kw.get("ws", A16), None, kw.get("m", 64), kw.get("n", 64),
+                         kw.get("k", 64), kw.get("c", A16), kw.get("work", P(0x10000)),
+                         kw.get("wb", 1 << 20), None]
+    assert f(*args(k=24)) == 2                      # k % 16
+    assert f(*args(m=-1)) == 2
+    assert f(*args(wb=-1)) == 2                     # negative workspace size
+    assert f(*args(c=None)) == 1
+    assert f(*args(ac=None)) == 1
+    assert f(*args(work=P(0x10080))) == 3           # workspace not 256-byte aligned
+    assert f(*args(c=P(0x10002))) == 3
+    assert f(*args(m=0)) == 0                       # nothing to compute, nothing launched
+
+
+def test_gemm_workspace_size(lib):
+    b = ctypes.c_int64(-1)
+    assert lib.mixfp4_gemm_workspace_size(16384, 8192, 8192, ctypes.byref(b)) == 0
+    assert b.value == (16384 + 8192) * 8192 * 2
+    assert lib.mixfp4_gemm_workspace_size(300, 1000, 288, ctypes.byref(b)) == 0
+    assert b.value == (512 + 1024) * 288 * 2
+    assert lib.mixfp4_gemm_workspace_size(16, 4096, 4096, ctypes.byref(b)) == 0 and b.value == 0
+    assert lib.mixfp4_gemm_workspace_size(64, 64, 48, ctypes.byref(b)) == 0 and b.value == 0
+    assert lib.mixfp4_gemm_workspace_size(64, 64, 40, ctypes.byref(b)) == 2
+    assert lib.mixfp4_gemm_workspace_size(64, 64, 64, None) == 1
+
+
+def test_decode_operand_and_decoded_gemm_reject(lib):
+    need = ctypes.c_int64(-1)
+    assert lib.mixfp4_decode_operand(None, None, 300, 288, None, 0, ctypes.byref(need), None) == 0
+    assert need.value == 512 * 288 * 2
+    assert lib.mixfp4_decode_operand(A16, A16, 300, 48, A16, 1 << 30, None, None) == 2   # k % 32
+    assert lib.mixfp4_decode_operand(A16, A16, -1, 64, A16, 1 << 30, None, None) == 2
+    assert lib.mixfp4_decode_operand(A16, A16, 300, 288, P(0x10000), 1000, None, None) == 2  # short
+    assert lib.mixfp4_decode_operand(A16, A16, 300, 288, P(0x10010), 1 << 30, None, None) == 3
+    assert lib.mixfp4_decode_operand(None, A16, 300, 288, P(0x10000), 1 << 30, None, None) == 1
+    g = lib.mixfp4_gemm_decoded
+    assert g(P(0x10000), None, P(0x10000), None, 64, 64, 48, A16, None) == 2
+    assert g(P(0x10000), None, P(0x10040), None, 64, 64, 64, A16, None) == 3
+    assert g(P(0x10000), None, None, None, 64, 64, 64, A16, None) == 1
+    assert g(P(0x10000), None, P(0x10000), None, 0, 64, 64, None, None) == 0
