@@ -26,7 +26,9 @@
 //
 // GEMM kernel.  A workgroup of 4 waves (one per SIMD) owns a 256 x 256 tile
 // of C; wave w computes rows 128 (w / 2) and columns 128 (w % 2) of it as
-// 4 x 4 v_mfma_f32_32x32x16_f16 tiles (256 accumulator registers).  The K loop
+// 4 x 4 v_mfma_f32_32x32x16_f16 tiles (256 accumulator registers), with W as
+// the first operand so that each lane ends up holding runs of four
+// consecutive columns of one C row (16-byte stores in the epilogue).  The K loop
 // steps 32; four LDS stages of 32 KB (A block then W block) hold the steps
 // t .. t+3, filled by 16-byte buffer loads straight into LDS three steps
 // ahead, so global latency hides under three steps of MFMAs.  Each step is
@@ -205,12 +207,14 @@ __global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restr
       fw[j] = *reinterpret_cast<const f16x8v*>(b + kBlkBytes + r * 64 + slot_of(r, g) * 16);
     }
   };
+  // W fragments are the first operand, so the accumulator tile is C^T: a lane
+  // holds row m of C and each register quad four consecutive columns
   auto mfmas = [&](const Frag& fa, const Frag& fw) {
 #pragma unroll
     for (int i = 0; i < 4; ++i)
 #pragma unroll
       for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fa[i], fw[j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fw[j], fa[i], acc[i][j], 0, 0, 0);
   };
   // At the barrier of step t, step t+1's loads (issued at step t-2) must have
   // landed: the two later steps' 16 loads may still be in flight.  The LDS
@@ -259,19 +263,34 @@ __global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restr
 
   const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
   const int64_t m0 = tm * kTileRows + wm, n0 = tn * kTileRows + wn;
-  // 32 x 32 accumulator layout: lane holds column lane%32; register q holds
-  // row 8*(q/4) + 4*(lane/32) + q%4.
+  // 32 x 32 accumulator layout of C^T: lane holds row m0 + 32 i + lane%32;
+  // register q holds column 32 j + 8*(q/4) + 4*(lane/32) + q%4.  Four
+  // consecutive registers are four consecutive columns: one 16-byte store
+  // when C's rows keep 16-byte alignment (n % 4 == 0, C 16-byte aligned).
+  const bool vec = (ldc % 4) == 0 && (reinterpret_cast<uintptr_t>(c) & 15u) == 0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < 4; ++i) {
+    const int64_t row = m0 + i * 32 + lrow;
+    if (row >= m) continue;
+    float* crow = c + row * ldc;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t col = n0 + j * 32 + lrow;
+    for (int j = 0; j < 4; ++j)
 #pragma unroll
-      for (int q = 0; q < 16; ++q) {
-        const int64_t row = m0 + i * 32 + 8 * (q >> 2) + 4 * half + (q & 3);
-        if (row < m && col < n) c[row * ldc + col] = acc[i][j][q] * scale;
+      for (int qq = 0; qq < 4; ++qq) {
+        const int64_t col = n0 + j * 32 + 8 * qq + 4 * half;
+        const f32x16& v = acc[i][j];
+        if (vec) {
+          if (col < n)
+            *reinterpret_cast<float4*>(crow + col) =
+                make_float4(v[4 * qq] * scale, v[4 * qq + 1] * scale, v[4 * qq + 2] * scale,
+                            v[4 * qq + 3] * scale);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < n) crow[col + e] = v[4 * qq + e] * scale;
+        }
       }
-    }
+  }
 }
 
 int64_t padded_rows(int64_t rows) { return (rows + kTileRows - 1) / kTileRows * kTileRows; }
