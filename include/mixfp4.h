@@ -43,7 +43,8 @@ typedef enum {
                              or a bad Hadamard block size                 */
   MIXFP4_ERR_ALIGN = 3,   /* a pointer misses its required alignment         */
   MIXFP4_ERR_FLAGS = 4,   /* unknown flag bits                               */
-  MIXFP4_ERR_LAUNCH = 5   /* the HIP runtime rejected a kernel launch        */
+  MIXFP4_ERR_LAUNCH = 5,  /* the HIP runtime rejected a kernel launch        */
+  MIXFP4_ERR_SCRATCH = 6  /* mixfp4_gemm_noalloc: static workspace too small  */
 } mixfp4_status;
 
 /* Tensor-scale modes of mixfp4_quantize (flags argument). */
@@ -254,6 +255,28 @@ int mixfp4_gemm_ws(const uint8_t *a_codes, const uint8_t *a_scales,
                    int64_t workspace_bytes, void *stream);
 
 /*
+ * mixfp4_gemm_noalloc - mixfp4_gemm_ws for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation): the workspace is the library's own static device
+ * array of mixfp4_gemm_noalloc_max_bytes() bytes (64 MiB), which each GPU the
+ * library runs on holds until the process ends.  The call itself allocates
+ * nothing.  Where mixfp4_gemm_ws would take the two-pass path the shape's
+ * workspace (mixfp4_gemm_workspace_size) must fit in that array, else
+ * MIXFP4_ERR_SCRATCH is returned and nothing is enqueued; decode shapes and
+ * k % 32 != 0 run the fused kernel as mixfp4_gemm does.  The result equals
+ * mixfp4_gemm_ws's bit for bit.  Every call on a GPU shares that GPU's
+ * array, and calls whose work overlaps in time on one GPU (different
+ * streams, or threads without ordering) race on it; calls ordered on one
+ * stream do not.  `stream` must belong to the calling thread's current
+ * device.
+ */
+int mixfp4_gemm_noalloc(const uint8_t *a_codes, const uint8_t *a_scales,
+                        const float *a_tensor_scale, const uint8_t *w_codes,
+                        const uint8_t *w_scales, const float *w_tensor_scale,
+                        int64_t m, int64_t n, int64_t k, float *c, void *stream);
+int64_t mixfp4_gemm_noalloc_max_bytes(void);
+
+/*
  * mixfp4_gemm_workspace_size - bytes of workspace with which mixfp4_gemm_ws
  * takes the two-pass path for this shape: 2 * k * (m + n) rounded up to
  * whole 256-row tiles of A and of W, or 0 where that path does not apply.
@@ -301,7 +324,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 105
+#define MIXFP4_ABI_VERSION 106
 
 #ifdef __cplusplus
 }

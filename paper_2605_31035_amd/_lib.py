@@ -16,7 +16,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libmixfp4.s
 SYMBOLS = ("mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_quantize_2d", "mixfp4_hadamard",
            "mixfp4_dequantize",
            "mixfp4_gemm", "mixfp4_gemm_ws", "mixfp4_gemm_workspace_size",
-           "mixfp4_decode_operand", "mixfp4_gemm_decoded",
+           "mixfp4_decode_operand", "mixfp4_gemm_decoded", "mixfp4_gemm_noalloc",
+           "mixfp4_gemm_noalloc_max_bytes",
            "mixfp4_status_string", "mixfp4_last_launch_error", "mixfp4_abi_version")
 
 
@@ -52,6 +53,10 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     h.mixfp4_decode_operand.restype = i32
     h.mixfp4_gemm_decoded.argtypes = [vp, vp, vp, vp, i64, i64, i64, vp, vp]
     h.mixfp4_gemm_decoded.restype = i32
+    h.mixfp4_gemm_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, i64, i64, i64, vp, vp]
+    h.mixfp4_gemm_noalloc.restype = i32
+    h.mixfp4_gemm_noalloc_max_bytes.argtypes = []
+    h.mixfp4_gemm_noalloc_max_bytes.restype = i64
     h.mixfp4_status_string.argtypes = [i32]
     h.mixfp4_status_string.restype = ctypes.c_char_p
     h.mixfp4_last_launch_error.argtypes = []

@@ -116,6 +116,7 @@ const char* mixfp4_status_string(int status) {
     case MIXFP4_ERR_ALIGN: return "MIXFP4_ERR_ALIGN: pointer misaligned";
     case MIXFP4_ERR_FLAGS: return "MIXFP4_ERR_FLAGS: unknown flag bits, or more than one format mode";
     case MIXFP4_ERR_LAUNCH: return "MIXFP4_ERR_LAUNCH: kernel launch failed";
+    case MIXFP4_ERR_SCRATCH: return "MIXFP4_ERR_SCRATCH: the shape needs more than the library's static workspace (mixfp4_gemm_noalloc), or its address could not be obtained";
     default: return "unknown mixfp4 status";
   }
 }
@@ -252,6 +253,29 @@ int mixfp4_gemm_ws(const uint8_t* a_codes, const uint8_t* a_scales, const float*
   return launch_status(mixfp4::launch_gemm(a_codes, a_scales, a_tensor_scale, w_codes, w_scales,
                                            w_tensor_scale, m, n, k, c, s));
 }
+
+int mixfp4_gemm_noalloc(const uint8_t* a_codes, const uint8_t* a_scales,
+                        const float* a_tensor_scale, const uint8_t* w_codes,
+                        const uint8_t* w_scales, const float* w_tensor_scale, int64_t m, int64_t n,
+                        int64_t k, float* c, void* stream) {
+  const int st = gemm_check(a_codes, a_scales, a_tensor_scale, w_codes, w_scales, w_tensor_scale,
+                            m, n, k, c);
+  if (st != MIXFP4_OK) return st == kEmpty ? MIXFP4_OK : st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t need = mixfp4::gemm_two_pass_workspace(m, n, k);
+  (void)hipGetLastError();
+  if (need == 0)   // decode shapes and k % 32 != 0: the fused kernel, no workspace
+    return launch_status(mixfp4::launch_gemm(a_codes, a_scales, a_tensor_scale, w_codes,
+                                             w_scales, w_tensor_scale, m, n, k, c, s));
+  if (need > mixfp4::kStaticScratchBytes) return MIXFP4_ERR_SCRATCH;
+  void* ws = nullptr;
+  if (mixfp4::static_scratch(&ws) != hipSuccess || !ws) return MIXFP4_ERR_SCRATCH;
+  return launch_status(mixfp4::launch_gemm_two_pass(a_codes, a_scales, a_tensor_scale, w_codes,
+                                                    w_scales, w_tensor_scale, m, n, k, c,
+                                                    static_cast<uint8_t*>(ws), s));
+}
+
+int64_t mixfp4_gemm_noalloc_max_bytes(void) { return mixfp4::kStaticScratchBytes; }
 
 int mixfp4_decode_operand(const uint8_t* codes, const uint8_t* scales, int64_t rows, int64_t k,
                           void* out, int64_t out_bytes, int64_t* bytes_needed, void* stream) {

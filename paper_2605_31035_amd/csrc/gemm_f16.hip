@@ -36,6 +36,8 @@
 // second slice's fragments, a barrier then makes step t+1 visible, and the
 // second half reads step t+1's first slice, so no LDS latency and no barrier
 // sits in front of an MFMA that has nothing else to wait for.
+#include <mutex>
+
 #include "decode.h"
 #include "internal.h"
 #include "tile_order.h"
@@ -339,6 +341,36 @@ hipError_t launch_gemm_two_pass(const uint8_t* a_codes, const uint8_t* a_scales,
   e = launch_decode_blocked(w_codes, w_scales, n, k, wblk, stream);
   if (e != hipSuccess) return e;
   return launch_gemm_decoded(ablk, a_ts, wblk, w_ts, m, n, k, c, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Workspace for callers that cannot allocate: a file-scope device array that
+// each GPU the library runs on holds until the process ends.  Host code never
+// passes `scratch` itself (on the host the name is only a stand-in for the
+// symbol): it takes the array's device address once per device with
+// hipGetSymbolAddress and passes that pointer to the kernels.
+namespace {
+static __device__ __align__(256) uint8_t scratch[kStaticScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+hipError_t static_scratch(void** ptr) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = p;
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 }  // namespace mixfp4

@@ -132,5 +132,10 @@ hipError_t launch_decode_blocked(const uint8_t* codes, const uint8_t* scales, in
 hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uint8_t* wblk,
                                const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
                                hipStream_t stream);
+// The library's static workspace (mixfp4_gemm_noalloc): kStaticScratchBytes
+// of device memory per GPU; *ptr receives its device address on the current
+// device (looked up once per device).
+constexpr int64_t kStaticScratchBytes = int64_t(64) << 20;
+hipError_t static_scratch(void** ptr);
 
 }  // namespace mixfp4
