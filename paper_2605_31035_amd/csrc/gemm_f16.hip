@@ -1,8 +1,8 @@
 // Two-pass MixFP4 GEMM for compute-bound shapes: C = s32_A s32_W A W^T.
 //
-// Pass 1 decodes each operand once into the exact 16-bit values s8 * v
-// (Sec. 3.3, App. B.5; see decode.h) in a blocked layout in the caller's
-// workspace.  Pass 2 is a GEMM on those fp16 operands with fp32 accumulation
+// Pass 1 (decode_operand.hip) decodes each operand once into the exact
+// 16-bit values s8 * v (Sec. 3.3, App. B.5) in a blocked layout in the
+// caller's workspace.  Pass 2 is a GEMM on those fp16 operands with fp32 accumulation
 // (Sec. 3.3 keeps the accumulation unchanged) whose main loop issues nothing
 // but matrix instructions, LDS reads and direct global -> LDS loads.
 //
@@ -15,14 +15,7 @@
 // (16 B of fp16 written and read back per 4.5 bits stored) moves that work to
 // an HBM-bound pass that takes ~4% of the GEMM's time at the large shapes.
 //
-// Blocked operand layout (rows padded to a multiple of 256, K % 32 == 0):
-// block (t, s) = rows [256 t, 256 t + 256) x K [32 s, 32 s + 32) is 16 KB at
-// byte offset (t * K/32 + s) * 16384.  Row r of a block takes 64 bytes at
-// 64 r; its 8-element group g (K 32 s + 8 g ..) is stored at 16-byte slot
-// g ^ ((r >> 2) & 3), in the order [e0 e2 e4 e6 e1 e3 e5 e7] that decode8
-// produces (A and W share the order; a dot product does not depend on it).
-// A whole block is then one contiguous copy into LDS, and the swizzle keeps
-// the 16 lanes of each LDS read pass on distinct banks.
+// The operands arrive in the blocked layout of blocked_layout.h.
 //
 // GEMM kernel.  A workgroup of 4 waves (one per SIMD) owns a 256 x 256 tile
 // of C; wave w computes rows 128 (w / 2) and columns 128 (w % 2) of it as
@@ -38,7 +31,7 @@
 // sits in front of an MFMA that has nothing else to wait for.
 #include <mutex>
 
-#include "decode.h"
+#include "blocked_layout.h"
 #include "internal.h"
 #include "tile_order.h"
 
@@ -56,82 +49,7 @@ namespace {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef mixfp4_i32x4 i32x4;
 
-constexpr int kTileRows = 256;                // rows of A or W per tile
-constexpr int kStepK = 32;                    // K per step (two 16-K MFMA slices)
-constexpr int kBlkBytes = kTileRows * kStepK * 2;   // 16 KB per (tile, step) block
-constexpr int kStageBytes = 2 * kBlkBytes;    // A block then W block
 constexpr int kStages = 4;
-
-__device__ __forceinline__ int slot_of(int r, int g) { return g ^ ((r >> 2) & 3); }
-
-// ---------------------------------------------------------------------------
-// Pass 1: decode a MixFP4 operand [rows, k] into the blocked layout.
-// A workgroup takes items of 32 rows x 8 steps.  Thread (row rl, step j)
-// reads 16 code bytes and two scale bytes (eight lanes cover 128 contiguous
-// code bytes of a row) and decodes them into the row's 64 output bytes in an
-// LDS tile [step][32 rows x 64 B]; after a barrier the tile leaves as eight
-// runs of 2 KB, one per step block (the item's rows are consecutive there),
-// so every store instruction writes contiguous memory.  The next item's loads
-// are issued before the current item's stores.  Rows beyond `rows` decode as
-// zeros into padding rows of the last tile; nothing beyond the padded layout
-// is written.
-constexpr int kDecRows = 32, kDecSteps = 8;
-
-__global__ __launch_bounds__(256) void decode_blocked_kernel(const uint8_t* __restrict__ codes,
-                                                             const uint8_t* __restrict__ scales,
-                                                             int64_t rows, int64_t k,
-                                                             uint8_t* __restrict__ out) {
-  __shared__ uint4 tile[kDecSteps * kDecRows * 4];
-  const int64_t steps = k / kStepK;
-  const int64_t sgroups = (steps + kDecSteps - 1) / kDecSteps;
-  const int64_t items = ((rows + kDecRows - 1) / kDecRows) * sgroups;
-  const int tid = threadIdx.x;
-  const int j = tid & 7, rl = tid >> 3;
-  struct In { uint4 c; uint32_t s0, s1; bool ok; };
-  auto load = [&](In& in, int64_t it) {
-    const int64_t row = (it / sgroups) * kDecRows + rl;
-    const int64_t s = (it % sgroups) * kDecSteps + j;
-    in.ok = it < items && row < rows && s < steps;
-    if (in.ok) {
-      in.c = *reinterpret_cast<const uint4*>(codes + row * (k / 2) + s * 16);
-      const uint8_t* sp = scales + row * (k / kBlock) + 2 * s;
-      in.s0 = sp[0];
-      in.s1 = sp[1];
-    } else {
-      in.c = make_uint4(0u, 0u, 0u, 0u);
-      in.s0 = in.s1 = 0u;
-    }
-  };
-  In cur;
-  int64_t it = blockIdx.x;
-  load(cur, it);
-  for (; it < items; it += gridDim.x) {
-    In nxt;
-    load(nxt, it + gridDim.x);
-    {
-      const BlockDec d0 = block_dec(cur.s0), d1 = block_dec(cur.s1);
-      const int r = (int)(((it / sgroups) * kDecRows + rl) % kTileRows);
-      uint4* t = tile + (j * kDecRows + rl) * 4;
-      t[slot_of(r, 0)] = decode8(cur.c.x, d0);
-      t[slot_of(r, 1)] = decode8(cur.c.y, d0);
-      t[slot_of(r, 2)] = decode8(cur.c.z, d1);
-      t[slot_of(r, 3)] = decode8(cur.c.w, d1);
-    }
-    __syncthreads();
-    const int64_t row0 = (it / sgroups) * kDecRows;
-    const int64_t s0 = (it % sgroups) * kDecSteps;
-    uint8_t* ob = out + (row0 / kTileRows) * steps * kBlkBytes + (row0 % kTileRows) * 64;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int ch = tid + 256 * q;          // 16-byte chunk of the tile
-      const int sj = ch >> 7;                // step within the item (128 chunks each)
-      if (s0 + sj < steps)
-        *reinterpret_cast<uint4*>(ob + (s0 + sj) * kBlkBytes + (ch & 127) * 16) = tile[ch];
-    }
-    __syncthreads();
-    cur = nxt;
-  }
-}
 
 // ---------------------------------------------------------------------------
 // Pass 2: the fp16 GEMM on blocked operands.
@@ -295,7 +213,6 @@ __global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restr
   }
 }
 
-int64_t padded_rows(int64_t rows) { return (rows + kTileRows - 1) / kTileRows * kTileRows; }
 
 }  // namespace
 
@@ -308,19 +225,6 @@ int64_t gemm_two_pass_workspace(int64_t m, int64_t n, int64_t k) {
   if (!gemm_two_pass_applies(m, n, k)) return 0;
   return (padded_rows(m) + padded_rows(n)) * k * 2;
 }
-
-hipError_t launch_decode_blocked(const uint8_t* codes, const uint8_t* scales, int64_t rows,
-                                 int64_t k, uint8_t* out, hipStream_t stream) {
-  static ResidentCache cache{};
-  const int64_t items = ((rows + kDecRows - 1) / kDecRows) * ((k / kStepK + kDecSteps - 1) / kDecSteps);
-  int64_t grid = resident_groups(decode_blocked_kernel, cache, 8, 256);
-  if (grid > items) grid = items;
-  if (grid < 1) grid = 1;
-  decode_blocked_kernel<<<(unsigned)grid, 256, 0, stream>>>(codes, scales, rows, k, out);
-  return hipGetLastError();
-}
-
-int64_t decoded_bytes(int64_t rows, int64_t k) { return padded_rows(rows) * k * 2; }
 
 hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uint8_t* wblk,
                                const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
