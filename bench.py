@@ -70,7 +70,7 @@ def gemm_traffic_bytes():
     t = GEMM_TRAFFIC
     if t is None:
         return None
-    with open(os.path.join(ROOT, "paper_2605_31035_amd", "csrc", "gemm.hip"), "rb") as f:
+    with open(os.path.join(ROOT, "paper_2605_31035_amd", "csrc", "gemm_f16.hip"), "rb") as f:
         sha = hashlib.sha256(f.read()).hexdigest()[:16]
     if sha != t["gemm_src_sha256_16"]:
         return None

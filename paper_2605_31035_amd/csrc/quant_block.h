@@ -146,17 +146,22 @@ __device__ __forceinline__ void encode_i_pair(const float (&xs)[16], const Scale
   po[J >> 3] = __builtin_amdgcn_cvt_pk_u8_f32(q1, (J & 7) >> 1, po[J >> 3]);
 }
 
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
 // E2M1 error sums of elements J, J+1 from the decoded codes, in two chains:
 //   af += x * q_F (same signs, so every term is >= 0),  bf += q_F^2.
+// The pair is decoded to two fp16 values (exact: E2M1 magnitudes have at
+// most two significant bits); x * q_F + af is one fp32 fma with the fp16
+// operand widened exactly (v_fma_mix), and q_F^2 summed by one dot2: its
+// terms are multiples of 1/4 below 2^6, so the sum is exact in fp32.
 template <int J>
 __device__ __forceinline__ void error_pair(const float (&xs)[16], const uint32_t (&pf)[2],
                                            float (&af)[2], float (&bf)[2]) {
-  const f32x2 qf = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(pf[J >> 3], 1.0f, (J & 7) >> 1);
+  const f16x2 qf = __builtin_amdgcn_cvt_scalef32_pk_f16_fp4(pf[J >> 3], 1.0f, (J & 7) >> 1);
   constexpr int c = (J >> 1) & 1;
-  af[c] = __builtin_fmaf(xs[J], qf.x, af[c]);
-  af[c] = __builtin_fmaf(xs[J + 1], qf.y, af[c]);
-  bf[c] = __builtin_fmaf(qf.x, qf.x, bf[c]);
-  bf[c] = __builtin_fmaf(qf.y, qf.y, bf[c]);
+  af[c] = __builtin_fmaf(xs[J], (float)qf.x, af[c]);
+  af[c] = __builtin_fmaf(xs[J + 1], (float)qf.y, af[c]);
+  bf[c] = __builtin_amdgcn_fdot2(qf, qf, bf[c], false);
 }
 
 // Exact contribution of elements J, J+1 to Err_E2M1 - Err_E1M2 in fp64:
@@ -176,6 +181,48 @@ __device__ __forceinline__ void exact_pair(const float (&xs)[16], const uint32_t
     const double di = (double)((float)ci * si);
     d += (di - df) * ((2.0 * ax - df) - di);
   }
+}
+
+// Nibbles of v (eight 4-bit codes) with a nonzero 3-bit magnitude, as one
+// bit per nibble (bit 4k for nibble k).
+__device__ __forceinline__ uint32_t nonzero_nibbles(uint32_t v) {
+  return (v | (v >> 1) | (v >> 2)) & 0x11111111u;
+}
+
+// The 3-bit magnitude of the only nonzero code among two words (the others
+// are zero).
+__device__ __forceinline__ uint32_t only_code(uint32_t w0, uint32_t w1) {
+  uint32_t w = (w0 | w1) & 0x77777777u;
+  w |= w >> 16;
+  w |= w >> 8;
+  w |= w >> 4;
+  return w & 7u;
+}
+
+// Err_A - Err_B of a block in which at most one element has a nonzero code
+// under either candidate A (E2M1 codes pa) or B (E1M2 codes pb, or E2M1
+// codes when kFF): every other element quantizes to 0 in both and adds
+// (|x| - 0)^2 to both errors, and the nonzero one is the block maximum
+// (|x| = bm: the element at bm always gets a nonzero code under a nonzero
+// scale).  The single term (D_B - D_A)(2 bm - D_A - D_B) is exact in fp64
+// (D_A, D_B have at most 7 significant bits).  In blocks dominated by one
+// element this is the common way for both candidates to tie, and it costs
+// a few instructions instead of the 16-element fp64 sum.
+template <bool kFF>
+__device__ __forceinline__ double single_element_delta(const uint32_t (&pa)[2],
+                                                       const uint32_t (&pb)[2], float sa,
+                                                       float sb, float bm) {
+  const uint32_t ca = only_code(pa[0], pa[1]), cb = only_code(pb[0], pb[1]);
+  const double da = (double)(e2m1_value(ca) * sa);
+  const double db = (double)((kFF ? e2m1_value(cb) : (float)cb) * sb);
+  return (db - da) * ((2.0 * (double)bm - da) - db);
+}
+
+// Number of elements of a block with a nonzero code under A or B.
+__device__ __forceinline__ uint32_t nonzero_elements(const uint32_t (&pa)[2],
+                                                     const uint32_t (&pb)[2]) {
+  return __builtin_popcount(nonzero_nibbles(pa[0] & 0x77777777u) | nonzero_nibbles(pb[0] & 0x77777777u)) +
+         __builtin_popcount(nonzero_nibbles(pa[1] & 0x77777777u) | nonzero_nibbles(pb[1] & 0x77777777u));
 }
 
 // Format modes: MixFP4 selection (Algorithm 1), or one branch for every
@@ -261,7 +308,7 @@ __device__ __forceinline__ uint2 sr_codes(const float (&xs)[16], const ScaleReci
 // selection (bounded fp32 estimate, exact fp64 sum inside the bound); /4 is
 // kept only where its error is strictly smaller.  T = 0.
 template <bool kSR, bool kTile>
-__device__ __forceinline__ void quantize_four_six(const float (&xs)[16], float bm,
+__device__ __forceinline__ void quantize_four_six(const float (&xs)[16], float bm, float bm_lane,
                                                   const ScaleRecip* __restrict__ tab, uint2& out,
                                                   uint32_t& scale_byte, uint4 rnd) {
   const ScaleRecip d6 = scale_recip(6.0f);
@@ -297,8 +344,17 @@ __device__ __forceinline__ void quantize_four_six(const float (&xs)[16], float b
   const float tau = kTile ? 0x1p-18f * (t6 + t4) + 0x1p-21f * (s62b + s42b)
                           : 0x1p-19f * (t6 + t4) + 0x1p-22f * (s62b + s42b);
   bool use4;
+  uint32_t nz = 0;
+  if (!(c6 != 0u && c4 != 0u && fabsf(est) > tau)) {
+    nz = nonzero_elements(p6, p4);
+    if constexpr (kTile) nz = row16_sum(nz);
+  }
   if (c6 != 0u && c4 != 0u && fabsf(est) > tau) {
     use4 = est > 0.0f;
+  } else if (nz <= 1u) {
+    double d = single_element_delta<true>(p6, p4, s6, s4, bm_lane);
+    if constexpr (kTile) d = row16_sum(d);
+    use4 = d > 0.0;
   } else {
     double d = 0.0;
     exact_pair_ff<0>(xs, p6, p4, s6, s4, d);
@@ -335,9 +391,10 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const ScaleRe
   float bm = 0.0f;
 #pragma unroll
   for (int j = 0; j < 16; ++j) bm = fmaxf(bm, fabsf(xs[j]));
+  const float bm_lane = bm;          // this lane's 16 elements (a tile row)
   if constexpr (kTile) bm = row16_max(bm);
   if constexpr (kMode == kFourSix) {
-    quantize_four_six<kSR, kTile>(xs, bm, tab, out, scale_byte, rnd);
+    quantize_four_six<kSR, kTile>(xs, bm, bm_lane, tab, out, scale_byte, rnd);
     return;
   }
   // Candidate block scales E4M3(bm/6), E4M3(bm/7): the exactly rounded
@@ -436,8 +493,17 @@ __device__ __forceinline__ void quantize_xs(const float (&xs)[16], const ScaleRe
   const float tau = kTile ? 0x1p-18f * (tf + ti) + 0x1p-21f * (sf2b + si2b)
                           : 0x1p-19f * (tf + ti) + 0x1p-22f * (sf2b + si2b);
   bool t1;
+  uint32_t nz = 0;
+  if (!(cf != 0u && ci != 0u && fabsf(est) > tau)) {
+    nz = nonzero_elements(pf, pi);
+    if constexpr (kTile) nz = row16_sum(nz);
+  }
   if (cf != 0u && ci != 0u && fabsf(est) > tau) {
     t1 = !(est < 0.0f);
+  } else if (nz <= 1u) {
+    double d = single_element_delta<false>(pf, pi, sf, si, bm_lane);
+    if constexpr (kTile) d = row16_sum(d);     // one nonzero term in the tile: exact
+    t1 = !(d < 0.0);
   } else {
     double d = 0.0;
     exact_pair<0>(xs, pf, pi, sf, si, d);

@@ -37,6 +37,8 @@
 #include "philox.h"
 #include "quant_block.h"
 
+typedef int mixfp4_i32x4q __attribute__((ext_vector_type(4)));
+
 namespace mixfp4 {
 namespace {
 
@@ -111,17 +113,32 @@ struct XDomain {
   float xmul, sx, rx, rh, rl;
 };
 
-// Grid-stride walk over the blocks.  The next block of this thread is
+// How x = fl32(X / s32) is computed: the two-term reciprocal of s32
+// (kTwoTerm), Markstein's step on X (kMarkstein), or Markstein's step on
+// X * xmul for tensor scales outside [2^-90, 2^120] (kScaledX).
+constexpr int kTwoTerm = 0, kMarkstein = 1, kScaledX = 2;
+
+template <int kDiv>
+__device__ __forceinline__ void to_x(uint4 r0, uint4 r1, const XDomain& xd, float (&xs)[16]) {
+  if constexpr (kDiv == kTwoTerm)
+    to_fp8_domain_two_term(r0, r1, xd.rh, xd.rl, xs);
+  else
+    to_fp8_domain<kDiv == kScaledX>(r0, r1, xd.xmul, xd.sx, xd.rx, xs);
+}
+
+// Grid-stride walk over the blocks of X in registers (row-strided X, and
+// the rotating quantizer, whose fp64 butterflies need the registers more
+// than the stream loop's bytes in flight help it: measured 400 against 446
+// us for 128-blocks on the 2^28 tensor).  The next block of this thread is
 // loaded as soon as the current one has been turned into x, so its load
-// overlaps this block's arithmetic (measured: two or three blocks in flight
-// per thread, at the lower occupancy their registers allow, are no faster).
+// overlaps this block's arithmetic.
 //
 // kSR: stochastic rounding with Philox draws per block (its global index).
 // kHad: each block is first rotated (block-diagonal Hadamard across the
 // L = b / 16 lanes holding one Hadamard block; the grid stride is a multiple
 // of 256, so a thread keeps its position in its Hadamard block and every
 // Hadamard block is processed by lanes of one wave in one iteration).
-template <bool kContig, bool kTwoTerm, int kMode, bool kSR, bool kHad>
+template <int kDiv, bool kContig, int kMode, bool kSR, bool kHad>
 __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, int64_t nbk,
                                               int64_t ldx, int64_t nblocks,
                                               uint8_t* __restrict__ codes,
@@ -135,7 +152,7 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
   auto load = [&](int64_t gi, uint4& p, uint4& q) {
     gi = gi < nblocks ? gi : nblocks - 1;
     const uint16_t* src;
-    if (kContig) {
+    if constexpr (kContig) {
       src = x + (gi << 4);
     } else {
       const int64_t r = gi / nbk;
@@ -153,10 +170,7 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
     float xs[16];
     uint4 r0 = a0, r1 = a1;
     if constexpr (kHad) hadamard_rotate(r0, r1, sm, hp);
-    if constexpr (kTwoTerm)
-      to_fp8_domain_two_term(r0, r1, xd.rh, xd.rl, xs);
-    else
-      to_fp8_domain<true>(r0, r1, xd.xmul, xd.sx, xd.rx, xs);
+    to_x<kDiv>(r0, r1, xd, xs);
     load(g + stride, a0, a1);
     uint2 out;
     uint32_t sb;
@@ -166,14 +180,119 @@ __device__ __forceinline__ void quantize_loop(const uint16_t* __restrict__ x, in
   }
 }
 
-// Quantize blocks [this thread's grid-stride share] with tensor scale s32.
-// The division steps stay in the normal range for every element that can get
-// a nonzero code when 2^-90 <= s32 <= 2^120; beyond that both X and s32 are
-// rescaled by 2^64 or 2^-64 first.  Within that range, the two-term division
-// is used when it reproduces the exact quotient on all 128 bf16 mantissas
-// (checked by the first 128 threads of every workgroup, so every workgroup
-// takes the same, deterministic decision); the kernel's barrier publishes
-// the check and the scale table together.
+// Contiguous X: each wave streams windows of 64 blocks (2 KB of X) through a
+// ring of two 2 KB LDS slots with 16-byte buffer loads that write straight
+// into LDS, one window ahead; lane l then reads block l of the window (32 B)
+// from LDS.  Every load instruction covers 1 KB of contiguous memory and
+// carries the non-temporal hint (X is read once), and the bytes in flight
+// hold no registers.  Measured on MI355X with this traffic (2 B read, 0.5625
+// B written per element) and no arithmetic: 6.36 TB/s, against 5.45 TB/s for
+// two 16-byte loads per lane straight into registers, which is what the
+// quantizer did before.  Windows are dealt round-robin over the waves of the
+// grid; every wave runs the same number of iterations, and windows past the
+// end read zeros and store nothing (buffer range checks), so the loop has no
+// divergent exit.  Codes and scales leave through buffer stores on the same
+// window bases.
+constexpr int kWindow = 64;          // blocks per wave per iteration
+constexpr int kWindowBytes = kWindow * 32;
+constexpr int kRingAux = 2;          // non-temporal loads
+
+typedef mixfp4_i32x4q i32x4q;
+__device__ __forceinline__ i32x4q raw_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  i32x4q r;
+  r[0] = (int)(uint32_t)b;
+  r[1] = (int)(uint32_t)(b >> 32);
+  r[2] = (int)bytes;
+  r[3] = 0x00020000;
+  return r;
+}
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t store_rsrc(void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(base, 0, (int)bytes, 0x00020000);
+}
+
+}  // namespace
+}  // namespace mixfp4
+
+// The 16-byte buffer load that writes straight into LDS (destination M0 +
+// offset + 16 * lane).
+__device__ void mixfp4_q_buffer_load_lds(mixfp4_i32x4q rsrc,
+                                         __attribute__((address_space(3))) uint32_t* lds,
+                                         int size, int voffset, int soffset, int offset,
+                                         int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+
+namespace mixfp4 {
+namespace {
+
+template <int kDiv, int kMode, bool kSR, bool kHad>
+__device__ __forceinline__ void stream_loop(const uint16_t* __restrict__ x, int64_t nblocks,
+                                            uint8_t* __restrict__ codes,
+                                            uint8_t* __restrict__ scales, const XDomain& xd,
+                                            const ScaleRecip* tab, const SrParams& sr,
+                                            const HadamardParams& hp, uint8_t* ring) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int64_t windows = (nblocks + kWindow - 1) / kWindow;
+  const int64_t waves = (int64_t)gridDim.x * (kThreads / 64);
+  const int64_t iters = (windows + waves - 1) / waves;
+  uint8_t* slots = ring + wave * 2 * kWindowBytes;
+  auto first_block = [&](int64_t i) {
+    return ((i * gridDim.x + blockIdx.x) * (kThreads / 64) + wave) * kWindow;
+  };
+  auto blocks_in = [&](int64_t base) {
+    const int64_t rem = nblocks - base;
+    return rem < 0 ? 0 : (rem < kWindow ? rem : kWindow);
+  };
+  auto issue = [&](int64_t i) {
+    const int64_t base = first_block(i);
+    const i32x4q r = raw_rsrc(x + base * 16, (uint32_t)(blocks_in(base) * 32));
+    __attribute__((address_space(3))) uint32_t* l =
+        (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(
+            reinterpret_cast<uintptr_t>(slots + (i & 1) * kWindowBytes));
+    mixfp4_q_buffer_load_lds(r, l, 16, lane * 16, 0, 0, kRingAux);
+    mixfp4_q_buffer_load_lds(r, l, 16, lane * 16, 0, 1024, kRingAux);
+  };
+  SignMasks sm;
+  if constexpr (kHad) sm = load_sign_masks(hp, lane & ((1 << hp.lanes_log2) - 1));
+  issue(0);
+  for (int64_t i = 0; i < iters; ++i) {
+    // Vector memory operations complete in issue order, and vmcnt counts
+    // stores as well as loads: after window i's two loads this wave issued
+    // only the previous window's two stores, which may stay in flight.
+    if (i == 0)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+    const uint4* src = reinterpret_cast<const uint4*>(slots + (i & 1) * kWindowBytes + lane * 32);
+    uint4 r0 = src[0], r1 = src[1];
+    // The other slot held window i - 1, whose reads finished last iteration.
+    issue(i + 1);
+    const int64_t base = first_block(i);
+    if constexpr (kHad) hadamard_rotate(r0, r1, sm, hp);
+    float xs[16];
+    to_x<kDiv>(r0, r1, xd, xs);
+    uint2 out;
+    uint32_t sb;
+    quantize_xs<kMode, kSR>(xs, tab, out, sb,
+                            kSR ? block_draws(base + lane, sr) : make_uint4(0, 0, 0, 0));
+    const int64_t n = blocks_in(base);
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    __builtin_amdgcn_raw_buffer_store_b64(u32x2{out.x, out.y},
+                                          store_rsrc(codes + base * 8, (uint32_t)(n * 8)), lane * 8,
+                                          0, 0);
+    __builtin_amdgcn_raw_buffer_store_b8((uint8_t)sb, store_rsrc(scales + base, (uint32_t)n),
+                                         lane, 0, 0);
+  }
+}
+
+// Quantize the blocks of X with tensor scale s32.  The division steps stay
+// in the normal range for every element that can get a nonzero code when
+// 2^-90 <= s32 <= 2^120; beyond that both X and s32 are rescaled by 2^64 or
+// 2^-64 first.  Within that range, the two-term division is used when it
+// reproduces the exact quotient on all 128 bf16 mantissas (checked by the
+// first 128 threads of every workgroup, so every workgroup takes the same,
+// deterministic decision); the kernel's barrier publishes the check and the
+// scale table together.
 template <bool kContig, int kMode, bool kSR, bool kHad>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const uint16_t* __restrict__ x, int64_t nbk, int64_t ldx, int64_t nblocks,
@@ -197,12 +316,25 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     ok = __float_as_uint(div_rn(xt, xd.sx, xd.rx)) == __float_as_uint(div_scale(xt, xd.rh, xd.rl));
   }
   const bool two_term = __syncthreads_and(ok) && direct;
-  if (two_term)
-    quantize_loop<kContig, true, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xd, tab,
-                                                   sr, hp);
-  else
-    quantize_loop<kContig, false, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xd, tab,
-                                                    sr, hp);
+  if constexpr (kContig && !kHad) {
+    __shared__ __attribute__((aligned(1024))) uint8_t ring[(kThreads / 64) * 2 * kWindowBytes];
+    if (two_term)
+      stream_loop<kTwoTerm, kMode, kSR, kHad>(x, nblocks, codes, scales, xd, tab, sr, hp, ring);
+    else if (direct)
+      stream_loop<kMarkstein, kMode, kSR, kHad>(x, nblocks, codes, scales, xd, tab, sr, hp, ring);
+    else
+      stream_loop<kScaledX, kMode, kSR, kHad>(x, nblocks, codes, scales, xd, tab, sr, hp, ring);
+  } else {
+    if (two_term)
+      quantize_loop<kTwoTerm, kContig, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xd, tab, sr,
+                                                hp);
+    else if (direct)
+      quantize_loop<kMarkstein, kContig, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xd, tab,
+                                                  sr, hp);
+    else
+      quantize_loop<kScaledX, kContig, kMode, kSR, kHad>(x, nbk, ldx, nblocks, codes, scales, xd, tab, sr,
+                                                hp);
+  }
 }
 
 // Small tensors with the tensor scale computed (at most kSmallElems
@@ -449,16 +581,30 @@ hipError_t launch_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, 
                        hipStream_t stream) {
   const int64_t nbk = k / kBlock;
   const int64_t nblocks = rows * nbk;
-  // A tensor that one round of resident workgroups covers gets one block per
-  // thread.  Larger ones are walked by a persistent grid, one wave of
-  // resident workgroups, so no partial second wave is left at the end, with
-  // at most kMaxPerCU workgroups per CU.  The single-format encodings do
-  // little arithmetic per byte and stream HBM better with fewer resident
-  // waves than their registers allow (measured on the 2^28 tensor: E2M1-only
-  // at 3 workgroups per CU takes 118 us against 137 us at 8; E1M2-only is
-  // best at 4).  For the other modes 4 to 8 measure the same; they take 6.
-  constexpr int kMaxPerCU = kMode == kForceE2M1 ? 3 : (kMode == kForceE1M2 ? 4 : 6);
   static ResidentCache cache_c, cache_s, capped_c, capped_s;
+  if (ldx == k && !kHad) {
+    // Contiguous X (stream_loop): one window of 64 blocks per wave, four
+    // per workgroup; a tensor with more windows is walked by a persistent
+    // grid of at most 3 workgroups per CU (measured on the 2^28 tensor: 3,
+    // 4 and 6 per CU within 3% for every mode, 3 the fastest or tied).
+    constexpr int kStreamPerCU = 3;
+    const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
+    const int64_t capped =
+        resident_groups(quantize_kernel<true, kMode, kSR, kHad>, capped_c, kStreamPerCU);
+    const int g = (int)(wanted <= capped ? wanted : capped);
+    quantize_kernel<true, kMode, kSR, kHad><<<g, kThreads, 0, stream>>>(
+        x, nbk, ldx, nblocks, codes, scales, tensor_scale, opt.srp, opt.hp);
+    return hipGetLastError();
+  }
+  // Row-strided X: a tensor that one round of resident workgroups covers
+  // gets one block per thread.  Larger ones are walked by a persistent grid,
+  // one wave of resident workgroups, so no partial second wave is left at
+  // the end, with at most kMaxPerCU workgroups per CU.  The single-format
+  // encodings do little arithmetic per byte and stream HBM better with fewer
+  // resident waves than their registers allow (E2M1-only at 3 workgroups per
+  // CU against 8: 118 us against 137 us on a contiguous 2^28 tensor;
+  // E1M2-only is best at 4).  For the other modes 4 to 8 measure the same.
+  constexpr int kMaxPerCU = kMode == kForceE2M1 ? 3 : (kMode == kForceE1M2 ? 4 : 6);
   const int64_t wanted = (nblocks + kThreads - 1) / kThreads;
   const bool contig = ldx == k;
   const int64_t resident =
@@ -468,7 +614,7 @@ hipError_t launch_mode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, 
       contig ? resident_groups(quantize_kernel<true, kMode, kSR, kHad>, capped_c, kMaxPerCU)
              : resident_groups(quantize_kernel<false, kMode, kSR, kHad>, capped_s, kMaxPerCU);
   const int g = (int)(wanted <= resident ? wanted : capped);
-  if (ldx == k)
+  if (contig)
     quantize_kernel<true, kMode, kSR, kHad><<<g, kThreads, 0, stream>>>(
         x, nbk, ldx, nblocks, codes, scales, tensor_scale, opt.srp, opt.hp);
   else
