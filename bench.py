@@ -62,7 +62,11 @@ AMAX_BYTES_PER_ELEM = 2                   # the tensor-scale pass re-reads X
 # copy (--calibrate-copy).  Valid only for the GEMM source it was measured on
 # (first 16 hex digits of its SHA-256); reported as null otherwise, and null
 # until it has been measured.
-GEMM_TRAFFIC = None
+GEMM_TRAFFIC = {
+    "gemm_src_sha256_16": "c8c37f193c291581",    # csrc/gemm_f16.hip as measured
+    "fetch_kib": 1577510, "write_kib": 605797,  # KiB per dispatch, gemm_f16_kernel
+    "fetch_scale": 2.0, "write_scale": 1.0,     # 512 MiB copy: 262168 KiB fetched, 524288 written
+}
 
 
 def gemm_traffic_bytes():
@@ -408,20 +412,22 @@ def gemm_decoded_bytes(m: int, n: int, k: int) -> float:
 
 def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -> dict:
     """One prefill step of a workload: quantize A (tensor scale computed on the
-    device), decode A once into exact 16-bit values, and for every weight of
-    the workload decode it and run the GEMM on the decoded operands (the two
-    passes of mixfp4_gemm_ws, called separately so that A, shared by the
-    workload's GEMMs, is decoded once and every kernel has its own span).  The
-    weights are quantized before timing; their decode is inside the step.  The
-    step time comes from `steps` steps with nothing else on the stream, timed
-    wall-clock between device synchronizations, after `warmup` untimed steps
-    and `spin_s` seconds of untimed steps that bring the clocks to their
-    loaded level.  The per-launch spans come from a second pass of the same
-    steps with HIP events recorded on the launching stream around each launch
-    (an event adds ~3.5 us of GPU time between launches, so the step time is
-    taken without them).  The fused single-kernel GEMM (mixfp4_gemm, which
-    decodes inside its MFMA loop) is timed on the same operands for
-    comparison."""
+    device), then every GEMM of the workload on the path the library's rule
+    picks for its shape (gemm_two_pass_preferred): two passes (A decoded once
+    into exact 16-bit values for all of the step's two-pass GEMMs, the weight
+    decoded, then the GEMM on the decoded operands; the passes of
+    mixfp4_gemm_ws, called separately so that A is decoded once and every
+    kernel has its own span) or the fused kernel (mixfp4_gemm, which decodes
+    inside its MFMA loop).  The weights are quantized before timing; their
+    decode is inside the step.  The step time comes from `steps` steps with
+    nothing else on the stream, timed wall-clock between device
+    synchronizations, after `warmup` untimed steps and `spin_s` seconds of
+    untimed steps that bring the clocks to their loaded level.  The
+    per-launch spans come from a second pass of the same steps with HIP
+    events recorded on the launching stream around each launch (an event
+    adds ~3.5 us of GPU time between launches, so the step time is taken
+    without them).  Both paths are also timed back to back on the same
+    operands for every GEMM, whichever the step uses."""
     x = {n: torch.from_numpy(b.view(np.int16)).to(dev).view(torch.bfloat16)
          for n, b in wl.tensors.items()}
     wnames = [w for _, w in wl.gemms]
@@ -434,6 +440,7 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
           torch.empty(1, dtype=torch.float32, device=dev))
     outs = {w: torch.empty((ra, qw[w][0].shape[0]), dtype=torch.float32, device=dev)
             for w in wnames}
+    two = {w: M.gemm_two_pass_preferred(ra, qw[w][0].shape[0], ka) for w in wnames}
     # decoded-operand buffers, allocated once (the step writes them every time)
     da = M.mixfp4_decode_operand(qa)
     dws = {w: M.mixfp4_decode_operand(qw[w]) for w in wnames}
@@ -446,14 +453,19 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
         M.mixfp4_quantize(x["A"], None, qa[0], qa[1], scale_out=qa[2])
         if e is not None:
             e[1].record()
-        M.mixfp4_decode_operand(qa, out=da.buf)
+        if any(two.values()):
+            M.mixfp4_decode_operand(qa, out=da.buf)
         for i, w in enumerate(wnames):
             if e is not None:
                 e[2 + 2 * i].record()
-            M.mixfp4_decode_operand(qw[w], out=dws[w].buf)
+            if two[w]:
+                M.mixfp4_decode_operand(qw[w], out=dws[w].buf)
             if e is not None:
                 e[3 + 2 * i].record()
-            M.mixfp4_gemm_decoded(da, dws[w], out=outs[w])
+            if two[w]:
+                M.mixfp4_gemm_decoded(da, dws[w], out=outs[w])
+            else:
+                M.mixfp4_gemm(qa, qw[w], out=outs[w])
         if e is not None:
             e[nspan].record()
 
@@ -475,6 +487,17 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
     da_ms = span(1, 2)
     gemms = {}
     total_flops = 0.0
+
+    def back_to_back(f) -> float:
+        spin_up(torch, f, 0.1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
     for i, w in enumerate(wnames):
         n = qw[w][0].shape[0]
         fl = 2.0 * ra * n * ka
@@ -484,43 +507,48 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
         tf = fl / (g_ms * 1e-3) / 1e12
         dec_bytes = n * ka * (0.5 + 1 / 16 + 2)
         gemms[w] = {"shape": [ra, n, ka], "flops": fl,
-                    "kernel": "gemm_f16_kernel (decoded operands)",
+                    "path": "two-pass" if two[w] else "fused",
+                    "kernel": "gemm_f16_kernel (decoded operands)" if two[w]
+                    else "gemm_kernel (decode inside the MFMA loop)",
                     "us_per_launch": round(g_ms * 1e3, 2),
                     "achieved": round(tf, 2), "unit": "TFLOP/s",
                     "frac": round(tf / PEAK_F16_TFLOPS, 4),
-                    "decode_w_us": round(dw_ms * 1e3, 2),
-                    "decode_w_GBps": round(dec_bytes / (dw_ms * 1e-3) / 1e9, 1),
                     "gemm_call_us": round((dw_ms + g_ms) * 1e3, 2),
                     "gemm_call_TFLOPs": round(fl / ((dw_ms + g_ms) * 1e-3) / 1e12, 2)}
-    # the fused kernel on the same operands: back-to-back launches
-    for w in wnames:
-        f = lambda: M.mixfp4_gemm(qa, qw[w], out=outs[w])  # noqa: E731
-        spin_up(torch, f, 0.1)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(steps):
-            f()
-        e1.record()
-        torch.cuda.synchronize()
-        f_ms = e0.elapsed_time(e1) / steps
-        fl = gemms[w]["flops"]
-        gemms[w]["fused_kernel"] = {"kernel": "gemm_kernel (decode inside the MFMA loop)",
-                                    "us_per_launch": round(f_ms * 1e3, 2),
-                                    "achieved": round(fl / (f_ms * 1e-3) / 1e12, 2),
-                                    "frac": round(fl / (f_ms * 1e-3) / 1e12 / PEAK_F16_TFLOPS, 4)}
+        if two[w]:
+            gemms[w]["decode_w_us"] = round(dw_ms * 1e3, 2)
+            gemms[w]["decode_w_GBps"] = round(dec_bytes / (dw_ms * 1e-3) / 1e9, 1)
+        # both paths back to back on the same operands (A decoded beforehand
+        # for the two-pass one, as the step does once for all its GEMMs)
+        f_ms = back_to_back(lambda: M.mixfp4_gemm(qa, qw[w], out=outs[w]))
+        M.mixfp4_decode_operand(qa, out=da.buf)
+
+        def two_pass_call():
+            M.mixfp4_decode_operand(qw[w], out=dws[w].buf)
+            M.mixfp4_gemm_decoded(da, dws[w], out=outs[w])
+        t_ms = back_to_back(two_pass_call)
+        gemms[w]["fused_call"] = {"kernel": "gemm_kernel", "us": round(f_ms * 1e3, 2),
+                                  "TFLOPs": round(fl / (f_ms * 1e-3) / 1e12, 2),
+                                  "frac": round(fl / (f_ms * 1e-3) / 1e12 / PEAK_F16_TFLOPS, 4)}
+        gemms[w]["two_pass_call"] = {"kernels": "decode_blocked_kernel (W) + gemm_f16_kernel",
+                                     "us": round(t_ms * 1e3, 2),
+                                     "TFLOPs": round(fl / (t_ms * 1e-3) / 1e12, 2)}
     out = {"ms_per_step": round(ms_step, 4), "steps": steps, "warmup": warmup,
            "spin_up_s": spin_s,
            "step_TFLOPs": round(total_flops / (ms_step * 1e-3) / 1e12, 3),
            "gemm_flops_per_step": total_flops,
+           "path_rule": "two passes where m n / (m + n) >= 2048 (gemm_two_pass_preferred), "
+                        "else the fused kernel",
            "quantize_a": {"what": f"A[{ra},{ka}] with the tensor scale computed on the device "
                                   "(amax pass + reduction + quantize kernel)",
                           "us": round(q_ms * 1e3, 2),
                           "GBps": round(ra * ka * QUANT_BYTES_PER_ELEM / (q_ms * 1e-3) / 1e9, 1),
                           "bytes_per_elem": QUANT_BYTES_PER_ELEM},
-           "decode_a": {"kernel": "decode_blocked_kernel", "us": round(da_ms * 1e3, 2),
-                        "bytes": ra * ka * (0.5 + 1 / 16 + 2),
-                        "GBps": round(ra * ka * (0.5 + 1 / 16 + 2) / (da_ms * 1e-3) / 1e9, 1)},
            "gemms": gemms}
+    if any(two.values()):
+        out["decode_a"] = {"kernel": "decode_blocked_kernel", "us": round(da_ms * 1e3, 2),
+                           "bytes": ra * ka * (0.5 + 1 / 16 + 2),
+                           "GBps": round(ra * ka * (0.5 + 1 / 16 + 2) / (da_ms * 1e-3) / 1e9, 1)}
     del x, qw, qa, outs, da, dws
     torch.cuda.empty_cache()
     return out
@@ -612,9 +640,10 @@ def main():
                               "decode_w_us": g["decode_w_us"], "decode_w_GBps": g["decode_w_GBps"],
                               "bound": "hbm", "bytes_per_elem": 0.5 + 1 / 16 + 2}
         out["gemm_call"] = {"what": "decode W + GEMM (the mixfp4_gemm_ws work for an operand "
-                                    "decoded once), and the fused single-kernel GEMM",
-                            "us": g["gemm_call_us"], "TFLOPs": g["gemm_call_TFLOPs"],
-                            "fused_kernel": g["fused_kernel"]}
+                                    "decoded once) in the step, and both paths back to back",
+                            "path": g["path"], "us": g["gemm_call_us"],
+                            "TFLOPs": g["gemm_call_TFLOPs"],
+                            "two_pass_call": g["two_pass_call"], "fused_call": g["fused_call"]}
     if "quantize" in only:
         out["quantize"] = measure_quantize(M, torch, dev)
     if "prefill_7b" in only:

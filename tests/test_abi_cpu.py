@@ -272,3 +272,17 @@ def test_decode_operand_and_decoded_gemm_reject(lib):
     assert g(P(0x10000), None, P(0x10040), None, 64, 64, 64, A16, None) == 3
     assert g(P(0x10000), None, None, None, 64, 64, 64, A16, None) == 1
     assert g(P(0x10000), None, P(0x10000), None, 0, 64, 64, None, None) == 0
+
+
+def test_two_pass_rule():
+    """The binding's path rule (host logic only): two passes for the large and
+    rotated GEMM shapes, the fused kernel for the 2048-row prefill shapes, and
+    never where the two-pass path does not apply."""
+    import paper_2605_31035_amd as M
+    assert M.gemm_two_pass_preferred(16384, 8192, 8192)
+    assert M.gemm_two_pass_preferred(4096, 14336, 4096)
+    assert M.gemm_two_pass_preferred(4096, 4096, 4096)          # m n / (m + n) = 2048 exactly
+    assert not M.gemm_two_pass_preferred(2048, 11008, 4096)
+    assert not M.gemm_two_pass_preferred(2048, 4096, 4096)
+    assert not M.gemm_two_pass_preferred(16, 1 << 20, 4096)     # decode shape: fused
+    assert not M.gemm_two_pass_preferred(16384, 16384, 48)      # k % 32 != 0
