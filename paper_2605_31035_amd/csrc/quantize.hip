@@ -83,6 +83,56 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(const uint16_t* __restri
   }
 }
 
+// The same maximum over a contiguous X: each wave reads windows of 4 KB
+// (256 16-byte vectors), four loads per lane that each cover 1 KB of
+// contiguous memory, with the non-temporal hint (X is read once here), the
+// next window's loads in flight while this one is reduced.  Windows past the
+// end read zeros (buffer range check), which leave the maximum unchanged.
+constexpr int kAmaxWindow = 256;      // vectors of 8 bf16 per wave per iteration
+
+__global__ __launch_bounds__(kThreads) void amax_stream_kernel(const uint16_t* __restrict__ x,
+                                                                int64_t nvec,
+                                                                uint32_t* __restrict__ partials,
+                                                                uint32_t* __restrict__ out) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const int lane = (int)(threadIdx.x & 63);
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int64_t windows = (nvec + kAmaxWindow - 1) / kAmaxWindow;
+  const int64_t waves = (int64_t)gridDim.x * (kThreads / 64);
+  const int64_t iters = (windows + waves - 1) / waves;
+  auto load = [&](int64_t i, u32x4 (&v)[4]) {
+    const int64_t base = ((i * gridDim.x + blockIdx.x) * (kThreads / 64) + wave) * kAmaxWindow;
+    int64_t rem = nvec - base;
+    rem = rem < 0 ? 0 : (rem < kAmaxWindow ? rem : kAmaxWindow);
+    const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<uint16_t*>(x + base * 8), 0, (int)(rem * 16), 0x00020000);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(r, lane * 16 + j * 1024, 0, 2);
+  };
+  u32x4 cur[4], nxt[4];
+  load(0, cur);
+  uint32_t m = 0u;
+  for (int64_t i = 0; i < iters; ++i) {
+    load(i + 1, nxt);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      m = max(m, absmax8(make_uint4(cur[j].x, cur[j].y, cur[j].z, cur[j].w)));
+      cur[j] = nxt[j];
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off));
+  __shared__ uint32_t wave_max[kThreads / 64];
+  if (lane == 0) wave_max[wave] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t r = wave_max[0];
+    for (int w = 1; w < kThreads / 64; ++w) r = max(r, wave_max[w]);
+    if (partials) partials[blockIdx.x] = r;
+    else if (r) atomicMax(out, r << 16);            // bf16 bits -> fp32 bits
+  }
+}
+
 // One workgroup: fold the per-workgroup maxima and write s32.
 __global__ __launch_bounds__(kThreads) void reduce_scale(const uint32_t* __restrict__ partials,
                                                           int count, float* __restrict__ out) {
@@ -526,6 +576,19 @@ hipError_t launch_tensor_scale(const uint16_t* x, int64_t rows, int64_t k, int64
                                uint8_t* scratch, int64_t scratch_bytes, float* tensor_scale,
                                hipStream_t stream) {
   const int64_t total = rows * (k >> 3);
+  if (ldx == k) {
+    // one window of 4 KB per wave, four waves per workgroup, at most 4
+    // workgroups per CU (a persistent grid for large tensors)
+    static ResidentCache cache;
+    const int64_t wanted = (total + 4 * kAmaxWindow - 1) / (4 * kAmaxWindow);
+    const int64_t resident = resident_groups(amax_stream_kernel, cache, 4);
+    const int g = (int)(wanted < resident ? (wanted > 0 ? wanted : 1) : resident);
+    return tensor_scale_with(total, g, scratch, scratch_bytes, tensor_scale, stream,
+                             [&](int grid, uint32_t* partials, uint32_t* out) {
+                               amax_stream_kernel<<<grid, kThreads, 0, stream>>>(x, total,
+                                                                                  partials, out);
+                             });
+  }
   // up to 1024 workgroups x 256 threads x 4 loads of 16 B keeps ~16 MB in flight
   int g = grid_for(total, 4);
   if (g > 1024) g = 1024;
