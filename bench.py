@@ -309,8 +309,24 @@ def measure_decode(M, torch, dev, iters: int = 50) -> dict:
     b1.record()
     torch.cuda.synchronize()
     st_ms = b0.elapsed_time(b1) / iters
+    # the same step as one launch (mixfp4_decode_step: A quantized by the
+    # first workgroups and handed to the GEMM inside the launch), steps back
+    # to back on the same buffers
+    sync = torch.zeros(4, dtype=torch.int32, device=dev)
+
+    def fused_step():
+        M.mixfp4_decode_step(xa, qw, out=out, a_out=qa, sync=sync)
+
+    spin_up(torch, fused_step)
+    b0.record()
+    for _ in range(iters):
+        fused_step()
+    b1.record()
+    torch.cuda.synchronize()
+    fs_ms = b0.elapsed_time(b1) / iters
     n = qw[0].shape[0]
     gemm_bytes = n * k / 2 + n * k / 16 + r * k / 2 + r * k / 16 + r * n * 4
+    step_bytes = gemm_bytes + r * k * 2          # plus reading A in bf16
     return {
         "workload": "decode: A[16,8192] N(0,1) with 4 outlier channels x30 quantized online; "
                     "W[28672,8192] N(0,0.02) with 0.5% outliers, quantized before timing",
@@ -321,9 +337,15 @@ def measure_decode(M, torch, dev, iters: int = 50) -> dict:
         "gemm_TFLOPs": round(2.0 * r * n * k / (g_ms * 1e-3) / 1e12, 2),
         "gemm_in_step_us": round(step_g_ms * 1e3, 2),
         "step_us": round(st_ms * 1e3, 2),
+        "fused_step_us": round(fs_ms * 1e3, 2),
+        "fused_step_GBps": round(step_bytes / (fs_ms * 1e-3) / 1e9, 1),
+        "fused_step_hbm_frac": round(step_bytes / (fs_ms * 1e-3) / 1e9 / PEAK_HBM_GBPS, 4),
+        "fused_step": "mixfp4_decode_step: tensor scale, quantization of A and the GEMM in one "
+                      "launch (A's codes, scales and s32 written as outputs)",
         "timing": "gemm_us: back-to-back GEMM launches; step_us: back-to-back steps of quantize "
-                  "A then GEMM (dispatch gaps included); quantize_a_us and gemm_in_step_us: HIP "
-                  "event spans around each launch of a separate pass of steps",
+                  "A then GEMM (dispatch gaps included); fused_step_us: back-to-back one-launch "
+                  "steps; quantize_a_us and gemm_in_step_us: HIP event spans around each launch "
+                  "of a separate pass of steps",
     }
 
 

@@ -318,13 +318,45 @@ int mixfp4_gemm_decoded(const void *a_decoded, const float *a_tensor_scale,
 /* Human-readable name of a mixfp4_status value (static storage). */
 const char *mixfp4_status_string(int status);
 
+/*
+ * mixfp4_decode_step - one decode step in one kernel launch: the tensor
+ * scale and MixFP4 quantization of the activation A (Algorithm 1, the
+ * compute mode of mixfp4_quantize) and C = A W^T with W already in MixFP4
+ * (App. B.1; the activation quantized on the fly before the block-scaled
+ * GEMM, Sec. 3.2 and Fig. 7).  A's codes, scales and tensor scale are
+ * written as outputs and equal mixfp4_quantize's bit for bit; C equals
+ * mixfp4_gemm on them bit for bit.
+ *   a          A, bf16 bit patterns, row-major [m, k] with row pitch k,
+ *              16-byte aligned (device).
+ *   m, k       1 <= m <= 16, k > 0, k % 512 == 0 (else MIXFP4_ERR_SHAPE).
+ *   w_codes, w_scales, w_tensor_scale, n
+ *              W [n, k] as for mixfp4_gemm (w_scales 4-byte aligned;
+ *              w_tensor_scale NULL means 1.0); n >= 1.
+ *   a_codes    out: A's codes [m, k/2], 16-byte aligned (device).
+ *   a_scales   out: A's scale bytes [m, k/16], 4-byte aligned (device).
+ *   a_tensor_scale  out: A's s32, one fp32 (device).
+ *   c          out: C [m, n] fp32 row-major (device).
+ *   sync       four uint32 on the device, zero before the first call; the
+ *              launch returns them to zero.  Calls that share `sync` must
+ *              not overlap in time (one stream orders them); a caller with
+ *              concurrent streams gives each its own.
+ * The first workgroups of the launch quantize A once and publish it to the
+ * others through `sync` (release / acquire at device scope); every wait is
+ * bounded, and a workgroup that gives up writes NaN into its columns of C.
+ * Null pointers: MIXFP4_ERR_NULL; misaligned: MIXFP4_ERR_ALIGN.
+ */
+int mixfp4_decode_step(const uint16_t *a, int64_t m, int64_t k, const uint8_t *w_codes,
+                       const uint8_t *w_scales, const float *w_tensor_scale, int64_t n,
+                       uint8_t *a_codes, uint8_t *a_scales, float *a_tensor_scale, float *c,
+                       uint32_t *sync, void *stream);
+
 /* HIP error string of the last MIXFP4_ERR_LAUNCH on the calling thread. */
 const char *mixfp4_last_launch_error(void);
 
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 106
+#define MIXFP4_ABI_VERSION 107
 
 #ifdef __cplusplus
 }

@@ -33,7 +33,7 @@ import torch
 
 from ._lib import LIB_PATH, MixFP4Error, lib
 
-__all__ = ["mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_hadamard", "mixfp4_dequantize",
+__all__ = ["mixfp4_decode_step", "decode_step_applies", "gemm_two_pass_preferred", "mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_hadamard", "mixfp4_dequantize",
            "mixfp4_gemm", "MixFP4Error", "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN",
            "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC", "TRANSPOSE", "mixfp4_quantize_2d",
            "mixfp4_gemm_workspace_size", "mixfp4_decode_operand", "mixfp4_gemm_decoded",
@@ -316,6 +316,64 @@ def mixfp4_gemm(a, w, out: torch.Tensor | None = None, workspace=None) -> torch.
                                 _stream(ac.device))
     _check(st)
     return out
+
+
+_STEP_SYNC: dict = {}
+
+
+def decode_step_applies(m: int, k: int) -> bool:
+    """Shapes mixfp4_decode_step takes: 1 <= m <= 16 rows, k % 512 == 0."""
+    return 1 <= m <= 16 and k > 0 and k % 512 == 0
+
+
+def mixfp4_decode_step(x: torch.Tensor, w, out: torch.Tensor | None = None, a_out=None,
+                       sync: torch.Tensor | None = None):
+    """One decode step in one launch (mixfp4_decode_step): quantize the bf16
+    activation x [m <= 16, k] (tensor scale computed on the device) and
+    return (C = x_q W^T fp32 [m, n], (codes, scales, s32) of x).  ``w`` is a
+    quantized (codes, scales, s32) triple.  ``a_out``: optional (codes,
+    scales, s32) tensors to write A's outputs into.  ``sync``: 4 zeroed
+    int32 on the device that the launch leaves zeroed; default, one per
+    device kept by this module (calls on one device must then be ordered,
+    e.g. on one stream)."""
+    if not isinstance(x, torch.Tensor) or x.dim() != 2 or x.dtype != torch.bfloat16:
+        raise ValueError("x must be a 2-D bfloat16 tensor")
+    wc, wsc, wts = w
+    m, k = x.shape
+    n = wc.shape[0] if isinstance(wc, torch.Tensor) and wc.dim() == 2 else -1
+    if not decode_step_applies(m, k) or n < 1:
+        raise ValueError(f"decode step needs 1 <= m <= 16, k % 512 == 0, n >= 1 (m={m}, k={k}, n={n})")
+    if not x.is_contiguous():
+        raise ValueError("x must be contiguous")
+    _require(wc, "W codes", torch.uint8, (n, k // 2))
+    _require(wsc, "W scales", torch.uint8, (n, k // 16))
+    if wts is not None:
+        _require(wts, "W tensor scale", torch.float32, numel=1)
+    dev = x.device
+    if a_out is None:
+        a_out = (torch.empty((m, k // 2), dtype=torch.uint8, device=dev),
+                 torch.empty((m, k // 16), dtype=torch.uint8, device=dev),
+                 torch.empty(1, dtype=torch.float32, device=dev))
+    ac, asc, ats = a_out
+    _require(ac, "A codes", torch.uint8, (m, k // 2))
+    _require(asc, "A scales", torch.uint8, (m, k // 16))
+    _require(ats, "A tensor scale", torch.float32, numel=1)
+    if out is None:
+        out = torch.empty((m, n), dtype=torch.float32, device=dev)
+    _require(out, "out", torch.float32, (m, n))
+    if sync is None:
+        key = (dev.type, dev.index if dev.index is not None else torch.cuda.current_device())
+        sync = _STEP_SYNC.get(key)
+        if sync is None:
+            sync = torch.zeros(4, dtype=torch.int32, device=dev)
+            _STEP_SYNC[key] = sync
+    _require(sync, "sync", torch.int32, numel=4)
+    _same_device(dev, ("x", x), ("W codes", wc), ("W scales", wsc), ("W tensor scale", wts),
+                 ("A codes", ac), ("A scales", asc), ("A tensor scale", ats), ("out", out),
+                 ("sync", sync))
+    _check(lib.mixfp4_decode_step(_ptr(x), m, k, _ptr(wc), _ptr(wsc), _ptr(wts), n, _ptr(ac),
+                                  _ptr(asc), _ptr(ats), _ptr(out), _ptr(sync), _stream(dev)))
+    return out, (ac, asc, ats)
 
 
 class Decoded(NamedTuple):

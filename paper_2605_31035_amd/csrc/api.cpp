@@ -227,6 +227,23 @@ int mixfp4_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_
                                            static_cast<hipStream_t>(stream)));
 }
 
+int mixfp4_decode_step(const uint16_t* a, int64_t m, int64_t k, const uint8_t* w_codes,
+                       const uint8_t* w_scales, const float* w_tensor_scale, int64_t n,
+                       uint8_t* a_codes, uint8_t* a_scales, float* a_tensor_scale, float* c,
+                       uint32_t* sync, void* stream) {
+  if (!a || !w_codes || !w_scales || !a_codes || !a_scales || !a_tensor_scale || !c || !sync)
+    return MIXFP4_ERR_NULL;
+  if (n < 1 || !mixfp4::decode_step_applies(m, k)) return MIXFP4_ERR_SHAPE;
+  if (!aligned(a, 16) || !aligned(a_codes, 16) || !aligned(a_scales, 4) || !aligned(w_scales, 4) ||
+      !aligned(w_codes, 16) || !aligned(sync, 4) || !aligned(c, 4) || !aligned(a_tensor_scale, 4) ||
+      (w_tensor_scale && !aligned(w_tensor_scale, 4)))
+    return MIXFP4_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launch_status(mixfp4::launch_decode_step(a, m, k, w_codes, w_scales, w_tensor_scale, n,
+                                                  a_codes, a_scales, a_tensor_scale, c, sync,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
 int mixfp4_gemm_workspace_size(int64_t m, int64_t n, int64_t k, int64_t* bytes) {
   if (!bytes) return MIXFP4_ERR_NULL;
   if (m < 0 || n < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;

@@ -39,6 +39,7 @@
 #include "decode.h"
 #include "formats.h"
 #include "internal.h"
+#include "quant_block.h"
 #include "tile_order.h"
 
 namespace mixfp4 {
@@ -304,12 +305,15 @@ struct APack {
   uint32_t s[kSkinnySw];
 };
 
-template <int kW, int kCG>
-__global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
+// The body of the decode-shape GEMM.  `before_a` runs once, after this
+// lane's first W loads are issued and before any A load; it returns false to
+// poison the workgroup's outputs (NaN) when A never became available.
+template <int kW, int kCG, typename BeforeA>
+__device__ __forceinline__ void skinny_body(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
-    int64_t n, int64_t k, float* __restrict__ c) {
+    int64_t n, int64_t k, float* __restrict__ c, BeforeA before_a) {
   constexpr int kCols = 16 * kCG;
   __shared__ f32x4 red[kW - 1][kCG][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -385,8 +389,9 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
   // are in flight.
   WPack<kCG> wp[2];
   APack ap[2];
-  load_a(ap[0], 0);
   load_w(wp[0], 0);
+  const bool a_ok = before_a();
+  load_a(ap[0], 0);
   auto step = [&](auto I_, int64_t s) {
     constexpr int I = decltype(I_)::value;
     __builtin_amdgcn_sched_barrier(0);
@@ -410,7 +415,7 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
   }
   __syncthreads();
   if (wave == 0) {
-    const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
+    const float scale = a_ok ? (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f) : __builtin_nanf("");
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
       f32x4 t = acc[cg];
@@ -425,6 +430,148 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
           if (row < m) c[row * n + col] = t[r] * scale;
         }
       }
+    }
+  }
+}
+
+template <int kW, int kCG>
+__global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
+    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+    const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
+    const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
+    int64_t n, int64_t k, float* __restrict__ c) {
+  skinny_body<kW, kCG>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c,
+                       []() { return true; });
+}
+
+// ---------------------------------------------------------------------------
+// One-launch decode step: tensor scale and MixFP4 quantization of the
+// activation A[m <= 16, k] (Algorithm 1), then C = A W^T by the decode-shape
+// GEMM above (the activation quantized on the fly and fed to the block-scaled
+// GEMM, Sec. 3.2 / Fig. 7, App. B.1).
+//
+// Quantizing A in every workgroup would multiply its VALU work by the number
+// of workgroups, so it is done once, by the first P <= 16 workgroups of the
+// grid ("producers"; workgroups are dispatched in index order on every XCD,
+// so the producers are resident before any other workgroup of the launch):
+//   1. each producer takes the max |A| of its 1/P of the blocks, folds it into
+//      sync[0] (atomic max of the bf16 magnitude bits) and counts itself in
+//      sync[1] with release semantics at device scope;
+//   2. once sync[1] == P it reads max|A| (acquire), forms s32 = max|A| / 2688
+//      exactly as the tensor-scale pass does (producer 0 stores it), and
+//      quantizes its blocks with the quantizer's own per-block code
+//      (quantize_xs), writing A's codes and scales;
+//   3. it counts itself in sync[2] (release).
+// Every workgroup (producers included, after their part) then runs the GEMM
+// body: it issues its first W loads, waits for sync[2] == P (acquire), and
+// reads A's codes, scales and s32 from the outputs.  The last workgroup to
+// finish (sync[3]) returns the four counters to zero for the next call.  All
+// waits are bounded (kSpinLimit polls with a sleep between them, far beyond
+// any real wait); a workgroup that gives up writes NaN to its columns of C.
+// Codes, scales and s32 are bit-identical to mixfp4_quantize in the compute
+// mode, and C to mixfp4_gemm on them (same GEMM body, same order).
+constexpr int kStepProducers = 16;
+constexpr uint32_t kSpinLimit = 1u << 22;
+constexpr int kSyncMax = 0, kSyncArrive = 1, kSyncDone = 2, kSyncExit = 3;
+
+// Polls are relaxed device-scope loads (no cache maintenance per poll); one
+// acquire fence follows the poll that sees the count, so the waiting
+// workgroup's later loads see everything the counting workgroups released.
+// (An acquire on every poll would invalidate the XCD's caches at each of
+// them, under every other workgroup's loads.)
+__device__ __forceinline__ bool wait_at_least(uint32_t* p, uint32_t target) {
+  for (uint32_t i = 0; i < kSpinLimit; ++i) {
+    if (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target) {
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      return true;
+    }
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return false;
+}
+
+// Steps 1-3 for producer blockIdx.x (block range [b0, b1) of the m * k / 16
+// blocks of A, row-major with k per row).
+__device__ __forceinline__ void produce_a(const uint16_t* __restrict__ x, int64_t m, int64_t k,
+                                          uint8_t* __restrict__ a_codes,
+                                          uint8_t* __restrict__ a_scales, float* __restrict__ a_ts,
+                                          uint32_t* sync, int producers) {
+  __shared__ ScaleRecip tab[128];
+  __shared__ uint32_t wave_max[16];
+  __shared__ float s32_sh;
+  fill_scale_table(tab);
+  const int tid = (int)threadIdx.x, nt = (int)blockDim.x;
+  const int64_t nb = m * (k / kBlock);
+  const int64_t per = (nb + producers - 1) / producers;
+  const int64_t b0 = (int64_t)blockIdx.x * per;
+  const int64_t b1 = b0 + per < nb ? b0 + per : nb;
+  uint32_t mx = 0u;
+  for (int64_t g = b0 + tid; g < b1; g += nt) {
+    const uint4* src = reinterpret_cast<const uint4*>(x + (g << 4));
+    mx = max(mx, max(absmax8(src[0]), absmax8(src[1])));
+  }
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+  if ((tid & 63) == 0) wave_max[tid >> 6] = mx;
+  __syncthreads();
+  if (tid == 0) {
+    uint32_t r = wave_max[0];
+    for (int w = 1; w < nt / 64; ++w) r = max(r, wave_max[w]);
+    if (r) atomicMax(sync + kSyncMax, r);
+    __hip_atomic_fetch_add(sync + kSyncArrive, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    const bool ok = wait_at_least(sync + kSyncArrive, (uint32_t)producers);
+    const float s32 = ok ? tensor_scale_of(__hip_atomic_load(sync + kSyncMax, __ATOMIC_RELAXED,
+                                                             __HIP_MEMORY_SCOPE_AGENT))
+                         : __builtin_nanf("");
+    s32_sh = s32;
+    if (blockIdx.x == 0) *a_ts = s32;
+  }
+  __syncthreads();                                  // also publishes the scale table
+  const float s32 = s32_sh;
+  const bool direct = s32 >= 0x1p-90f && s32 <= 0x1p120f;
+  const float xmul = direct ? 1.0f : (s32 < 1.0f ? 0x1p64f : 0x1p-64f);
+  const float sx = s32 * xmul, rx = __fdiv_rn(1.0f, sx);
+  for (int64_t g = b0 + tid; g < b1; g += nt) {
+    const uint4* src = reinterpret_cast<const uint4*>(x + (g << 4));
+    const uint4 v0 = src[0], v1 = src[1];
+    float xs[16];
+    if (direct)
+      to_fp8_domain<false>(v0, v1, 1.0f, sx, rx, xs);
+    else
+      to_fp8_domain<true>(v0, v1, xmul, sx, rx, xs);
+    uint2 out;
+    uint32_t sb;
+    quantize_xs<kSelect, false>(xs, tab, out, sb, make_uint4(0, 0, 0, 0));
+    *reinterpret_cast<uint2*>(a_codes + (g << 3)) = out;
+    a_scales[g] = (uint8_t)sb;
+  }
+  __syncthreads();                                  // every thread's stores are complete
+  if (tid == 0)
+    __hip_atomic_fetch_add(sync + kSyncDone, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <int kW, int kCG>
+__global__ __launch_bounds__(64 * kW) void decode_step_kernel(
+    const uint16_t* __restrict__ x, uint8_t* __restrict__ a_codes, uint8_t* __restrict__ a_scales,
+    float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
+    const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m, int64_t n,
+    int64_t k, float* __restrict__ c, uint32_t* sync, int producers) {
+  __shared__ int ok_sh;
+  if ((int)blockIdx.x < producers) produce_a(x, m, k, a_codes, a_scales, a_ts, sync, producers);
+  skinny_body<kW, kCG>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, [&]() {
+    if (threadIdx.x == 0) ok_sh = wait_at_least(sync + kSyncDone, (uint32_t)producers);
+    __syncthreads();
+    return ok_sh != 0;
+  });
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    // (relaxed: the count only needs atomicity; no data rides on it)
+    const uint32_t done = __hip_atomic_fetch_add(sync + kSyncExit, 1u, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT);
+    if (done + 1 == gridDim.x) {
+      // every workgroup has passed its waits: ready the counters for the next call
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        __hip_atomic_store(sync + i, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   }
 }
@@ -466,7 +613,42 @@ hipError_t launch_skinny(const uint8_t* a_codes, const uint8_t* a_scales, const 
   return hipGetLastError();
 }
 
+template <int kCG>
+hipError_t launch_step(const uint16_t* x, uint8_t* a_codes, uint8_t* a_scales, float* a_ts,
+                       const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
+                       int64_t m, int64_t n, int64_t k, float* c, uint32_t* sync,
+                       hipStream_t stream) {
+  const int64_t groups = (n + 16 * kCG - 1) / (16 * kCG);
+  const int producers = (int)(groups < kStepProducers ? groups : kStepProducers);
+  if (k % (4 * kSkinnyStep) == 0)
+    decode_step_kernel<4, kCG><<<(unsigned)groups, 256, 0, stream>>>(
+        x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, producers);
+  else
+    decode_step_kernel<2, kCG><<<(unsigned)groups, 128, 0, stream>>>(
+        x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, producers);
+  return hipGetLastError();
+}
+
 }  // namespace
+
+bool decode_step_applies(int64_t m, int64_t k) {
+  return m >= 1 && m <= kSkinnyRows && k > 0 && k % (2 * kSkinnyStep) == 0;
+}
+
+hipError_t launch_decode_step(const uint16_t* x, int64_t m, int64_t k, const uint8_t* w_codes,
+                              const uint8_t* w_scales, const float* w_ts, int64_t n,
+                              uint8_t* a_codes, uint8_t* a_scales, float* a_ts, float* c,
+                              uint32_t* sync, hipStream_t stream) {
+  // the column-group choice of the decode-shape GEMM (launch_gemm)
+  const int64_t cus = 256;
+  if (n <= 16 * cus)
+    return launch_step<1>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
+  if (n <= 32 * cus)
+    return launch_step<2>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
+  if (n <= 48 * cus)
+    return launch_step<3>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
+  return launch_step<4>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
+}
 
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
                        const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,

@@ -132,6 +132,15 @@ hipError_t launch_decode_blocked(const uint8_t* codes, const uint8_t* scales, in
 hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uint8_t* wblk,
                                const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
                                hipStream_t stream);
+// One-launch decode step (A[m, k] bf16 row-major, quantized in the launch,
+// then C = A W^T): applies for 1 <= m <= 16 and k % 512 == 0 (the decode-
+// shape GEMM's K split); `sync` is 4 zeroed uint32 on the device, returned
+// to zero by the launch.
+bool decode_step_applies(int64_t m, int64_t k);
+hipError_t launch_decode_step(const uint16_t* x, int64_t m, int64_t k, const uint8_t* w_codes,
+                              const uint8_t* w_scales, const float* w_ts, int64_t n,
+                              uint8_t* a_codes, uint8_t* a_scales, float* a_ts, float* c,
+                              uint32_t* sync, hipStream_t stream);
 // The library's static workspace (mixfp4_gemm_noalloc): kStaticScratchBytes
 // of device memory per GPU; *ptr receives its device address on the current
 // device (looked up once per device).

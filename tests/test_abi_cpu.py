@@ -286,3 +286,28 @@ def test_two_pass_rule():
     assert not M.gemm_two_pass_preferred(2048, 4096, 4096)
     assert not M.gemm_two_pass_preferred(16, 1 << 20, 4096)     # decode shape: fused
     assert not M.gemm_two_pass_preferred(16384, 16384, 48)      # k % 32 != 0
+
+
+def test_decode_step_rejects(lib):
+    """mixfp4_decode_step's argument checks, all before any device access."""
+    f = lib.mixfp4_decode_step
+    args = lambda **kw: [kw.get("a", A16), kw.get("m", 16), kw.get("k", 4096), A16, A16, None,
+                         kw.get("n", 64), kw.get("ac", A16), kw.get("as_", A16), A16,
+                         kw.get("c", A16), kw.get("sync", A16), None]
+    assert f(*args(a=None)) == 1
+    assert f(*args(sync=None)) == 1
+    assert f(*args(c=None)) == 1
+    assert f(*args(m=17)) == 2                      # more than 16 rows
+    assert f(*args(m=0)) == 2
+    assert f(*args(k=256)) == 2                     # k % 512
+    assert f(*args(n=0)) == 2
+    assert f(*args(a=P(0x10008))) == 3              # A not 16-byte aligned
+    assert f(*args(ac=P(0x10008))) == 3
+    assert f(*args(as_=P(0x10002))) == 3
+    assert f(*args(sync=P(0x10002))) == 3
+
+
+def test_decode_step_applies_rule():
+    import paper_2605_31035_amd as M
+    assert M.decode_step_applies(16, 8192) and M.decode_step_applies(1, 512)
+    assert not M.decode_step_applies(17, 8192) and not M.decode_step_applies(16, 768)
