@@ -107,7 +107,7 @@ def _blas_threads() -> int | None:
 SAMPLE_ROWS, SAMPLE_COLS = 512, 2048
 
 
-def cpu_baseline(wl, budget_s: float = 12.0, max_reps: int = 8) -> dict:
+def cpu_baseline(wl, budget_s: float = 12.0, max_reps: int = 200) -> dict:
     """The CPU oracle on a bounded sample of the headline step: the oracle
     quantize of A's first SAMPLE_ROWS rows (row chunks in a process pool; the
     tensor scale is the oracle's max over all of A) and the oracle GEMM of
