@@ -28,7 +28,8 @@
 // two halves of 16 MFMAs (one 16-K slice each): the first half reads the
 // second slice's fragments, a barrier then makes step t+1 visible, and the
 // second half reads step t+1's first slice, so no LDS latency and no barrier
-// sits in front of an MFMA that has nothing else to wait for.
+// sits in front of an MFMA that has nothing else to wait for.  The eight
+// loads a wave issues per step are spread one per four MFMAs.
 #include <mutex>
 
 #include "blocked_layout.h"
@@ -88,16 +89,12 @@ __global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restr
                        (wave & 1) * (kBlkBytes / 2);
   const i32x4 rsrc = make_rsrc(src, (uint32_t)(steps * kBlkBytes));
   const int ldst = (is_a ? 0 : kBlkBytes) + (wave & 1) * (kBlkBytes / 2);
-  auto issue = [&](int stage, int64_t st) {
-    auto* l0 = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(
-        reinterpret_cast<uintptr_t>(lds) + stage * kStageBytes + ldst);
-    auto* l1 = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(
-        reinterpret_cast<uintptr_t>(lds) + stage * kStageBytes + ldst + 4096);
-    const int so = (int)(st * kBlkBytes);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) raw_buffer_load_lds(rsrc, l0, 16, lane * 16, so, i * 1024, 0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) raw_buffer_load_lds(rsrc, l1, 16, lane * 16, so + 4096, i * 1024, 0);
+  // Part p (0-7) of this wave's share of step st: 1 KB into `stage`.
+  auto issue = [&](int stage, int64_t st, int p) {
+    const int hoff = (p >> 2) * 4096;
+    auto* l = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(
+        reinterpret_cast<uintptr_t>(lds) + stage * kStageBytes + ldst + hoff);
+    raw_buffer_load_lds(rsrc, l, 16, lane * 16, (int)(st * kBlkBytes) + hoff, (p & 3) * 1024, 0);
   };
 
   const int wm = (wave >> 1) * 128, wn = (wave & 1) * 128;
@@ -110,74 +107,71 @@ __global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restr
 #pragma unroll
       for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
 
-  // fragments of one 16-K slice: 4 A and 4 W 32-row tiles; lane (lrow, half)
-  // takes the 8-element group 2 sl + half of its row
+  // Fragments of one 16-K slice: 4 A and 4 W 32-row tiles.  Lane (lrow,
+  // half) takes the 8-element group 2 sl + half of its row.  read_pair
+  // fetches the A and W fragments of 32-row tile c.
   typedef f16x8v Frag[4];
-  auto read = [&](Frag& fa, Frag& fw, int stage, int sl) {
+  auto read_pair = [&](Frag& fa, Frag& fw, int stage, int sl, int c) {
     const uint8_t* b = lds + stage * kStageBytes;
     const int g = 2 * sl + half;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = wm + 32 * i + lrow;
-      fa[i] = *reinterpret_cast<const f16x8v*>(b + r * 64 + slot_of(r, g) * 16);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int r = wn + 32 * j + lrow;
-      fw[j] = *reinterpret_cast<const f16x8v*>(b + kBlkBytes + r * 64 + slot_of(r, g) * 16);
-    }
+    const int ra = wm + 32 * c + lrow, rw = wn + 32 * c + lrow;
+    fa[c] = *reinterpret_cast<const f16x8v*>(b + ra * 64 + slot_of(ra, g) * 16);
+    fw[c] = *reinterpret_cast<const f16x8v*>(b + kBlkBytes + rw * 64 + slot_of(rw, g) * 16);
   };
-  // W fragments are the first operand, so the accumulator tile is C^T: a lane
-  // holds row m of C and each register quad four consecutive columns
-  auto mfmas = [&](const Frag& fa, const Frag& fw) {
+  // The four MFMAs of A tile i.  W fragments are the first operand, so the
+  // accumulator tile is C^T: a lane holds row m of C and each register quad
+  // four consecutive columns.
+  auto mfma_row = [&](const Frag& fa, const Frag& fw, int i) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fw[j], fa[i], acc[i][j], 0, 0, 0);
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(fw[j], fa[i], acc[i][j], 0, 0, 0);
   };
-  // At the barrier of step t, step t+1's loads (issued at step t-2) must have
-  // landed: the two later steps' 16 loads may still be in flight.  The LDS
-  // reads of the step are complete too, so the stage refilled after the
-  // barrier is free in every wave.
-  auto wait_loads = [&]() { asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)" ::: "memory"); };
 
   const int64_t last = steps - 1;
 #pragma unroll
-  for (int p = 0; p < kStages - 1; ++p) issue(p, p < last ? p : last);
-  wait_loads();
+  for (int s0 = 0; s0 < kStages - 1; ++s0)
+#pragma unroll
+    for (int p = 0; p < 8; ++p) issue(s0, s0 < last ? s0 : last, p);
+  // step 0 landed (the two later steps' 16 loads may be in flight)
+  asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
   __builtin_amdgcn_s_barrier();
   Frag pa, pw, qa, qw;
-  read(pa, pw, 0, 0);
-  // Invariant at the top of step t: P holds slice 0 of step t; steps t+1 and
-  // t+2 are in flight or landed.  Loads and reads past the last step are
-  // clamped to it (they refill a stage that is never read again).
-  for (int64_t t = 0; t < steps; ++t) {
-    const int cur = (int)(t % kStages);
-    const int64_t tl = t + kStages - 1 < last ? t + kStages - 1 : last;
-    issue((int)((t + kStages - 1) % kStages), tl);   // the stage of step t-1
-    read(qa, qw, cur, 1);
-    mfmas(pa, pw);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // MFMA
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);   // global -> LDS load
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // LDS read
+  for (int c = 0; c < 4; ++c) read_pair(pa, pw, 0, 0, c);
+  // Invariant at the top of step t: P holds slice 0 of step t; the loads of
+  // steps t+1 and t+2 are in flight or landed.  Each half of a step runs in
+  // four chunks of one A tile's four MFMAs, each followed by one of the
+  // wave's eight 1 KB loads of step t+3 (into the stage of step t-1, which
+  // every wave finished reading before the barrier of step t-1).  Issued
+  // together, the loads fill the texture unit's address queue (the reads
+  // wait ~350 cycles on L2 and beyond), and a wave that cannot issue its
+  // next load cannot issue its next MFMA either; spread like this they
+  // measured 7% faster on 16384 x 8192 x 8192.  Loads and reads past the
+  // last step are clamped to it (they refill a stage never read again).
+  for (int64_t t = 0; t < steps; ++t) {
+    const int cur = (int)(t % kStages), ls = (int)((t + kStages - 1) % kStages);
+    const int64_t tl = t + kStages - 1 < last ? t + kStages - 1 : last;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      read_pair(qa, qw, cur, 1, c);
+      mfma_row(pa, pw, c);
+      __builtin_amdgcn_sched_barrier(0);
+      issue(ls, tl, c);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    __builtin_amdgcn_sched_barrier(0);
-    wait_loads();
+    // step t+1 landed: after its loads this wave issued the 8 of step t+2
+    // and 4 of step t+3.  The reads of slice 1 are complete too.
+    asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)" ::: "memory");
     __builtin_amdgcn_s_barrier();
     __builtin_amdgcn_sched_barrier(0);
-    read(pa, pw, (int)((t + 1) % kStages), 0);
-    mfmas(qa, qw);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int c = 0; c < 4; ++c) {
+      read_pair(pa, pw, (int)((t + 1) % kStages), 0, c);
+      mfma_row(qa, qw, c);
+      __builtin_amdgcn_sched_barrier(0);
+      issue(ls, tl, 4 + c);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
-    __builtin_amdgcn_sched_barrier(0);
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 
