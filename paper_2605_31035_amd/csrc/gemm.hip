@@ -275,8 +275,10 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // ---------------------------------------------------------------------------
 // Decode-shape GEMM (m <= 16): HBM-bound, W is read once.
 //
-// A workgroup owns 16 kCG columns of C (kCG = 1 to 4 MFMA column groups)
-// and splits K over its kW waves (4, or 2 when k is not a multiple of 1024);
+// A workgroup owns 16 kCG columns of C (kCG = 1 to 4 MFMA column groups),
+// or two such ranges one after the other (4 + 1 .. 4 + 4 groups, so that one
+// workgroup per CU covers W), and splits K over its kW waves (4, or 2 when k
+// is not a multiple of 1024);
 // each wave walks its K range in steps of 256 with no barrier and no LDS
 // until the end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
 // nn + 16 c (c < kCG, one per 16-column group) and the quarter
@@ -305,12 +307,13 @@ struct APack {
   uint32_t s[kSkinnySw];
 };
 
-// The body of the decode-shape GEMM.  `before_a` runs once, after this
-// lane's first W loads are issued and before any A load; it returns false to
-// poison the workgroup's outputs (NaN) when A never became available.
+// The body of the decode-shape GEMM for columns [col0, col0 + 16 kCG).
+// `before_a` runs once, after this lane's first W loads are issued and before
+// any A load; it returns false to poison these outputs (NaN) when A never
+// became available.
 template <int kW, int kCG, typename BeforeA>
 __device__ __forceinline__ void skinny_body(
-    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+    int64_t col0, const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c, BeforeA before_a) {
@@ -322,7 +325,6 @@ __device__ __forceinline__ void skinny_body(
   const int64_t kq = k / kW;                        // this wave's K range
   const int64_t steps = kq / kSkinnyStep;
   const int64_t kbase = wave * kq;
-  const int64_t col0 = (int64_t)blockIdx.x * kCols;
   const uint8_t* wc[kCG];
   const uint8_t* ws[kCG];
 #pragma unroll
@@ -434,14 +436,36 @@ __device__ __forceinline__ void skinny_body(
   }
 }
 
-template <int kW, int kCG>
+// Columns [16 (kA + kB) b, 16 (kA + kB) (b + 1)) of workgroup b: kA groups,
+// then kB more (kB = 0: one range).  Each column's sum is formed in the same
+// order whatever the split, so C does not depend on it.
+template <int kW, int kA, int kB, typename BeforeA>
+__device__ __forceinline__ void skinny_columns(
+    const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
+    const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
+    const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
+    int64_t n, int64_t k, float* __restrict__ c, BeforeA before_a) {
+  const int64_t col0 = (int64_t)blockIdx.x * 16 * (kA + kB);
+  bool ok = true;
+  skinny_body<kW, kA>(col0, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, [&]() {
+    ok = before_a();
+    return ok;
+  });
+  if constexpr (kB > 0) {
+    __syncthreads();                                // the reduction buffer is reused
+    skinny_body<kW, kB>(col0 + 16 * kA, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n,
+                        k, c, [&]() { return ok; });
+  }
+}
+
+template <int kW, int kA, int kB>
 __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c) {
-  skinny_body<kW, kCG>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c,
-                       []() { return true; });
+  skinny_columns<kW, kA, kB>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c,
+                             []() { return true; });
 }
 
 // ---------------------------------------------------------------------------
@@ -451,28 +475,36 @@ __global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
 // GEMM, Sec. 3.2 / Fig. 7, App. B.1).
 //
 // Quantizing A in every workgroup would multiply its VALU work by the number
-// of workgroups, so it is done once, by the first P <= 16 workgroups of the
-// grid ("producers"; workgroups are dispatched in index order on every XCD,
-// so the producers are resident before any other workgroup of the launch):
-//   1. each producer takes the max |A| of its 1/P of the blocks, folds it into
-//      sync[0] (atomic max of the bf16 magnitude bits) and counts itself in
-//      sync[1] with release semantics at device scope;
-//   2. once sync[1] == P it reads max|A| (acquire), forms s32 = max|A| / 2688
-//      exactly as the tensor-scale pass does (producer 0 stores it), and
-//      quantizes its blocks with the quantizer's own per-block code
-//      (quantize_xs), writing A's codes and scales;
-//   3. it counts itself in sync[2] (release).
+// of workgroups, so it is done once, by the first P <= 32 workgroups of the
+// grid ("producers"; workgroups are dispatched in index order, so the
+// producers are resident before any other workgroup of the launch).  Each
+// producer reads all of A for max|A| (256 KB at most, from L2 after the
+// first reader on an XCD) and forms s32 = max|A| / 2688 itself, so the
+// producers never wait for each other: an exchange of partial maxima costs a
+// chain of device-scope atomics, each a round trip of ~1.5 us across the
+// XCDs, and measured 4.7 us against ~2.5 us for the redundant read.  A
+// producer then quantizes its 1/P of the blocks with the quantizer's own
+// per-block code (quantize_xs), writing A's codes and scales (producer 0
+// also s32), and counts itself in sync[0] with release semantics at device
+// scope.
 // Every workgroup (producers included, after their part) then runs the GEMM
-// body: it issues its first W loads, waits for sync[2] == P (acquire), and
+// body: it issues its first W loads, waits for sync[0] == P (acquire), and
 // reads A's codes, scales and s32 from the outputs.  The last workgroup to
-// finish (sync[3]) returns the four counters to zero for the next call.  All
+// finish (sync[1]) returns the counters to zero for the next call.  All
 // waits are bounded (kSpinLimit polls with a sleep between them, far beyond
 // any real wait); a workgroup that gives up writes NaN to its columns of C.
 // Codes, scales and s32 are bit-identical to mixfp4_quantize in the compute
 // mode, and C to mixfp4_gemm on them (same GEMM body, same order).
-constexpr int kStepProducers = 16;
+//
+// Measured on 16 x 28672 x 8192 (one workgroup per CU): the producers have
+// s32 after ~6 us and A quantized after ~8.5 us, and the consumers see the
+// count at ~11.8 us; the GEMM bodies then take ~31 us.  A separate quantize
+// launch before the GEMM costs less (~7 us, kernel boundaries being the
+// cheapest grid-wide synchronization here), so the one-launch step serves
+// callers that want a single dispatch, not speed.
+constexpr int kStepProducers = 32;
 constexpr uint32_t kSpinLimit = 1u << 22;
-constexpr int kSyncMax = 0, kSyncArrive = 1, kSyncDone = 2, kSyncExit = 3;
+constexpr int kSyncDone = 0, kSyncExit = 1;
 
 // Polls are relaxed device-scope loads (no cache maintenance per poll); one
 // acquire fence follows the poll that sees the count, so the waiting
@@ -490,43 +522,40 @@ __device__ __forceinline__ bool wait_at_least(uint32_t* p, uint32_t target) {
   return false;
 }
 
-// Steps 1-3 for producer blockIdx.x (block range [b0, b1) of the m * k / 16
-// blocks of A, row-major with k per row).
+// Producer blockIdx.x < producers: s32 from all of A, then the blocks
+// [b0, b1) of its share of the m * k / 16 blocks of A (row-major, k per row).
 __device__ __forceinline__ void produce_a(const uint16_t* __restrict__ x, int64_t m, int64_t k,
                                           uint8_t* __restrict__ a_codes,
                                           uint8_t* __restrict__ a_scales, float* __restrict__ a_ts,
                                           uint32_t* sync, int producers) {
   __shared__ ScaleRecip tab[128];
   __shared__ uint32_t wave_max[16];
-  __shared__ float s32_sh;
   fill_scale_table(tab);
   const int tid = (int)threadIdx.x, nt = (int)blockDim.x;
+  // max |A| over all of A: 16-byte words, eight loads in flight per thread
+  const int64_t nvec = m * k / 8;
+  const uint4* xv = reinterpret_cast<const uint4*>(x);
+  uint32_t mx = 0u;
+  int64_t i = tid;
+  for (; i + 7 * nt < nvec; i += 8 * nt) {
+    uint4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = xv[i + j * nt];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) mx = max(mx, absmax8(v[j]));
+  }
+  for (; i < nvec; i += nt) mx = max(mx, absmax8(xv[i]));
+  for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
+  if ((tid & 63) == 0) wave_max[tid >> 6] = mx;
+  __syncthreads();                                  // also publishes the scale table
+  uint32_t r = wave_max[0];
+  for (int w = 1; w < nt / 64; ++w) r = max(r, wave_max[w]);
+  const float s32 = tensor_scale_of(r);
+  if (blockIdx.x == 0 && tid == 0) *a_ts = s32;
   const int64_t nb = m * (k / kBlock);
   const int64_t per = (nb + producers - 1) / producers;
   const int64_t b0 = (int64_t)blockIdx.x * per;
   const int64_t b1 = b0 + per < nb ? b0 + per : nb;
-  uint32_t mx = 0u;
-  for (int64_t g = b0 + tid; g < b1; g += nt) {
-    const uint4* src = reinterpret_cast<const uint4*>(x + (g << 4));
-    mx = max(mx, max(absmax8(src[0]), absmax8(src[1])));
-  }
-  for (int off = 32; off > 0; off >>= 1) mx = max(mx, (uint32_t)__shfl_xor((int)mx, off));
-  if ((tid & 63) == 0) wave_max[tid >> 6] = mx;
-  __syncthreads();
-  if (tid == 0) {
-    uint32_t r = wave_max[0];
-    for (int w = 1; w < nt / 64; ++w) r = max(r, wave_max[w]);
-    if (r) atomicMax(sync + kSyncMax, r);
-    __hip_atomic_fetch_add(sync + kSyncArrive, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-    const bool ok = wait_at_least(sync + kSyncArrive, (uint32_t)producers);
-    const float s32 = ok ? tensor_scale_of(__hip_atomic_load(sync + kSyncMax, __ATOMIC_RELAXED,
-                                                             __HIP_MEMORY_SCOPE_AGENT))
-                         : __builtin_nanf("");
-    s32_sh = s32;
-    if (blockIdx.x == 0) *a_ts = s32;
-  }
-  __syncthreads();                                  // also publishes the scale table
-  const float s32 = s32_sh;
   const bool direct = s32 >= 0x1p-90f && s32 <= 0x1p120f;
   const float xmul = direct ? 1.0f : (s32 < 1.0f ? 0x1p64f : 0x1p-64f);
   const float sx = s32 * xmul, rx = __fdiv_rn(1.0f, sx);
@@ -549,7 +578,7 @@ __device__ __forceinline__ void produce_a(const uint16_t* __restrict__ x, int64_
     __hip_atomic_fetch_add(sync + kSyncDone, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-template <int kW, int kCG>
+template <int kW, int kA, int kB>
 __global__ __launch_bounds__(64 * kW) void decode_step_kernel(
     const uint16_t* __restrict__ x, uint8_t* __restrict__ a_codes, uint8_t* __restrict__ a_scales,
     float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
@@ -557,7 +586,7 @@ __global__ __launch_bounds__(64 * kW) void decode_step_kernel(
     int64_t k, float* __restrict__ c, uint32_t* sync, int producers) {
   __shared__ int ok_sh;
   if ((int)blockIdx.x < producers) produce_a(x, m, k, a_codes, a_scales, a_ts, sync, producers);
-  skinny_body<kW, kCG>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, [&]() {
+  skinny_columns<kW, kA, kB>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, [&]() {
     if (threadIdx.x == 0) ok_sh = wait_at_least(sync + kSyncDone, (uint32_t)producers);
     __syncthreads();
     return ok_sh != 0;
@@ -599,34 +628,60 @@ hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   return hipGetLastError();
 }
 
-template <int kCG>
+template <int kA, int kB>
 hipError_t launch_skinny(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
                          const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
                          int64_t m, int64_t n, int64_t k, float* c, hipStream_t stream) {
-  const unsigned groups = (unsigned)((n + 16 * kCG - 1) / (16 * kCG));
+  const unsigned groups = (unsigned)((n + 16 * (kA + kB) - 1) / (16 * (kA + kB)));
   if (k % (4 * kSkinnyStep) == 0)
-    gemm_skinny_kernel<4, kCG><<<groups, 256, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
-                                                           w_scales, w_ts, m, n, k, c);
+    gemm_skinny_kernel<4, kA, kB><<<groups, 256, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
+                                                              w_scales, w_ts, m, n, k, c);
   else
-    gemm_skinny_kernel<2, kCG><<<groups, 128, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
-                                                           w_scales, w_ts, m, n, k, c);
+    gemm_skinny_kernel<2, kA, kB><<<groups, 128, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
+                                                              w_scales, w_ts, m, n, k, c);
   return hipGetLastError();
 }
 
-template <int kCG>
+template <int kA, int kB>
 hipError_t launch_step(const uint16_t* x, uint8_t* a_codes, uint8_t* a_scales, float* a_ts,
                        const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
                        int64_t m, int64_t n, int64_t k, float* c, uint32_t* sync,
                        hipStream_t stream) {
-  const int64_t groups = (n + 16 * kCG - 1) / (16 * kCG);
+  const int64_t groups = (n + 16 * (kA + kB) - 1) / (16 * (kA + kB));
   const int producers = (int)(groups < kStepProducers ? groups : kStepProducers);
   if (k % (4 * kSkinnyStep) == 0)
-    decode_step_kernel<4, kCG><<<(unsigned)groups, 256, 0, stream>>>(
+    decode_step_kernel<4, kA, kB><<<(unsigned)groups, 256, 0, stream>>>(
         x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, producers);
   else
-    decode_step_kernel<2, kCG><<<(unsigned)groups, 128, 0, stream>>>(
+    decode_step_kernel<2, kA, kB><<<(unsigned)groups, 128, 0, stream>>>(
         x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, producers);
   return hipGetLastError();
+}
+
+// Column groups per workgroup of the decode-shape GEMM: the fewest 16-column
+// groups G that cover W with at most one workgroup per CU, run as one range
+// (G <= 4) or as 4 + (G - 4); beyond 8 groups, 4 per workgroup and several
+// workgroups per CU.  Narrow W then still spreads over every CU, and no CU
+// gets two workgroups while others get one.  Measured, m = 16:
+// k = 4096, n = 4096: 5.3 us with G = 1 against 11.7 with 4; n = 8192 7.5
+// against 11.8; n = 11008 9.7 against 11.6; 16 x 28672 x 8192: 33.3 us with
+// 4 + 3 groups on 256 workgroups against 35.4 with 4 groups on 448 (192 CUs
+// with two of them).
+template <typename Launch>
+hipError_t by_column_split(int64_t n, Launch launch) {
+  const int64_t cus = compute_units();
+  const int64_t g = (n + 16 * cus - 1) / (16 * cus);
+  switch (g) {
+    case 1: return launch(std::integral_constant<int, 1>{}, std::integral_constant<int, 0>{});
+    case 2: return launch(std::integral_constant<int, 2>{}, std::integral_constant<int, 0>{});
+    case 3: return launch(std::integral_constant<int, 3>{}, std::integral_constant<int, 0>{});
+    case 4: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 0>{});
+    case 5: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 1>{});
+    case 6: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 2>{});
+    case 7: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 3>{});
+    case 8: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 4>{});
+    default: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 0>{});
+  }
 }
 
 }  // namespace
@@ -639,15 +694,11 @@ hipError_t launch_decode_step(const uint16_t* x, int64_t m, int64_t k, const uin
                               const uint8_t* w_scales, const float* w_ts, int64_t n,
                               uint8_t* a_codes, uint8_t* a_scales, float* a_ts, float* c,
                               uint32_t* sync, hipStream_t stream) {
-  // the column-group choice of the decode-shape GEMM (launch_gemm)
-  const int64_t cus = 256;
-  if (n <= 16 * cus)
-    return launch_step<1>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
-  if (n <= 32 * cus)
-    return launch_step<2>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
-  if (n <= 48 * cus)
-    return launch_step<3>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
-  return launch_step<4>(x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
+  // the column split of the decode-shape GEMM (launch_gemm)
+  return by_column_split(n, [&](auto A, auto B) {
+    return launch_step<decltype(A)::value, decltype(B)::value>(
+        x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, stream);
+  });
 }
 
 hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
@@ -666,19 +717,10 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   const bool skinny_aligned = ((reinterpret_cast<uintptr_t>(w_scales) |
                                 reinterpret_cast<uintptr_t>(a_scales)) & 3u) == 0;
   if (m <= kSkinnyRows && skinny_aligned && k % (2 * kSkinnyStep) == 0) {
-    // The narrowest workgroups (16, 32, 48 or 64 columns) that need at most
-    // one workgroup per CU, so that narrow W still spreads over every CU
-    // without leaving some CUs two; wider W takes 64 columns (best per column,
-    // one A decode for four column groups).  Measured, m = 16, k = 4096:
-    // n = 4096 5.3 us with 16 columns against 11.7 with 64; n = 8192 7.5
-    // against 11.8 with 32; n = 11008 9.7 against 11.6 with 48; n = 14336
-    // 12.0 with 64 against 16.8 with 48 (299 workgroups); 16 x 28672 x 8192
-    // 35.0 us with 64.
-    const int64_t cus = 256;
-    if (n <= 16 * cus) return launch_skinny<1>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
-    if (n <= 32 * cus) return launch_skinny<2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
-    if (n <= 48 * cus) return launch_skinny<3>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
-    return launch_skinny<4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    return by_column_split(n, [&](auto A, auto B) {
+      return launch_skinny<decltype(A)::value, decltype(B)::value>(
+          a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);
+    });
   }
   // Tile choice (measured on MI355X): 256 x 256 with 8 waves is the most
   // efficient tile per compute unit (least LDS traffic and decode work per
@@ -691,14 +733,15 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   const int64_t tm = (m + 255) / 256, tn = (n + 255) / 256;
   const int64_t tiles256 = tm * tn;
   const int64_t tiles128x256 = ((m + 127) / 128) * tn;
-  if (4 * tiles256 >= 3 * 256) {
+  const int64_t cus = compute_units();
+  if (4 * tiles256 >= 3 * cus) {
     // A short last round of 256 x 256 tiles keeps only a few CUs busy for a
     // whole tile time.  Its columns go to a second launch of 128 x 256 tiles
     // (half the work per CU) when those fit in one round: every output still
     // sums its K range in the same order, so C is bit-identical.
-    const int64_t nt1 = (tiles256 / 256) * 256 / tm;    // 256-column tiles in whole rounds
+    const int64_t nt1 = (tiles256 / cus) * cus / tm;    // 256-column tiles in whole rounds
     const int64_t rest = 2 * tm * (tn - nt1);           // 128 x 256 tiles left
-    if (nt1 > 0 && nt1 < tn && rest <= 256) {
+    if (nt1 > 0 && nt1 < tn && rest <= cus) {
       const int64_t n1 = 256 * nt1;
       const hipError_t e = launch_tile<256, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales,
                                                        w_ts, m, n1, k, c, n, stream);
@@ -710,7 +753,7 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     return launch_tile<256, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
                                        c, n, stream);
   }
-  if (tiles128x256 >= 192)
+  if (4 * tiles128x256 >= 3 * cus)
     return launch_tile<128, 256, 2, 4>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,
                                        c, n, stream);
   return launch_tile<128, 128, 2, 2>(a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k,

@@ -63,6 +63,22 @@ int64_t resident_groups(Kernel kernel, ResidentCache& cache, int max_per_cu = 0,
   return v;
 }
 
+// Compute units of the current device (queried once per device; 256 if the
+// query fails).
+inline int64_t compute_units() {
+  static std::atomic<int64_t> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  const int64_t known = cache[dev].load(std::memory_order_relaxed);
+  if (known) return known;
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  cache[dev].store(cus, std::memory_order_relaxed);
+  return cus;
+}
+
 // Launchers: shapes are validated by the ABI layer before these are called.
 // Tensor scale s32 = max|X| / 2688 (1.0 for all-zero X) into *tensor_scale.
 // `scratch` (may be NULL) is device memory of `scratch_bytes` that the call

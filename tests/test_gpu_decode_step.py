@@ -45,7 +45,7 @@ def _step(a_bits, qw_dev):
 def test_shapes(m, n, k):
     """Every column-group width (16 .. 64 columns per workgroup), both K
     splits (k % 1024 == 0: four waves, else two), ragged m and n, and grids
-    smaller than the 16 producer workgroups (n = 17: two workgroups)."""
+    smaller than the 32 producer workgroups (n = 17: two workgroups)."""
     import paper_2605_31035_amd as M
     a_bits = W.adversarial(m + 3 * n, m, k)
     w_bits = W.adversarial(n + 7, n, k)
@@ -61,6 +61,31 @@ def test_shapes(m, n, k):
         [[0, n - 1], np.random.default_rng(n).integers(0, n, 256)]))
     _check_c(c, qa, qw, cols)
     assert M.decode_step_applies(m, k)
+
+
+@pytest.mark.parametrize("m,n,k", [(16, 22000, 1024), (3, 28000, 512), (16, 31000, 1024),
+                                   (8, 40000, 512)])
+def test_wide_w_column_splits(m, n, k):
+    """Wide W: 4 + 2, 4 + 3 and 4 + 4 column groups per workgroup (one
+    workgroup per CU) and 4 groups with several workgroups per CU.  W is
+    quantized on the device; A's outputs are checked against the oracle bit
+    for bit and C on sampled columns."""
+    import paper_2605_31035_amd as M
+    a_bits = W.adversarial(2 * m + n, m, k)
+    w_bits = W.adversarial(5 * n + 3, n, k)
+    log(f"decode step wide m={m} n={n} k={k}")
+    qw_dev = M.mixfp4_quantize(dev_bf16(w_bits))
+    torch.cuda.synchronize()
+    c, codes, scales, s32 = _step(a_bits, qw_dev)
+    qa = Q.quantize(a_bits)
+    assert np.float32(s32) == np.float32(qa.s32)
+    np.testing.assert_array_equal(codes, qa.codes)
+    np.testing.assert_array_equal(scales, qa.scales)
+    cols = np.unique(np.concatenate([[0, n - 1], np.arange(0, n, 1792)[:40],
+                                     np.random.default_rng(n).integers(0, n, 96)]))
+    qw = Q.quantize(w_bits[cols], s32=Q.tensor_scale(w_bits))
+    np.testing.assert_array_equal(host(qw_dev[0])[cols], qw.codes)
+    _check_c(c[:, cols], qa, qw)
 
 
 def test_decode_workload_full_size():

@@ -218,3 +218,40 @@ def test_workload_full_size(name):
         qw = Q.quantize(w_bits[cols], s32=Q.tensor_scale(w_bits))
         worst = _check(c[np.ix_(rows, cols)], qa, qw)
         log(f"{name} {a_name}x{w_name} ok, worst ratio {worst:.3g}")
+
+
+@pytest.mark.parametrize("m,n,k", [(16, 17000, 512), (5, 22000, 1024), (16, 28672, 512),
+                                   (11, 30000, 1024), (16, 40000, 512)])
+def test_decode_shapes_column_splits(m, n, k):
+    """Wide W on the decode-shape kernel: 4 + 1, 4 + 2, 4 + 3 and 4 + 4
+    column groups per workgroup (one workgroup per CU), and 4 groups with
+    several workgroups per CU beyond that.  W is quantized on the device (the
+    quantizer's parity is tested on its own); C is checked on sampled columns,
+    both ends of each workgroup's column range included, against the oracle
+    quantizing those W rows with W's tensor scale; and column slices cut
+    inside a workgroup's range equal the full product bit for bit."""
+    import paper_2605_31035_amd as M
+    a_bits = W.adversarial(m + n, m, k)
+    w_bits = W.adversarial(3 * n + 1, n, k)
+    log(f"gemm decode-shape split m={m} n={n} k={k}")
+    qa = Q.quantize(a_bits)
+    a = (dev_u8(qa.codes), dev_u8(qa.scales), dev_f32(qa.s32))
+    wc, ws, wt = gpu_quantize(w_bits)
+    full = M.mixfp4_gemm(a, (wc, ws, wt))
+    groups = -(-n // (16 * 256))
+    per = 16 * (groups if groups <= 8 else 4)
+    edges = np.arange(0, n, per)
+    rng = np.random.default_rng(n)
+    cols = np.unique(np.concatenate([edges, np.minimum(edges + per - 1, n - 1),
+                                     np.minimum(edges + 64, n - 1), [n - 1],
+                                     rng.integers(0, n, 128)]))
+    cols = cols[(cols >= 0) & (cols < n)]
+    cols = np.unique(np.concatenate([cols[::max(1, len(cols) // 160)], [0, n - 1]]))
+    qw = Q.quantize(w_bits[cols], s32=Q.tensor_scale(w_bits))
+    np.testing.assert_array_equal(host(wc)[cols], qw.codes)
+    worst = _check(host(full)[:, cols], qa, qw)
+    lo, hi = per + 40, 3 * per + 17
+    part = M.mixfp4_gemm(a, (wc[lo:hi], ws[lo:hi], wt))
+    torch.cuda.synchronize()
+    assert torch.equal(part, full[:, lo:hi])
+    log(f"split ok, worst ratio {worst:.3g}")
