@@ -220,7 +220,10 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
     torch.cuda.empty_cache()
     yq = torch.empty_like(xq)
     ms_had = time_calls(lambda: M.mixfp4_hadamard(xq, 128, signs, out=yq))
-    del xq, yq
+    del yq
+    torch.cuda.empty_cache()
+    variants = measure_variants(M, torch, xq, time_calls)
+    del xq
     torch.cuda.empty_cache()
     gbps = n * QUANT_BYTES_PER_ELEM / (ms_given * 1e-3) / 1e9
 
@@ -254,7 +257,42 @@ def measure_quantize(M, torch, dev, iters: int = 20) -> dict:
         "hadamard128_us": round(ms_had * 1e3, 2), "hadamard128_GBps": rate(ms_had, 4.0),
         "hadamard_note": "standalone mixfp4_hadamard, 128-blocks with signs: 2 B read + 2 B "
                          "written per element",
+        "variants": variants,
     }
+
+
+VARIANT_SETS = (("e2m1",), ("e2m1", "e1m2"), ("e2m1", "e3m0"), ("e2m1", "e1m2", "e3m0"))
+
+
+def measure_variants(M, torch, xq, time_calls) -> dict:
+    """Algorithm 1's selection over the candidate sets and block sizes of the
+    paper's ablation (Table 5: FP4-E2, +FP4-E1, +FP4-E3, +E1+E3 at block
+    sizes 8, 16, 32, 64) on the same 2^28-element tensor: the kernel's rate
+    (tensor scale given; 2 B read, 0.5 B of codes and two bytes per block
+    written) and the relative squared error sum (X - dequant)^2 / sum X^2 of
+    the result (tensor scale computed), summed in fp64 on the device."""
+    n = xq.numel()
+    x64 = None
+    out = {}
+    for block in (8, 16, 32, 64):
+        for cands in VARIANT_SETS:
+            q = M.mixfp4_quantize_variant(xq, block, cands)
+            ms = time_calls(lambda: M.mixfp4_quantize_variant(xq, block, cands, q.s32))
+            d = M.mixfp4_dequantize_variant(q)
+            if x64 is None:
+                x64 = xq.to(torch.float64)
+                den = float((x64 * x64).sum())
+            err = float(((x64 - d.to(torch.float64)) ** 2).sum()) / den
+            frac = [round(float((q.fmt == i).sum()) / q.fmt.numel(), 4) for i in range(len(cands))]
+            del d, q
+            bpe = 2.0 + 0.5 + 2.0 / block
+            out[f"g{block}_" + "+".join(cands)] = {
+                "us": round(ms * 1e3, 2), "GBps": round(n * bpe / (ms * 1e-3) / 1e9, 1),
+                "bytes_per_elem": round(bpe, 4), "rel_sse": float(f"{err:.6g}"),
+                "chosen_fraction": frac}
+    del x64
+    torch.cuda.empty_cache()
+    return out
 
 
 def measure_decode(M, torch, dev, iters: int = 50) -> dict:

@@ -203,6 +203,56 @@ int mixfp4_dequantize(const uint8_t *codes, const uint8_t *scales,
                       float *out, void *stream);
 
 /*
+ * mixfp4_quantize_variant - the block-wise format selection of Algorithm 1
+ * over another FP4 candidate set or block size, as the paper's ablations
+ * study it (Sec. 2.3-2.4 and Fig. 3: the sets {E2M1}, {E2M1, E1M2},
+ * {E2M1, E1M2, E3M0}; Table 5: block sizes 8, 16, 32, 64).  The tensor scale
+ * and FP8 domain are Algorithm 1's (s32 = max|X| / 2688); each block of
+ * `block` consecutive K elements takes, per candidate f, the E4M3 scale
+ * FP8_E4M3(bm / Q_f) (Q = 6 for E2M1, 7 for E1M2 x2, 16 for E3M0), rounds
+ * |x| / s_f to f's grid (nearest, ties to the even code, saturating), and
+ * keeps the candidate with the smallest exact squared error, ties going to
+ * the later candidate in the order E2M1, E1M2, E3M0 (so {E2M1, E1M2} at
+ * block 16 is mixfp4_quantize's MixFP4, bit for bit).  E3M0 is the FP4
+ * format with three exponent bits and bias 3: code p > 0 is 2^(p - 3), so
+ * its grid is {0, 1/4, 1/2, 1, 2, 4, 8, 16}.
+ *
+ *   x, rows, k, ldx  as for mixfp4_quantize, with k % block == 0.
+ *   block            8, 16, 32 or 64 (else MIXFP4_ERR_SHAPE).
+ *   candidates       non-empty OR of MIXFP4_CAND_E2M1 / _E1M2 / _E3M0
+ *                    (else MIXFP4_ERR_FLAGS).
+ *   codes            out, [rows, k/2], nibble [sign | 3-bit code] as in
+ *                    MixFP4, 16-byte aligned.
+ *   scales           out, [rows, k/block]: the chosen candidate's E4M3 code in
+ *                    bits 6:0; bit 7 is the chosen index for two candidates
+ *                    (T, as in MixFP4) and 0 otherwise.
+ *   fmt              out, [rows, k/block] chosen candidate index (0-based in
+ *                    the order above), or NULL; required with all three
+ *                    candidates (two bits do not fit the scale byte).
+ *   tensor_scale, flags  as for mixfp4_quantize (MIXFP4_SCALE_COMPUTE or
+ *                    MIXFP4_SCALE_GIVEN only).
+ */
+#define MIXFP4_CAND_E2M1 1u
+#define MIXFP4_CAND_E1M2 2u
+#define MIXFP4_CAND_E3M0 4u
+int mixfp4_quantize_variant(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
+                            int32_t block, unsigned candidates, uint8_t *codes,
+                            uint8_t *scales, uint8_t *fmt, float *tensor_scale,
+                            unsigned flags, void *stream);
+
+/*
+ * mixfp4_dequantize_variant - decode mixfp4_quantize_variant's output:
+ * out = fl32(s32 * (E4M3(scale & 0x7F) * v)) * sign with v from the block's
+ * chosen candidate (fmt if given, else bit 7 of the scale byte for two
+ * candidates, else the only one).  Arguments as for the quantizer; out is
+ * rows * k floats, contiguous, 16-byte aligned; tensor_scale NULL means 1.0.
+ */
+int mixfp4_dequantize_variant(const uint8_t *codes, const uint8_t *scales,
+                              const uint8_t *fmt, const float *tensor_scale,
+                              int64_t rows, int64_t k, int32_t block,
+                              unsigned candidates, float *out, void *stream);
+
+/*
  * mixfp4_gemm - C[m, n] = sum_k A[m, k] * W[n, k] for two MixFP4 operands
  * (C = A W^T, both quantized along the reduction dimension K, App. B.1).
  * Each element is decoded through the unified E2M2 value set (Sec. 3.3,
@@ -356,7 +406,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 107
+#define MIXFP4_ABI_VERSION 108
 
 #ifdef __cplusplus
 }

@@ -26,6 +26,10 @@ def _value(e: int, m: int, we: int, wm: int) -> Fraction:
 E2M1 = [(p, _value(p >> 1, p & 1, 2, 1)) for p in range(8)]
 E1M2X2 = [(p, 2 * _value(p >> 2, p & 3, 1, 2)) for p in range(8)]
 E4M3 = [(c, _value(c >> 3, c & 7, 4, 3)) for c in range(127)]
+# E3M0 (W_E = 3, W_M = 0): the exponent-only FP4 micro-format of Sec. 2.3.
+E3M0 = [(p, _value(p, 0, 3, 0)) for p in range(8)]
+# candidate name -> (codebook, divisor of the block max)
+BOOKS = {"e2m1": (E2M1, 6), "e1m2": (E1M2X2, 7), "e3m0": (E3M0, 16)}
 
 
 def nearest(q: Fraction, book) -> tuple[int, Fraction]:
@@ -167,3 +171,55 @@ def decode_value(nibble: int, scale_byte: int) -> Fraction:
     s8 = E4M3[scale_byte & 0x7F][1]
     mag = (E1M2X2 if t else E2M1)[nibble & 7][1]
     return (-1 if nibble & 8 else 1) * mag * s8
+
+
+def quantize_block_variant(xb_bits, s32: Fraction, candidates):
+    """One block (any length) of bf16 bit patterns under Algorithm 1 with the
+    given candidate formats (names of BOOKS): each candidate's E4M3 scale of
+    fl32(bm / divisor), codes scanned for the nearest value of the exact
+    quotient, the exact squared error; the smallest error wins and ties go to
+    the later candidate.  Returns (scale code, chosen index, [nibbles],
+    [errors])."""
+    X = [bf16_value(int(b)) for b in xb_bits]
+    x = [round_f32(v / s32) for v in X]
+    bm = max(abs(v) for v in x)
+    res = []
+    for name in candidates:
+        book, div = BOOKS[name]
+        scode, s8 = nearest(round_f32(bm / div), E4M3)
+        codes, err = [], Fraction(0)
+        for v in x:
+            c, qv = (0, Fraction(0)) if s8 == 0 else nearest(abs(v) / s8, book)
+            err += (abs(v) - qv * s8) ** 2
+            codes.append(c)
+        res.append((scode, codes, err))
+    best = 0
+    for j in range(1, len(res)):
+        if res[j][2] <= res[best][2]:
+            best = j
+    scode, mags, _ = res[best]
+    nibs = [((int(b) >> 15) << 3) | c for b, c in zip(xb_bits, mags)]
+    return scode, best, nibs, [r[2] for r in res]
+
+
+def quantize_variant(x_bits_2d, block: int, candidates, s32=None):
+    """Brute force of ``oracle.variants.quantize_variant`` on a small array:
+    (codes bytes [rows][K/2], scale bytes [rows][K/g], chosen index
+    [rows][K/g], s32).  T is bit 7 of the scale byte for two candidates."""
+    rows = [list(map(int, r)) for r in x_bits_2d]
+    flat = [b for r in rows for b in r]
+    s = tensor_scale(flat) if s32 is None else Fraction(s32)
+    codes, scales, fmts = [], [], []
+    for r in rows:
+        crow, srow, frow = [], [], []
+        for j in range(0, len(r), block):
+            sc, best, nibs, _ = quantize_block_variant(r[j:j + block], s, candidates)
+            t = best if len(candidates) == 2 else 0
+            srow.append((t << 7) | sc)
+            frow.append(best)
+            crow.extend(nibs[i] | (nibs[i + 1] << 4) for i in range(0, block, 2))
+        codes.append(crow)
+        scales.append(srow)
+        fmts.append(frow)
+    return codes, scales, fmts, s
+

@@ -37,7 +37,8 @@ __all__ = ["mixfp4_decode_step", "decode_step_applies", "gemm_two_pass_preferred
            "mixfp4_gemm", "MixFP4Error", "LIB_PATH", "lib", "SCALE_COMPUTE", "SCALE_GIVEN",
            "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC", "TRANSPOSE", "mixfp4_quantize_2d",
            "mixfp4_gemm_workspace_size", "mixfp4_decode_operand", "mixfp4_gemm_decoded",
-           "Decoded"]
+           "Decoded", "mixfp4_quantize_variant", "mixfp4_dequantize_variant", "Variant",
+           "CANDIDATES"]
 
 SCALE_COMPUTE = 0
 SCALE_GIVEN = 1
@@ -242,6 +243,69 @@ def mixfp4_dequantize(codes: torch.Tensor, scales: torch.Tensor,
     st = lib.mixfp4_dequantize(_ptr(codes), _ptr(scales), _ptr(tensor_scale), rows, k,
                                _ptr(out), _stream(codes.device))
     _check(st)
+    return out
+
+
+# candidate formats of mixfp4_quantize_variant and their bits in the ABI
+CANDIDATES = {"e2m1": 1, "e1m2": 2, "e3m0": 4}
+
+
+class Variant(NamedTuple):
+    """Output of mixfp4_quantize_variant."""
+    codes: torch.Tensor      # uint8 [rows, k/2]
+    scales: torch.Tensor     # uint8 [rows, k/block]
+    fmt: torch.Tensor        # uint8 [rows, k/block], chosen candidate index
+    s32: torch.Tensor        # fp32 [1]
+    block: int
+    mask: int
+
+
+def _cand_mask(candidates) -> int:
+    mask = 0
+    for c in candidates:
+        if c not in CANDIDATES or mask & CANDIDATES[c]:
+            raise ValueError(f"candidates must be distinct names among {sorted(CANDIDATES)}")
+        mask |= CANDIDATES[c]
+    if not mask:
+        raise ValueError("at least one candidate format is needed")
+    return mask
+
+
+def mixfp4_quantize_variant(x: torch.Tensor, block: int = 16, candidates=("e2m1", "e1m2"),
+                            tensor_scale: torch.Tensor | None = None) -> Variant:
+    """Algorithm 1's block-wise selection over another candidate set and
+    block size (mixfp4_quantize_variant): ``candidates`` a subset of
+    ("e2m1", "e1m2", "e3m0"), taken in that order whatever the order given;
+    ``block`` 8, 16, 32 or 64.  ``tensor_scale`` None computes s32."""
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D bfloat16 CUDA tensor with unit stride along K")
+    mask = _cand_mask(candidates)
+    rows, k = x.shape
+    if block not in (8, 16, 32, 64) or k % block:
+        raise ValueError("block must be 8, 16, 32 or 64 and divide k")
+    dev = x.device
+    codes = torch.empty((rows, k // 2), dtype=torch.uint8, device=dev)
+    scales = torch.empty((rows, k // block), dtype=torch.uint8, device=dev)
+    fmt = torch.empty((rows, k // block), dtype=torch.uint8, device=dev)
+    if tensor_scale is None:
+        ts, flags = torch.empty(1, dtype=torch.float32, device=dev), SCALE_COMPUTE
+    else:
+        ts, flags = tensor_scale, SCALE_GIVEN
+        _require(ts, "tensor_scale", torch.float32, numel=1)
+    _same_device(dev, ("x", x), ("tensor scale", ts))
+    _check(lib.mixfp4_quantize_variant(_ptr(x), rows, k, x.stride(0), block, mask, _ptr(codes),
+                                       _ptr(scales), _ptr(fmt), _ptr(ts), flags, _stream(dev)))
+    return Variant(codes, scales, fmt, ts, block, mask)
+
+
+def mixfp4_dequantize_variant(q: Variant, use_fmt: bool = True) -> torch.Tensor:
+    """Decode a Variant to fp32 [rows, k] (with its s32).  ``use_fmt`` False
+    decodes from the scale bytes alone (possible for sets of one or two)."""
+    rows, k = q.codes.shape[0], q.codes.shape[1] * 2
+    out = torch.empty((rows, k), dtype=torch.float32, device=q.codes.device)
+    _check(lib.mixfp4_dequantize_variant(_ptr(q.codes), _ptr(q.scales),
+                                         _ptr(q.fmt) if use_fmt else None, _ptr(q.s32), rows, k,
+                                         q.block, q.mask, _ptr(out), _stream(q.codes.device)))
     return out
 
 

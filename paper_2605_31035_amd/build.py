@@ -22,7 +22,7 @@ CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libmixfp4.so")
 SOURCES = ["api.cpp", "quantize.hip", "quantize2d.hip", "dequantize.hip", "gemm.hip",
-           "gemm_f16.hip", "decode_operand.hip"]
+           "gemm_f16.hip", "decode_operand.hip", "quantize_variant.hip"]
 
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 HIPCC = os.path.join(ROCM, "bin", "hipcc")

@@ -183,6 +183,56 @@ int mixfp4_hadamard(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, int
                                                static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+bool valid_variant(int32_t block, unsigned candidates) {
+  return (block == 8 || block == 16 || block == 32 || block == 64) && candidates >= 1u &&
+         candidates <= 7u;
+}
+}  // namespace
+
+int mixfp4_quantize_variant(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx, int32_t block,
+                            unsigned candidates, uint8_t* codes, uint8_t* scales, uint8_t* fmt,
+                            float* tensor_scale, unsigned flags, void* stream) {
+  if ((flags & ~MIXFP4_SCALE_GIVEN) != 0u || candidates < 1u || candidates > 7u)
+    return MIXFP4_ERR_FLAGS;
+  if (!valid_variant(block, candidates)) return MIXFP4_ERR_SHAPE;
+  if (rows < 0 || k < 0 || (k % block) != 0) return MIXFP4_ERR_SHAPE;
+  if (rows > 0 && (ldx < k || (ldx % 8) != 0)) return MIXFP4_ERR_SHAPE;
+  if (!tensor_scale) return MIXFP4_ERR_NULL;
+  if (!aligned(tensor_scale, 4)) return MIXFP4_ERR_ALIGN;
+  const bool empty = rows == 0 || k == 0;
+  const bool three = candidates == 7u;
+  if (!empty && (!x || !codes || !scales || (three && !fmt))) return MIXFP4_ERR_NULL;
+  if (!empty && (!aligned(x, 16) || !aligned(codes, 16))) return MIXFP4_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  if ((flags & MIXFP4_SCALE_GIVEN) == 0u) {
+    const int st = launch_status(mixfp4::launch_tensor_scale(
+        x, empty ? 0 : rows, k, ldx, empty ? nullptr : scales, empty ? 0 : rows * (k / block),
+        tensor_scale, s));
+    if (st != MIXFP4_OK) return st;
+  }
+  if (empty) return MIXFP4_OK;
+  return launch_status(mixfp4::launch_quantize_variant(x, rows, k, ldx, block, candidates, codes,
+                                                       scales, fmt, tensor_scale, s));
+}
+
+int mixfp4_dequantize_variant(const uint8_t* codes, const uint8_t* scales, const uint8_t* fmt,
+                              const float* tensor_scale, int64_t rows, int64_t k, int32_t block,
+                              unsigned candidates, float* out, void* stream) {
+  if (candidates < 1u || candidates > 7u) return MIXFP4_ERR_FLAGS;
+  if (!valid_variant(block, candidates)) return MIXFP4_ERR_SHAPE;
+  if (rows < 0 || k < 0 || (k % block) != 0) return MIXFP4_ERR_SHAPE;
+  if (rows == 0 || k == 0) return MIXFP4_OK;
+  if (!codes || !scales || !out || (candidates == 7u && !fmt)) return MIXFP4_ERR_NULL;
+  if (!aligned(codes, 16) || !aligned(out, 16)) return MIXFP4_ERR_ALIGN;
+  if (tensor_scale && !aligned(tensor_scale, 4)) return MIXFP4_ERR_ALIGN;
+  (void)hipGetLastError();
+  return launch_status(mixfp4::launch_dequantize_variant(codes, scales, fmt, tensor_scale, rows, k,
+                                                         block, candidates, out,
+                                                         static_cast<hipStream_t>(stream)));
+}
+
 int mixfp4_dequantize(const uint8_t* codes, const uint8_t* scales, const float* tensor_scale,
                       int64_t rows, int64_t k, float* out, void* stream) {
   if (rows < 0 || k < 0 || (k % mixfp4::kBlock) != 0) return MIXFP4_ERR_SHAPE;

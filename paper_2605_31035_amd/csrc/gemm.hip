@@ -317,7 +317,6 @@ __device__ __forceinline__ void skinny_body(
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c, BeforeA before_a) {
-  constexpr int kCols = 16 * kCG;
   __shared__ f32x4 red[kW - 1][kCG][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nn = lane & 15, g = lane >> 4;

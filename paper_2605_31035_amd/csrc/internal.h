@@ -157,6 +157,17 @@ hipError_t launch_decode_step(const uint16_t* x, int64_t m, int64_t k, const uin
                               const uint8_t* w_scales, const float* w_ts, int64_t n,
                               uint8_t* a_codes, uint8_t* a_scales, float* a_ts, float* c,
                               uint32_t* sync, hipStream_t stream);
+// Algorithm 1's selection over the candidate set `set` (bit 0 E2M1, bit 1
+// E1M2 x2, bit 2 E3M0) with blocks of `block` (8, 16, 32, 64) elements along
+// K; scales [rows, k/block] (T in bit 7 for two candidates), fmt [rows,
+// k/block] the chosen index (may be NULL); s32 read from *tensor_scale.
+hipError_t launch_quantize_variant(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                                   int block, unsigned set, uint8_t* codes, uint8_t* scales,
+                                   uint8_t* fmt, const float* tensor_scale, hipStream_t stream);
+hipError_t launch_dequantize_variant(const uint8_t* codes, const uint8_t* scales,
+                                     const uint8_t* fmt, const float* tensor_scale, int64_t rows,
+                                     int64_t k, int block, unsigned set, float* out,
+                                     hipStream_t stream);
 // The library's static workspace (mixfp4_gemm_noalloc): kStaticScratchBytes
 // of device memory per GPU; *ptr receives its device address on the current
 // device (looked up once per device).

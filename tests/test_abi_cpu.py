@@ -311,3 +311,44 @@ def test_decode_step_applies_rule():
     import paper_2605_31035_amd as M
     assert M.decode_step_applies(16, 8192) and M.decode_step_applies(1, 512)
     assert not M.decode_step_applies(17, 8192) and not M.decode_step_applies(16, 768)
+
+
+def test_quantize_variant_rejects(lib):
+    """mixfp4_quantize_variant / mixfp4_dequantize_variant argument checks,
+    all before any device access."""
+    f = lib.mixfp4_quantize_variant
+
+    def qv(**kw):
+        return f(kw.get("x", A16), kw.get("rows", 2), kw.get("k", 64), kw.get("ldx", 64),
+                 kw.get("block", 32), kw.get("cand", 5), kw.get("codes", A16),
+                 kw.get("scales", A16), kw.get("fmt", A16), kw.get("ts", A16),
+                 kw.get("flags", 0), None)
+
+    assert qv(block=24) == 2 and qv(block=128) == 2 and qv(block=0) == 2
+    assert qv(cand=0) == 4 and qv(cand=8) == 4
+    assert qv(flags=2) == 4 and qv(flags=8) == 4
+    assert qv(k=48) == 2                            # k % block
+    assert qv(rows=-1) == 2 and qv(ldx=32) == 2 and qv(ldx=68) == 2
+    assert qv(ts=P(0)) == 1 and qv(x=P(0)) == 1 and qv(codes=P(0)) == 1
+    assert qv(scales=P(0)) == 1
+    assert qv(cand=7, fmt=P(0)) == 1                # three candidates need the index array
+    assert qv(x=P(0x10008)) == 3 and qv(codes=P(0x10008)) == 3 and qv(ts=P(0x10002)) == 3
+    d = lib.mixfp4_dequantize_variant
+    assert d(A16, A16, A16, None, 2, 64, 24, 5, A16, None) == 2
+    assert d(A16, A16, A16, None, 2, 64, 32, 0, A16, None) == 4
+    assert d(A16, A16, A16, None, 2, 48, 32, 5, A16, None) == 2
+    assert d(A16, A16, P(0), None, 2, 64, 32, 7, A16, None) == 1
+    assert d(P(0), A16, A16, None, 2, 64, 32, 5, A16, None) == 1
+    assert d(A16, A16, A16, None, 2, 64, 32, 5, A4, None) == 3
+    assert d(P(0), P(0), P(0), None, 0, 64, 32, 5, P(0), None) == 0    # empty
+
+
+def test_binding_variant_rejects():
+    import torch
+
+    import paper_2605_31035_amd as M
+    x = torch.zeros((2, 64), dtype=torch.bfloat16)
+    for kw in (dict(block=24), dict(candidates=()), dict(candidates=("e2m1", "e2m1")),
+               dict(candidates=("e4m3",)), dict(block=128)):
+        with pytest.raises(ValueError):
+            M.mixfp4_quantize_variant(x, **kw)
