@@ -507,14 +507,19 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
     torch.cuda.synchronize()
     nspan = 2 + 2 * len(wnames)
 
+    fused_a = any(two.values())
+
     def step(e=None):
         if e is not None:
             e[0].record()
-        M.mixfp4_quantize(x["A"], None, qa[0], qa[1], scale_out=qa[2])
+        if fused_a:
+            # A quantized and decoded for the two-pass GEMMs in one pass
+            M.mixfp4_quantize_decode(x["A"], None, out=da.buf, codes=qa[0], scales=qa[1],
+                                     scale_out=qa[2])
+        else:
+            M.mixfp4_quantize(x["A"], None, qa[0], qa[1], scale_out=qa[2])
         if e is not None:
             e[1].record()
-        if any(two.values()):
-            M.mixfp4_decode_operand(qa, out=da.buf)
         for i, w in enumerate(wnames):
             if e is not None:
                 e[2 + 2 * i].record()
@@ -544,7 +549,6 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
     torch.cuda.synchronize()
     span = lambda a, b: float(np.mean([m[a].elapsed_time(m[b]) for m in marks]))  # noqa: E731
     q_ms = span(0, 1)
-    da_ms = span(1, 2)
     gemms = {}
     total_flops = 0.0
 
@@ -599,16 +603,23 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
            "gemm_flops_per_step": total_flops,
            "path_rule": "two passes where m n / (m + n) >= 2048 (gemm_two_pass_preferred), "
                         "else the fused kernel",
-           "quantize_a": {"what": f"A[{ra},{ka}] with the tensor scale computed on the device "
-                                  "(amax pass + reduction + quantize kernel)",
-                          "us": round(q_ms * 1e3, 2),
-                          "GBps": round(ra * ka * QUANT_BYTES_PER_ELEM / (q_ms * 1e-3) / 1e9, 1),
-                          "bytes_per_elem": QUANT_BYTES_PER_ELEM},
+           "quantize_a": ({"what": f"A[{ra},{ka}] quantized and decoded for the two-pass GEMM "
+                                   "in one pass (mixfp4_quantize_decode: amax pass + reduction + "
+                                   "quantize_decode_kernel), tensor scale computed on the device",
+                           "us": round(q_ms * 1e3, 2),
+                           "GBps": round(ra * ka * (QUANT_BYTES_PER_ELEM + 2.0) / (q_ms * 1e-3)
+                                         / 1e9, 1),
+                           "bytes_per_elem": QUANT_BYTES_PER_ELEM + 2.0,
+                           "bytes_note": "2 B read + 0.5625 B of codes and scales + 2 B of "
+                                         "decoded operand written (the amax pass's read of A "
+                                         "is not counted)"}
+                          if fused_a else
+                          {"what": f"A[{ra},{ka}] with the tensor scale computed on the device "
+                                   "(amax pass + reduction + quantize kernel)",
+                           "us": round(q_ms * 1e3, 2),
+                           "GBps": round(ra * ka * QUANT_BYTES_PER_ELEM / (q_ms * 1e-3) / 1e9, 1),
+                           "bytes_per_elem": QUANT_BYTES_PER_ELEM}),
            "gemms": gemms}
-    if any(two.values()):
-        out["decode_a"] = {"kernel": "decode_blocked_kernel", "us": round(da_ms * 1e3, 2),
-                           "bytes": ra * ka * (0.5 + 1 / 16 + 2),
-                           "GBps": round(ra * ka * (0.5 + 1 / 16 + 2) / (da_ms * 1e-3) / 1e9, 1)}
     del x, qw, qa, outs, da, dws
     torch.cuda.empty_cache()
     return out
@@ -677,9 +688,9 @@ def main():
         out["config"] = {
             "workload": "large (seed 4): quantize A[16384,8192] (block mixture: 90% of "
                         "16-blocks N(0,0.1), 10% Laplace(0,1) with one x40 spike; tensor scale "
-                        "computed on the device), decode A and W once to exact 16-bit values, "
-                        "then C = A W^T [16384,8192] fp32; W[8192,8192] N(0,0.02) quantized "
-                        "before timing (its decode is inside the step)",
+                        "computed on the device) and decode it to exact 16-bit values in the "
+                        "same pass, decode W, then C = A W^T [16384,8192] fp32; W[8192,8192] "
+                        "N(0,0.02) quantized before timing (its decode is inside the step)",
             "seed": 4, "gemm_flops_per_step": r["gemm_flops_per_step"],
             "quantized_elements_per_step": 16384 * 8192, "spin_up_s": args.spin_up,
             "timing": "value: K steps back to back, wall clock between device "
@@ -696,9 +707,9 @@ def main():
                            "flops_per_launch": g["flops"],
                            "us_per_launch": g["us_per_launch"]}
         out["quantize_step"] = r["quantize_a"]
-        out["decode_step"] = {"decode_a": r["decode_a"],
-                              "decode_w_us": g["decode_w_us"], "decode_w_GBps": g["decode_w_GBps"],
-                              "bound": "hbm", "bytes_per_elem": 0.5 + 1 / 16 + 2}
+        out["decode_w"] = {"kernel": "decode_blocked_kernel", "us": g["decode_w_us"],
+                           "GBps": g["decode_w_GBps"], "bound": "hbm",
+                           "bytes_per_elem": 0.5 + 1 / 16 + 2}
         out["gemm_call"] = {"what": "decode W + GEMM (the mixfp4_gemm_ws work for an operand "
                                     "decoded once) in the step, and both paths back to back",
                             "path": g["path"], "us": g["gemm_call_us"],

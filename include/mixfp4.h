@@ -365,6 +365,29 @@ int mixfp4_gemm_decoded(const void *a_decoded, const float *a_tensor_scale,
                         const void *w_decoded, const float *w_tensor_scale,
                         int64_t m, int64_t n, int64_t k, float *c, void *stream);
 
+/*
+ * mixfp4_quantize_decode - the activation's quantization fused with the first
+ * pass of the two-pass GEMM (the activation quantized on the fly before the
+ * block-scaled GEMM, Sec. 3.2 / Fig. 7): one pass over X writes its MixFP4
+ * codes, scales and tensor scale exactly as mixfp4_quantize does (Algorithm
+ * 1) and, in the same launch, the exact 16-bit decode of those codes in the
+ * layout mixfp4_decode_operand writes (Sec. 3.3, App. B.5), ready for
+ * mixfp4_gemm_decoded.  With MIXFP4_SCALE_COMPUTE the tensor scale takes one
+ * read of X before that pass.
+ *   x, rows, k, ldx, codes, scales, tensor_scale
+ *                  as for mixfp4_quantize, with k % 32 == 0 and k <= 2^22.
+ *   out, out_bytes the decoded operand: device memory of at least
+ *                  mixfp4_decode_operand's size for [rows, k], 256-byte
+ *                  aligned (padding rows beyond the next multiple of 32 are
+ *                  left unwritten).
+ *   flags          MIXFP4_SCALE_COMPUTE or MIXFP4_SCALE_GIVEN, optionally
+ *                  one format mode (MIXFP4_FORCE_E2M1, MIXFP4_FORCE_E1M2,
+ *                  MIXFP4_FOUR_SIX).
+ */
+int mixfp4_quantize_decode(const uint16_t *x, int64_t rows, int64_t k, int64_t ldx,
+                           uint8_t *codes, uint8_t *scales, float *tensor_scale,
+                           void *out, int64_t out_bytes, unsigned flags, void *stream);
+
 /* Human-readable name of a mixfp4_status value (static storage). */
 const char *mixfp4_status_string(int status);
 
@@ -406,7 +429,7 @@ const char *mixfp4_last_launch_error(void);
 /* ABI version of this header (major * 100 + minor). */
 int mixfp4_abi_version(void);
 
-#define MIXFP4_ABI_VERSION 108
+#define MIXFP4_ABI_VERSION 109
 
 #ifdef __cplusplus
 }

@@ -38,7 +38,7 @@ __all__ = ["mixfp4_decode_step", "decode_step_applies", "gemm_two_pass_preferred
            "FORCE_E2M1", "FORCE_E1M2", "STOCHASTIC", "TRANSPOSE", "mixfp4_quantize_2d",
            "mixfp4_gemm_workspace_size", "mixfp4_decode_operand", "mixfp4_gemm_decoded",
            "Decoded", "mixfp4_quantize_variant", "mixfp4_dequantize_variant", "Variant",
-           "CANDIDATES"]
+           "CANDIDATES", "mixfp4_quantize_decode"]
 
 SCALE_COMPUTE = 0
 SCALE_GIVEN = 1
@@ -448,6 +448,49 @@ class Decoded(NamedTuple):
     rows: int
     k: int
     s32: torch.Tensor | None
+
+
+def mixfp4_quantize_decode(x: torch.Tensor, tensor_scale: torch.Tensor | None = None,
+                           mode: str = "mixfp4", out: torch.Tensor | None = None,
+                           codes: torch.Tensor | None = None, scales: torch.Tensor | None = None,
+                           scale_out: torch.Tensor | None = None):
+    """Quantize a bf16 [rows, k] activation (Algorithm 1, as mixfp4_quantize)
+    and decode it for mixfp4_gemm_decoded in the same pass
+    (mixfp4_quantize_decode).  ``tensor_scale`` None computes s32 (into
+    ``scale_out`` if given).  Returns ((codes, scales, s32), Decoded)."""
+    if mode not in _MODES:
+        raise ValueError(f"mode must be one of {sorted(_MODES)}")
+    if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+        raise ValueError("x must be a 2-D bfloat16 CUDA tensor with unit stride along K")
+    rows, k = x.shape
+    if k % 32:
+        raise ValueError("k must be a multiple of 32 for the decoded GEMM")
+    dev = x.device
+    need = ctypes.c_int64(0)
+    _check(lib.mixfp4_decode_operand(None, None, rows, k, None, 0, ctypes.byref(need), None))
+    if out is None:
+        out = torch.empty(max(1, need.value), dtype=torch.uint8, device=dev)
+    if codes is None:
+        codes = torch.empty((rows, k // 2), dtype=torch.uint8, device=dev)
+    if scales is None:
+        scales = torch.empty((rows, k // 16), dtype=torch.uint8, device=dev)
+    _require(out, "out", torch.uint8)
+    _require(codes, "codes", torch.uint8, (rows, k // 2))
+    _require(scales, "scales", torch.uint8, (rows, k // 16))
+    if out.numel() < need.value:
+        raise ValueError(f"out must hold {need.value} bytes")
+    if tensor_scale is None:
+        ts = scale_out if scale_out is not None else torch.empty(1, dtype=torch.float32, device=dev)
+        flags = SCALE_COMPUTE
+    else:
+        ts, flags = tensor_scale, SCALE_GIVEN
+    _require(ts, "tensor_scale", torch.float32, numel=1)
+    _same_device(dev, ("x", x), ("codes", codes), ("scales", scales), ("tensor scale", ts),
+                 ("out", out))
+    _check(lib.mixfp4_quantize_decode(_ptr(x), rows, k, x.stride(0), _ptr(codes), _ptr(scales),
+                                      _ptr(ts), _ptr(out), out.numel(), flags | _MODES[mode],
+                                      _stream(dev)))
+    return (codes, scales, ts), Decoded(out, rows, k, ts)
 
 
 def mixfp4_decode_operand(q, out: torch.Tensor | None = None) -> Decoded:

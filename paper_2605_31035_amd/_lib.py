@@ -18,7 +18,7 @@ SYMBOLS = ("mixfp4_quantize", "mixfp4_quantize_ex", "mixfp4_quantize_2d", "mixfp
            "mixfp4_gemm", "mixfp4_gemm_ws", "mixfp4_gemm_workspace_size",
            "mixfp4_decode_operand", "mixfp4_gemm_decoded", "mixfp4_gemm_noalloc",
            "mixfp4_gemm_noalloc_max_bytes", "mixfp4_decode_step",
-           "mixfp4_quantize_variant", "mixfp4_dequantize_variant",
+           "mixfp4_quantize_variant", "mixfp4_dequantize_variant", "mixfp4_quantize_decode",
            "mixfp4_status_string", "mixfp4_last_launch_error", "mixfp4_abi_version")
 
 
@@ -62,6 +62,8 @@ def load(path: str = LIB_PATH) -> ctypes.CDLL:
     h.mixfp4_quantize_variant.restype = i32
     h.mixfp4_dequantize_variant.argtypes = [vp, vp, vp, vp, i64, i64, i32, u32, vp, vp]
     h.mixfp4_dequantize_variant.restype = i32
+    h.mixfp4_quantize_decode.argtypes = [vp, i64, i64, i64, vp, vp, vp, vp, i64, u32, vp]
+    h.mixfp4_quantize_decode.restype = i32
     h.mixfp4_gemm_noalloc_max_bytes.argtypes = []
     h.mixfp4_gemm_noalloc_max_bytes.restype = i64
     h.mixfp4_status_string.argtypes = [i32]

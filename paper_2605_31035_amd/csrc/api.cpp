@@ -360,6 +360,34 @@ int mixfp4_decode_operand(const uint8_t* codes, const uint8_t* scales, int64_t r
                                                      static_cast<hipStream_t>(stream)));
 }
 
+int mixfp4_quantize_decode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                           uint8_t* codes, uint8_t* scales, float* tensor_scale, void* out,
+                           int64_t out_bytes, unsigned flags, void* stream) {
+  if ((flags & ~(MIXFP4_SCALE_GIVEN | kModeFlags)) != 0u || format_mode(flags) < 0)
+    return MIXFP4_ERR_FLAGS;
+  if (rows < 0 || k < 0 || (k % 32) != 0 || k > (int64_t(1) << 22)) return MIXFP4_ERR_SHAPE;
+  if (rows > 0 && (ldx < k || (ldx % 8) != 0)) return MIXFP4_ERR_SHAPE;
+  if (!tensor_scale) return MIXFP4_ERR_NULL;
+  if (!aligned(tensor_scale, 4)) return MIXFP4_ERR_ALIGN;
+  const bool empty = rows == 0 || k == 0;
+  if (!empty && (!x || !codes || !scales || !out)) return MIXFP4_ERR_NULL;
+  if (!empty && out_bytes < mixfp4::decoded_bytes(rows, k)) return MIXFP4_ERR_SHAPE;
+  if (!empty && (!aligned(x, 16) || !aligned(codes, 16) || !aligned(out, 256)))
+    return MIXFP4_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  (void)hipGetLastError();
+  if ((flags & MIXFP4_SCALE_GIVEN) == 0u) {
+    const int st = launch_status(mixfp4::launch_tensor_scale(
+        x, empty ? 0 : rows, k, ldx, empty ? nullptr : scales,
+        empty ? 0 : rows * (k / mixfp4::kBlock), tensor_scale, s));
+    if (st != MIXFP4_OK) return st;
+  }
+  if (empty) return MIXFP4_OK;
+  return launch_status(mixfp4::launch_quantize_decode(x, rows, k, ldx, codes, scales, tensor_scale,
+                                                      format_mode(flags),
+                                                      static_cast<uint8_t*>(out), s));
+}
+
 int mixfp4_gemm_decoded(const void* a_decoded, const float* a_tensor_scale,
                         const void* w_decoded, const float* w_tensor_scale, int64_t m, int64_t n,
                         int64_t k, float* c, void* stream) {

@@ -145,6 +145,13 @@ hipError_t launch_gemm_two_pass(const uint8_t* a_codes, const uint8_t* a_scales,
 int64_t decoded_bytes(int64_t rows, int64_t k);
 hipError_t launch_decode_blocked(const uint8_t* codes, const uint8_t* scales, int64_t rows,
                                  int64_t k, uint8_t* out, hipStream_t stream);
+// Quantization of X [rows, k] (k % 32 == 0; s32 given on the device; `mode`
+// a format mode of quant_block.h) fused with its decode into the blocked
+// layout `out` (decoded_bytes(rows, k) bytes): codes and scales as
+// launch_quantize writes them.
+hipError_t launch_quantize_decode(const uint16_t* x, int64_t rows, int64_t k, int64_t ldx,
+                                  uint8_t* codes, uint8_t* scales, const float* tensor_scale,
+                                  int mode, uint8_t* out, hipStream_t stream);
 hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uint8_t* wblk,
                                const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
                                hipStream_t stream);

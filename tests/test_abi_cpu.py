@@ -352,3 +352,18 @@ def test_binding_variant_rejects():
                dict(candidates=("e4m3",)), dict(block=128)):
         with pytest.raises(ValueError):
             M.mixfp4_quantize_variant(x, **kw)
+
+
+def test_quantize_decode_rejects(lib):
+    f = lib.mixfp4_quantize_decode
+
+    def qd(**kw):
+        return f(kw.get("x", A16), kw.get("rows", 2), kw.get("k", 64), kw.get("ldx", 64),
+                 kw.get("codes", A16), kw.get("scales", A16), kw.get("ts", A16),
+                 kw.get("out", P(0x10000)), kw.get("out_bytes", 1 << 20), kw.get("flags", 0), None)
+
+    assert qd(flags=8) == 4 and qd(flags=6) == 4 and qd(flags=16) == 4
+    assert qd(k=48) == 2 and qd(k=1 << 23) == 2 and qd(rows=-1) == 2 and qd(ldx=32) == 2
+    assert qd(out_bytes=100) == 2                   # smaller than the decoded layout
+    assert qd(ts=P(0)) == 1 and qd(x=P(0)) == 1 and qd(out=P(0)) == 1 and qd(codes=P(0)) == 1
+    assert qd(out=P(0x10010)) == 3 and qd(x=P(0x10008)) == 3 and qd(ts=P(0x10002)) == 3

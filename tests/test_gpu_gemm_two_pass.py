@@ -180,3 +180,52 @@ def test_decoded_k_zero_and_empty():
     out = torch.full((4, 3), 7.0, device="cuda")
     M.mixfp4_gemm_decoded(da, dw, out=out)
     assert torch.all(out == 0)
+
+
+def _valid_rows(dec, rows, k):
+    """The bytes of rows [0, rows) of a decoded operand (blocked layout: 256-row
+    tiles x 32-K steps of 16 KB, 64 bytes per row and step)."""
+    steps = k // 32
+    b = dec.buf[: ((rows + 255) // 256) * steps * 16384].view(-1, steps, 256, 64)
+    return b.permute(0, 2, 1, 3).reshape(-1, steps * 64)[:rows]
+
+
+@pytest.mark.parametrize("rows,k,mode,given,pad", [
+    (1, 32, "mixfp4", False, 0), (33, 96, "mixfp4", True, 0), (300, 288, "mixfp4", False, 8),
+    (257, 1024, "e2m1", False, 0), (70, 512, "e1m2", True, 64), (129, 256, "four_six", False, 0),
+    (2048, 4096, "mixfp4", False, 0)])
+def test_quantize_decode_fused(rows, k, mode, given, pad):
+    """mixfp4_quantize_decode: codes, scales and s32 equal mixfp4_quantize's
+    (and the oracle's) bit for bit, the decoded operand equals
+    mixfp4_decode_operand's on every real row, and a GEMM on it stays within
+    the oracle's tolerance."""
+    import paper_2605_31035_amd as M
+    from tests._gpu import dev_bf16
+    bits = W.prefill_7b().tensors["A"] if rows == 2048 else W.adversarial(rows + k, rows, k)
+    log(f"quantize+decode rows={rows} k={k} mode={mode} given={given} pad={pad}")
+    x = dev_bf16(bits)
+    if pad:
+        big = torch.zeros((rows, k + pad), dtype=torch.bfloat16, device="cuda")
+        big[:, :k] = x
+        x = big[:, :k]
+    s32 = dev_f32(np.float32(0.37)) if given else None
+    (codes, scales, ts), dec = M.mixfp4_quantize_decode(x, s32, mode=mode)
+    rc, rs, rt = M.mixfp4_quantize(x, s32, mode=mode)
+    torch.cuda.synchronize()
+    assert torch.equal(codes, rc) and torch.equal(scales, rs) and torch.equal(ts, rt)
+    if rows <= 300:
+        ref = Q.quantize(bits, s32=np.float32(0.37) if given else None,
+                         mode={"mixfp4": "select"}.get(mode, mode))
+        np.testing.assert_array_equal(host(codes), ref.codes)
+        np.testing.assert_array_equal(host(scales), ref.scales)
+    dref = M.mixfp4_decode_operand((codes, scales, ts))
+    assert torch.equal(_valid_rows(dec, rows, k), _valid_rows(dref, rows, k))
+    n = 96
+    qw = Q.quantize(W.adversarial(n + 1, n, k))
+    dw = M.mixfp4_decode_operand(_dev(qw))
+    c = M.mixfp4_gemm_decoded(dec, dw)
+    assert torch.equal(c, M.mixfp4_gemm_decoded(dref, dw))
+    qa = Q.Quantized(codes=host(codes), scales=host(scales), s32=host(ts)[0], t=None,
+                     sf_code=None, si_code=None, delta=None)
+    rr = np.unique(np.concatenate([[0, rows - 1], np.random.default_rng(rows).integers(0, rows, 64)]))
+    _check(host(c), qa, qw, rows=rr, cols=np.arange(n))
