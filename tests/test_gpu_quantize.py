@@ -217,6 +217,41 @@ def test_workload_full_size(name, tensors):
         log(f"{name}.{tname} ok; E1M2 share {ref.t.mean():.3f}")
 
 
+@pytest.mark.parametrize("tie_share", [1.0, 0.5])
+def test_many_undecided_blocks(tie_share):
+    """Blocks with one nonzero element +-42 * 2^e: E2M1 under the scale 7 * 2^e
+    and INT4 under 6 * 2^e both hold it exactly, so the two errors tie and only
+    the exact decision settles the block (T = 1).  A 6144 x 4096 tensor of
+    them (half of them among random blocks at tie_share 0.5): every wave of
+    the streaming quantizer takes its exact path, many times over.  s32 given
+    (1) and computed (672 / 2688 = 1/4 keeps the ties); codes and scales on
+    sampled rows."""
+    rng = np.random.default_rng(11)
+    rows, k = 6144, 4096
+    nb = rows * k // 16
+    x = np.zeros((nb, 16), np.float32)
+    tie = rng.random(nb) < tie_share
+    val = 42.0 * np.exp2(rng.integers(-4, 5, nb)) * np.where(rng.random(nb) < 0.5, -1.0, 1.0)
+    x[np.arange(nb), rng.integers(0, 16, nb)] = np.where(tie, val, 0.0)
+    x[~tie] = rng.standard_normal((int((~tie).sum()), 16)) * 3.0
+    tie[0] = True                                   # block 0 holds the tensor maximum
+    x[0] = 0.0
+    x[0, 0] = 672.0                                 # 42 * 16; s32 = 672 / 2688 = 1/4
+    bits = W.f32_to_bf16_bits(x.reshape(rows, k))
+    for s32 in (1.0, None):
+        log(f"undecided blocks tie_share={tie_share} s32={s32}")
+        codes, scales, s = gpu_quantize(bits, s32)
+        s_ref = np.float32(s32) if s32 is not None else Q.tensor_scale(bits)
+        assert s_ref == np.float32(1.0 if s32 is not None else 0.25)
+        assert host(s)[0] == s_ref
+        sample = _sampled_rows(rng, rows, 48)
+        ref = Q.quantize(bits[sample], s32=s_ref)
+        idx = torch.from_numpy(sample).to("cuda")
+        np.testing.assert_array_equal(host(scales.index_select(0, idx)), ref.scales)
+        np.testing.assert_array_equal(host(codes.index_select(0, idx)), ref.codes)
+        assert (ref.delta[tie.reshape(rows, k // 16)[sample]] == 0).all()
+
+
 def test_four_six_ties_and_full_size():
     """4/6 on blocks where both candidates are exact (ties keep max/6), and
     on the full 7B-class prefill activation (sampled rows)."""
