@@ -277,8 +277,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 //
 // A workgroup owns 16 kCG columns of C (kCG = 1 to 4 MFMA column groups),
 // or two such ranges one after the other (4 + 1 .. 4 + 4 groups, so that one
-// workgroup per CU covers W), and splits K over its kW waves (4, or 2 when k
-// is not a multiple of 1024);
+// workgroup per CU covers W), and splits K (k % 256 == 0) over its kW waves
+// in whole 256-wide steps (skinny_waves: 2 equal shares when k / 256 is 2 mod
+// 4, else 4 shares that differ by at most one step);
 // each wave walks its K range in steps of 256 with no barrier and no LDS
 // until the end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
 // nn + 16 c (c < kCG, one per 16-column group) and the quarter
@@ -321,9 +322,12 @@ __device__ __forceinline__ void skinny_body(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nn = lane & 15, g = lane >> 4;
   const int64_t code_pitch = k / 2, scale_pitch = k / kBlock;
-  const int64_t kq = k / kW;                        // this wave's K range
-  const int64_t steps = kq / kSkinnyStep;
-  const int64_t kbase = wave * kq;
+  // this wave's K range: steps [S w / kW, S (w + 1) / kW) of the S = k / 256
+  // (an equal share when kW divides S; a wave may have none when S < kW)
+  const int64_t total_steps = k / kSkinnyStep;
+  const int64_t s_first = total_steps * wave / kW;
+  const int64_t steps = total_steps * (wave + 1) / kW - s_first;
+  const int64_t kbase = s_first * kSkinnyStep;
   const uint8_t* wc[kCG];
   const uint8_t* ws[kCG];
 #pragma unroll
@@ -390,9 +394,9 @@ __device__ __forceinline__ void skinny_body(
   // are in flight.
   WPack<kCG> wp[2];
   APack ap[2];
-  load_w(wp[0], 0);
-  const bool a_ok = before_a();
-  load_a(ap[0], 0);
+  if (steps > 0) load_w(wp[0], 0);
+  const bool a_ok = before_a();                     // every wave: it may synchronize
+  if (steps > 0) load_a(ap[0], 0);
   auto step = [&](auto I_, int64_t s) {
     constexpr int I = decltype(I_)::value;
     __builtin_amdgcn_sched_barrier(0);
@@ -627,12 +631,19 @@ hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   return hipGetLastError();
 }
 
+// Waves splitting K in the decode-shape kernel: 2 when k / 256 is even but
+// not a multiple of 4 (equal shares, as measured best), else 4 (equal shares
+// when k % 1024 == 0, otherwise shares differing by one 256-wide step).
+inline int skinny_waves(int64_t k) {
+  return (k % (4 * kSkinnyStep) != 0 && k % (2 * kSkinnyStep) == 0) ? 2 : 4;
+}
+
 template <int kA, int kB>
 hipError_t launch_skinny(const uint8_t* a_codes, const uint8_t* a_scales, const float* a_ts,
                          const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
                          int64_t m, int64_t n, int64_t k, float* c, hipStream_t stream) {
   const unsigned groups = (unsigned)((n + 16 * (kA + kB) - 1) / (16 * (kA + kB)));
-  if (k % (4 * kSkinnyStep) == 0)
+  if (skinny_waves(k) == 4)
     gemm_skinny_kernel<4, kA, kB><<<groups, 256, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
                                                               w_scales, w_ts, m, n, k, c);
   else
@@ -648,7 +659,7 @@ hipError_t launch_step(const uint16_t* x, uint8_t* a_codes, uint8_t* a_scales, f
                        hipStream_t stream) {
   const int64_t groups = (n + 16 * (kA + kB) - 1) / (16 * (kA + kB));
   const int producers = (int)(groups < kStepProducers ? groups : kStepProducers);
-  if (k % (4 * kSkinnyStep) == 0)
+  if (skinny_waves(k) == 4)
     decode_step_kernel<4, kA, kB><<<(unsigned)groups, 256, 0, stream>>>(
         x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, producers);
   else
@@ -686,7 +697,7 @@ hipError_t by_column_split(int64_t n, Launch launch) {
 }  // namespace
 
 bool decode_step_applies(int64_t m, int64_t k) {
-  return m >= 1 && m <= kSkinnyRows && k > 0 && k % (2 * kSkinnyStep) == 0;
+  return m >= 1 && m <= kSkinnyRows && k > 0 && k % kSkinnyStep == 0;
 }
 
 hipError_t launch_decode_step(const uint16_t* x, int64_t m, int64_t k, const uint8_t* w_codes,
@@ -710,12 +721,11 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     fill_zero<<<(int)g, 256, 0, stream>>>(c, m * n);
     return hipGetLastError();
   }
-  // decode shape: 4 waves split K when k % 1024 == 0, else 2 when k % 512 == 0
-  // (each wave's range a whole number of 256-wide steps); scale loads are
-  // 4-byte words
+  // decode shape: the waves split K in whole 256-wide steps (skinny_waves);
+  // scale loads are 4-byte words
   const bool skinny_aligned = ((reinterpret_cast<uintptr_t>(w_scales) |
                                 reinterpret_cast<uintptr_t>(a_scales)) & 3u) == 0;
-  if (m <= kSkinnyRows && skinny_aligned && k % (2 * kSkinnyStep) == 0) {
+  if (m <= kSkinnyRows && skinny_aligned && k % kSkinnyStep == 0) {
     return by_column_split(n, [&](auto A, auto B) {
       return launch_skinny<decltype(A)::value, decltype(B)::value>(
           a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);

@@ -72,10 +72,13 @@ def test_ragged_shapes(m, n, k):
 @pytest.mark.parametrize("m,n,k", [(1, 1, 512), (5, 127, 1024), (16, 129, 512), (9, 1000, 2048),
                                    (16, 256, 8192), (3, 300, 1536), (16, 6150, 1024),
                                    (2, 7000, 1536), (16, 10250, 2048), (7, 10256, 512),
-                                   (16, 12300, 1024)])
+                                   (16, 12300, 1024), (1, 33, 256), (16, 500, 768),
+                                   (4, 1300, 1280), (16, 1100, 11008), (13, 9000, 2816)])
 def test_decode_shapes(m, n, k):
-    """m <= 16 with k % 512 == 0 takes the decode-shape kernel (K split over 4
-    waves when k % 1024 == 0, else over 2; odd and single step counts), with
+    """m <= 16 with k % 256 == 0 takes the decode-shape kernel: K split over
+    4 waves in equal shares (k % 1024 == 0) or in shares that differ by one
+    256-wide step (k / 256 odd or 1 mod 4 or 3 mod 4: 1, 3, 5, 43, 11 steps;
+    fewer steps than waves leave waves idle), over 2 when k / 256 is 2 mod 4;
     16, 32, 48 or 64 columns per workgroup (n up to 4096, 8192, 12288, above),
     ragged last column groups included."""
     a = W.adversarial(7 * m + k, m, k)
