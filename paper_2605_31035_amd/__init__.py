@@ -322,12 +322,13 @@ def gemm_two_pass_preferred(m: int, n: int, k: int) -> bool:
     GEMM) is expected to beat the fused kernel for C[m, n] = A W^T: the
     decode costs (m + n) k elements of HBM traffic, the faster GEMM saves a
     share of 2 m n k flops, so it pays off from m n / (m + n) on.  Measured
-    on MI355X (decode included): 16384x8192x8192 1717 against 1956 us and
-    4096x14336x4096 429 against 464 us favour two passes, 2048x11008x4096
-    (220 against 203 us) and 2048x4096x4096 (103 against 84 us) the fused
-    kernel; the threshold 2048 lies between them."""
+    on MI355X (decode of W included): 16384x8192x8192 1626 against 1990 us,
+    4096x14336x4096 408 against 470 us and 2048x11008x4096 (m n / (m + n) =
+    1727) 189 against 225 us favour two passes; 2048x4096x4096 (1365) is a
+    toss-up (86.6 against 90.7 us on one box, 85.5 against 83.9 on another)
+    and smaller products favour the fused kernel.  Threshold: 1536."""
     m, n, k = int(m), int(n), int(k)
-    return mixfp4_gemm_workspace_size(m, n, k) > 0 and m * n >= 2048 * (m + n)
+    return mixfp4_gemm_workspace_size(m, n, k) > 0 and m * n >= 1536 * (m + n)
 
 
 def mixfp4_gemm(a, w, out: torch.Tensor | None = None, workspace=None) -> torch.Tensor:

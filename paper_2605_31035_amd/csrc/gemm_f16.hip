@@ -208,6 +208,154 @@ __global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restr
 }
 
 
+// The same GEMM on 128 x 256 tiles, for the columns of a short last round
+// of 256 x 256 tiles (launch_gemm_decoded): a tile does half the work, so the
+// columns left after the whole rounds fill one round of 128 x 256 tiles in
+// half a tile time.  Wave w computes rows 64 (w / 2) and columns 128 (w % 2)
+// of the tile as 2 x 4 MFMA tiles; an A tile is one half (8 KB, contiguous)
+// of each 256-row step block.  Each step's 24 KB are 24 loads of 1 KB, six
+// per wave, spread one per four MFMAs; the pipeline, stages and barriers are
+// those of gemm_f16_kernel, and every output sums its K steps in the same
+// order, so C is bit-identical to the 256 x 256 tiles'.
+constexpr int kHalfRows = 128;
+constexpr int kHalfStageBytes = kBlkBytes / 2 + kBlkBytes;       // A half block, W block
+
+__global__ __launch_bounds__(256, 1) void gemm_f16_half_kernel(
+    const uint8_t* __restrict__ ablk, const uint8_t* __restrict__ wblk,
+    const float* __restrict__ a_ts, const float* __restrict__ w_ts, int64_t m, int64_t n,
+    int64_t k, float* __restrict__ c, int64_t ldc) {
+  typedef _Float16 f16x8v __attribute__((ext_vector_type(8)));
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kStages * kHalfStageBytes];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t steps = k / kStepK;
+  // both halves of every 256-row block of A (the blocked layout pads the
+  // rows to 256; a half past m reads padding and stores nothing)
+  const int64_t ntm = 2 * ((m + kTileRows - 1) / kTileRows), ntn = (n + kTileRows - 1) / kTileRows;
+  const int64_t tile = grouped_tile(xcd_item(blockIdx.x, gridDim.x), ntm, ntn);
+  const int64_t tm = tile / ntn, tn = tile % ntn;
+
+  // part q (0-23) of a step: q < 8 is KB q of the A tile's half block, else
+  // KB q - 8 of the W block; wave w issues parts 6 w .. 6 w + 5
+  const i32x4 rsrc_a = make_rsrc(ablk + (tm >> 1) * steps * kBlkBytes, (uint32_t)(steps * kBlkBytes));
+  const i32x4 rsrc_w = make_rsrc(wblk + tn * steps * kBlkBytes, (uint32_t)(steps * kBlkBytes));
+  const int a_half = (int)(tm & 1) * (kBlkBytes / 2);
+  auto issue = [&](int stage, int64_t st, int j) {
+    const int q = 6 * wave + j;
+    const bool is_a = q < 8;
+    const int lofs = is_a ? q * 1024 : kBlkBytes / 2 + (q - 8) * 1024;
+    const int gofs = (int)(st * kBlkBytes) + (is_a ? a_half + q * 1024 : (q - 8) * 1024);
+    auto* l = (__attribute__((address_space(3))) uint32_t*)(uintptr_t)(
+        reinterpret_cast<uintptr_t>(lds) + stage * kHalfStageBytes + lofs);
+    raw_buffer_load_lds(is_a ? rsrc_a : rsrc_w, l, 16, lane * 16, gofs, 0, 0);
+  };
+
+  const int wm = (wave >> 1) * 64, wn = (wave & 1) * 128;
+  const int half = lane >> 5, lrow = lane & 31;
+  f32x16 acc[2][4];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int q = 0; q < 16; ++q) acc[i][j][q] = 0.0f;
+
+  // Fragments of one 16-K slice: 2 A and 4 W 32-row tiles.  The A half
+  // block's rows keep their swizzle (128 is a multiple of 16).
+  struct Frags {
+    f16x8v a[2], w[4];
+  };
+  auto read_a = [&](Frags& f, int stage, int sl, int cc) {
+    const uint8_t* b = lds + stage * kHalfStageBytes;
+    const int g = 2 * sl + half, ra = wm + 32 * cc + lrow;
+    f.a[cc] = *reinterpret_cast<const f16x8v*>(b + ra * 64 + slot_of(ra, g) * 16);
+  };
+  auto read_w = [&](Frags& f, int stage, int sl, int cc) {
+    const uint8_t* b = lds + stage * kHalfStageBytes + kBlkBytes / 2;
+    const int g = 2 * sl + half, rw = wn + 32 * cc + lrow;
+    f.w[cc] = *reinterpret_cast<const f16x8v*>(b + rw * 64 + slot_of(rw, g) * 16);
+  };
+  auto mfma_row = [&](const Frags& f, int i) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(f.w[j], f.a[i], acc[i][j], 0, 0, 0);
+  };
+  // One half step: read the next slice's fragments while the current
+  // slice's 8 MFMAs run, with three of the wave's six loads of step t + 3.
+  auto half_step = [&](Frags& cur, Frags& nxt, int stage, int sl, int ls, int64_t tl, int j0) {
+    read_a(nxt, stage, sl, 0);
+    read_w(nxt, stage, sl, 0);
+    read_w(nxt, stage, sl, 1);
+    mfma_row(cur, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    issue(ls, tl, j0);
+    __builtin_amdgcn_sched_barrier(0);
+    read_a(nxt, stage, sl, 1);
+    read_w(nxt, stage, sl, 2);
+    read_w(nxt, stage, sl, 3);
+    mfma_row(cur, 1);
+    __builtin_amdgcn_sched_barrier(0);
+    issue(ls, tl, j0 + 1);
+    issue(ls, tl, j0 + 2);
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  const int64_t last = steps - 1;
+#pragma unroll
+  for (int s0 = 0; s0 < kStages - 1; ++s0)
+#pragma unroll
+    for (int j = 0; j < 6; ++j) issue(s0, s0 < last ? s0 : last, j);
+  // step 0 landed (the two later steps' 12 loads may be in flight)
+  asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  Frags p, q;
+  read_a(p, 0, 0, 0);
+  read_a(p, 0, 0, 1);
+#pragma unroll
+  for (int cc = 0; cc < 4; ++cc) read_w(p, 0, 0, cc);
+  // Invariant at the top of step t as in gemm_f16_kernel: P holds slice 0 of
+  // step t; the loads of steps t+1 and t+2 are in flight or landed.
+  for (int64_t t = 0; t < steps; ++t) {
+    const int cur = (int)(t % kStages), ls = (int)((t + kStages - 1) % kStages);
+    const int64_t tl = t + kStages - 1 < last ? t + kStages - 1 : last;
+    half_step(p, q, cur, 1, ls, tl, 0);
+    // step t+1 landed: after its loads this wave issued the 6 of step t+2
+    // and 3 of step t+3.  The reads of slice 1 are complete too.
+    asm volatile("s_waitcnt vmcnt(9) lgkmcnt(0)" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    half_step(q, p, (int)((t + 1) % kStages), 0, ls, tl, 3);
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  const float scale = (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f);
+  const int64_t m0 = tm * kHalfRows + wm, n0 = tn * kTileRows + wn;
+  const bool vec = (ldc % 4) == 0 && (reinterpret_cast<uintptr_t>(c) & 15u) == 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int64_t row = m0 + i * 32 + lrow;
+    if (row >= m) continue;
+    float* crow = c + row * ldc;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+      for (int qq = 0; qq < 4; ++qq) {
+        const int64_t col = n0 + j * 32 + 8 * qq + 4 * half;
+        const f32x16& v = acc[i][j];
+        if (vec) {
+          if (col < n)
+            *reinterpret_cast<float4*>(crow + col) =
+                make_float4(v[4 * qq] * scale, v[4 * qq + 1] * scale, v[4 * qq + 2] * scale,
+                            v[4 * qq + 3] * scale);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            if (col + e < n) crow[col + e] = v[4 * qq + e] * scale;
+        }
+      }
+  }
+}
+
 }  // namespace
 
 bool gemm_two_pass_applies(int64_t m, int64_t n, int64_t k) {
@@ -223,8 +371,26 @@ int64_t gemm_two_pass_workspace(int64_t m, int64_t n, int64_t k) {
 hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uint8_t* wblk,
                                const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
                                hipStream_t stream) {
-  const unsigned tiles = (unsigned)((padded_rows(m) / kTileRows) * (padded_rows(n) / kTileRows));
-  gemm_f16_kernel<<<tiles, 256, 0, stream>>>(ablk, wblk, a_ts, w_ts, m, n, k, c, n);
+  const int64_t tm = padded_rows(m) / kTileRows, tn = padded_rows(n) / kTileRows;
+  const int64_t tiles = tm * tn;
+  // A short last round of 256 x 256 tiles keeps a few CUs busy for a whole
+  // tile time: its columns go to 128 x 256 tiles (half the work each) when
+  // those fit in one round.  Each output sums its K steps in the same order
+  // either way, so C is bit-identical.
+  const int64_t cus = compute_units();
+  const int64_t nt1 = tiles > cus ? (tiles / cus) * cus / tm : 0;   // tile columns in whole rounds
+  const int64_t rest = 2 * tm * (tn - nt1);                          // 128 x 256 tiles left
+  if (nt1 > 0 && nt1 < tn && rest <= cus) {
+    const int64_t n1 = kTileRows * nt1;
+    gemm_f16_kernel<<<(unsigned)(tm * nt1), 256, 0, stream>>>(ablk, wblk, a_ts, w_ts, m, n1, k,
+                                                               c, n);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    gemm_f16_half_kernel<<<(unsigned)rest, 256, 0, stream>>>(
+        ablk, wblk + nt1 * (k / kStepK) * kBlkBytes, a_ts, w_ts, m, n - n1, k, c + n1, n);
+    return hipGetLastError();
+  }
+  gemm_f16_kernel<<<(unsigned)tiles, 256, 0, stream>>>(ablk, wblk, a_ts, w_ts, m, n, k, c, n);
   return hipGetLastError();
 }
 

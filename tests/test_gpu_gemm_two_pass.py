@@ -107,6 +107,31 @@ def test_many_tiles(m, n, k):
         _check(c, qa, qw, rows=rows, cols=cols)
 
 
+@pytest.mark.parametrize("m,n,k,n1", [(2048, 11008, 4096, 8192), (4100, 4100, 512, 3840),
+                                      (4096, 14336, 1024, 12288)])
+def test_short_last_round_bit_identical(m, n, k, n1):
+    """Shapes whose 256 x 256 tiles leave a short last round send its columns
+    to 128 x 256 tiles (a second launch).  C must equal, bit for bit, the GEMMs
+    of the W row slices [0, n1) and [n1, n), which each fill whole rounds or
+    less than one and so run on 256 x 256 tiles only."""
+    import paper_2605_31035_amd as M
+    qa = Q.quantize(W.adversarial(m + 13, m, k))
+    qw = Q.quantize(W.adversarial(n + 17, n, k))
+    log(f"two-pass short last round m={m} n={n} k={k} split at {n1}")
+    a = _dev(qa)
+    wc, wsc, wts = _dev(qw)
+    full = M.mixfp4_gemm(a, (wc, wsc, wts), workspace=True)
+    left = M.mixfp4_gemm(a, (wc[:n1].contiguous(), wsc[:n1].contiguous(), wts), workspace=True)
+    right = M.mixfp4_gemm(a, (wc[n1:].contiguous(), wsc[n1:].contiguous(), wts), workspace=True)
+    torch.cuda.synchronize()
+    assert torch.equal(full[:, :n1], left)
+    assert torch.equal(full[:, n1:], right)
+    rng = np.random.default_rng(n)
+    rows = np.unique(np.concatenate([[0, m - 1], rng.integers(0, m, 40)]))
+    cols = np.unique(np.concatenate([[0, n1 - 1, n1, n - 1], rng.integers(n1, n, 40)]))
+    _check(host(full), qa, qw, rows=rows, cols=cols)
+
+
 @pytest.mark.parametrize("m,n,k,ws_bytes", [(16, 300, 4096, None), (64, 64, 48, None),
                                             (512, 512, 512, "short")])
 def test_falls_back_to_fused(m, n, k, ws_bytes):
