@@ -601,7 +601,7 @@ def measure_prefill(M, torch, dev, wl, steps: int, warmup: int, spin_s: float) -
            "spin_up_s": spin_s,
            "step_TFLOPs": round(total_flops / (ms_step * 1e-3) / 1e12, 3),
            "gemm_flops_per_step": total_flops,
-           "path_rule": "two passes where m n / (m + n) >= 1536 (gemm_two_pass_preferred), "
+           "path_rule": "two passes where m n / (m + n) >= 1280 (gemm_two_pass_preferred), "
                         "else the fused kernel",
            "quantize_a": ({"what": f"A[{ra},{ka}] quantized and decoded for the two-pass GEMM "
                                    "in one pass (mixfp4_quantize_decode: amax pass + reduction + "

@@ -323,12 +323,12 @@ def gemm_two_pass_preferred(m: int, n: int, k: int) -> bool:
     decode costs (m + n) k elements of HBM traffic, the faster GEMM saves a
     share of 2 m n k flops, so it pays off from m n / (m + n) on.  Measured
     on MI355X (decode of W included): 16384x8192x8192 1626 against 1990 us,
-    4096x14336x4096 408 against 470 us and 2048x11008x4096 (m n / (m + n) =
-    1727) 189 against 225 us favour two passes; 2048x4096x4096 (1365) is a
-    toss-up (86.6 against 90.7 us on one box, 85.5 against 83.9 on another)
-    and smaller products favour the fused kernel.  Threshold: 1536."""
+    4096x14336x4096 408 against 470 us, 2048x11008x4096 (m n / (m + n) =
+    1727) 189 against 219 us and 2048x4096x4096 (1365, on 128 x 256 tiles)
+    74 against 89 us favour two passes; smaller products favour the fused
+    kernel.  Threshold: 1280."""
     m, n, k = int(m), int(n), int(k)
-    return mixfp4_gemm_workspace_size(m, n, k) > 0 and m * n >= 1536 * (m + n)
+    return mixfp4_gemm_workspace_size(m, n, k) > 0 and m * n >= 1280 * (m + n)
 
 
 def mixfp4_gemm(a, w, out: torch.Tensor | None = None, workspace=None) -> torch.Tensor:

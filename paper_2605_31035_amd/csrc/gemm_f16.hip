@@ -209,9 +209,9 @@ __global__ __launch_bounds__(256, 1) void gemm_f16_kernel(const uint8_t* __restr
 
 
 // The same GEMM on 128 x 256 tiles, for the columns of a short last round
-// of 256 x 256 tiles (launch_gemm_decoded): a tile does half the work, so the
-// columns left after the whole rounds fill one round of 128 x 256 tiles in
-// half a tile time.  Wave w computes rows 64 (w / 2) and columns 128 (w % 2)
+// of 256 x 256 tiles and for products of at most half a round
+// (launch_gemm_decoded): a tile does half the work, so such columns fill one
+// round of 128 x 256 tiles in half a tile time.  Wave w computes rows 64 (w / 2) and columns 128 (w % 2)
 // of the tile as 2 x 4 MFMA tiles; an A tile is one half (8 KB, contiguous)
 // of each 256-row step block.  Each step's 24 KB are 24 loads of 1 KB, six
 // per wave, spread one per four MFMAs; the pipeline, stages and barriers are
@@ -375,9 +375,17 @@ hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uin
   const int64_t tiles = tm * tn;
   // A short last round of 256 x 256 tiles keeps a few CUs busy for a whole
   // tile time: its columns go to 128 x 256 tiles (half the work each) when
-  // those fit in one round.  Each output sums its K steps in the same order
-  // either way, so C is bit-identical.
+  // those fit in one round, and so does the whole product when it is half a
+  // round or less.  Each output sums its K steps in the same order either
+  // way, so C is bit-identical.
   const int64_t cus = compute_units();
+  if (2 * tiles <= cus) {
+    // at most half a round of 256 x 256 tiles: 128 x 256 tiles fill (at most)
+    // one round in half the time
+    gemm_f16_half_kernel<<<(unsigned)(2 * tiles), 256, 0, stream>>>(ablk, wblk, a_ts, w_ts, m, n,
+                                                                     k, c, n);
+    return hipGetLastError();
+  }
   const int64_t nt1 = tiles > cus ? (tiles / cus) * cus / tm : 0;   // tile columns in whole rounds
   const int64_t rest = 2 * tm * (tn - nt1);                          // 128 x 256 tiles left
   if (nt1 > 0 && nt1 < tn && rest <= cus) {

@@ -283,7 +283,8 @@ def test_two_pass_rule():
     assert M.gemm_two_pass_preferred(4096, 14336, 4096)
     assert M.gemm_two_pass_preferred(4096, 4096, 4096)          # m n / (m + n) = 2048 exactly
     assert M.gemm_two_pass_preferred(2048, 11008, 4096)
-    assert not M.gemm_two_pass_preferred(2048, 4096, 4096)
+    assert M.gemm_two_pass_preferred(2048, 4096, 4096)
+    assert not M.gemm_two_pass_preferred(1024, 4096, 4096)
     assert not M.gemm_two_pass_preferred(16, 1 << 20, 4096)     # decode shape: fused
     assert not M.gemm_two_pass_preferred(16384, 16384, 48)      # k % 32 != 0
 

@@ -132,6 +132,32 @@ def test_short_last_round_bit_identical(m, n, k, n1):
     _check(host(full), qa, qw, rows=rows, cols=cols)
 
 
+@pytest.mark.parametrize("m,n,k", [(2048, 4096, 1024), (300, 1000, 288), (1000, 260, 512)])
+def test_small_products_on_half_tiles(m, n, k):
+    """Products of at most half a round of 256 x 256 tiles run on 128 x 256
+    tiles.  Rows are independent, so C must equal, bit for bit, the first m
+    rows of the product with A stacked four times over, which has enough
+    tiles to run on 256 x 256 tiles (2048 x 4096: two whole rounds); ragged
+    shapes checked against the oracle."""
+    import paper_2605_31035_amd as M
+    qa = Q.quantize(W.adversarial(m + 21, m, k))
+    qw = Q.quantize(W.adversarial(n + 23, n, k))
+    log(f"two-pass half tiles m={m} n={n} k={k}")
+    a, w = _dev(qa), _dev(qw)
+    c = M.mixfp4_gemm(a, w, workspace=True)
+    big = (a[0].repeat(4, 1), a[1].repeat(4, 1), a[2])
+    c4 = M.mixfp4_gemm(big, w, workspace=True)
+    torch.cuda.synchronize()
+    assert torch.equal(c, c4[:m])
+    if m * n <= 1000 * 1000:
+        _check(host(c), qa, qw)
+    else:
+        rng = np.random.default_rng(m + n)
+        rows = np.unique(np.concatenate([[0, m - 1], rng.integers(0, m, 40)]))
+        cols = np.unique(np.concatenate([[0, n - 1], rng.integers(0, n, 40)]))
+        _check(host(c), qa, qw, rows=rows, cols=cols)
+
+
 @pytest.mark.parametrize("m,n,k,ws_bytes", [(16, 300, 4096, None), (64, 64, 48, None),
                                             (512, 512, 512, "short")])
 def test_falls_back_to_fused(m, n, k, ws_bytes):
