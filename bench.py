@@ -409,6 +409,13 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
                          .astype(np.int8), device=dev)
     names = ["quantize X", "quantize_2d W", "fprop gemm", "quantize dY (SR)", "dgrad gemm",
              "quantize dY^T (RHT16, SR)", "quantize X^T (RHT16)", "wgrad gemm"]
+    # every GEMM on its preferred route (gemm_two_pass_preferred), the
+    # two-pass workspace allocated once before timing
+    shapes = {"fprop": (tok, d_out, d_in), "dgrad": (tok, d_in, d_out), "wgrad": (d_out, d_in, tok)}
+    two = {g: M.gemm_two_pass_preferred(*mnk) for g, mnk in shapes.items()}
+    ws_bytes = max([M.mixfp4_gemm_workspace_size(*shapes[g]) for g in shapes if two[g]] + [1])
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    wsp = {g: (ws if two[g] else None) for g in shapes}
 
     def step(e=None, it=0):
         def mark(i):
@@ -419,18 +426,18 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
         mark(1)
         qw, qwt = M.mixfp4_quantize_2d(Wt)
         mark(2)
-        M.mixfp4_gemm(qx, qw)
+        M.mixfp4_gemm(qx, qw, workspace=wsp["fprop"])
         mark(3)
         qg = M.mixfp4_quantize(dY, rounding="stochastic", seed=it)
         mark(4)
-        M.mixfp4_gemm(qg, qwt)
+        M.mixfp4_gemm(qg, qwt, workspace=wsp["dgrad"])
         mark(5)
         qgt = M.mixfp4_quantize(dY, rounding="stochastic", seed=it, offset=1, hadamard_block=16,
                                 hadamard_signs=signs, transpose=True)
         mark(6)
         qxt = M.mixfp4_quantize(X, hadamard_block=16, hadamard_signs=signs, transpose=True)
         mark(7)
-        M.mixfp4_gemm(qgt, qxt)
+        M.mixfp4_gemm(qgt, qxt, workspace=wsp["wgrad"])
         mark(8)
 
     spin_up(torch, step, 0.3)
@@ -454,12 +461,14 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
         "us": {n: round(v * 1e3, 2) for n, v in zip(names, spans)},
         "gemm_TFLOPs": {n: round(flops / (spans[j] * 1e-3) / 1e12, 1)
                         for n, j in (("fprop", 2), ("dgrad", 4), ("wgrad", 7))},
+        "gemm_path": {g: ("two-pass (both operands decoded in the call)" if two[g] else "fused")
+                      for g in shapes},
         "quantize_GBps": {n: round(el * QUANT_BYTES_PER_ELEM / (spans[j] * 1e-3) / 1e9, 1)
                           for n, j, el in (("quantize_2d W (COMPUTE)", 1, d_out * d_in),
                                            ("quantize dY^T (COMPUTE, RHT16, SR)", 5, tok * d_out),
                                            ("quantize X^T (COMPUTE, RHT16)", 6, tok * d_in))},
     }
-    del X, Wt, dY, t
+    del X, Wt, dY, t, ws
     torch.cuda.empty_cache()
     return out
 
