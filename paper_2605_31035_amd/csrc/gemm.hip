@@ -275,13 +275,14 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // ---------------------------------------------------------------------------
 // Decode-shape GEMM (m <= 16): HBM-bound, W is read once.
 //
-// A workgroup owns 16 kCG columns of C (kCG = 1 to 4 MFMA column groups),
-// or two such ranges one after the other (4 + 1 .. 4 + 4 groups, so that one
-// workgroup per CU covers W), and splits K (k % 256 == 0) over its kW waves
-// in whole 256-wide steps (skinny_waves: 2 equal shares when k / 256 is 2 mod
-// 4, else 4 shares that differ by at most one step);
-// each wave walks its K range in steps of 256 with no barrier and no LDS
-// until the end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
+// A workgroup owns 16 G columns of C (G = 1 to 8 MFMA column groups, so that
+// one workgroup per CU covers W): one range of G groups for G <= 6, or for
+// G = 7, 8 two ranges of 4 and G - 4 groups worked on at the same time by two
+// sets of kW waves (two waves per SIMD).  A set splits K (k % 256 == 0) over
+// its kW waves in whole 256-wide steps (skinny_waves: 2 equal shares when
+// k / 256 is 2 mod 4, else 4 shares that differ by at most one step); each
+// wave walks its K range in steps of 256 with no barrier and no LDS until the
+// end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
 // nn + 16 c (c < kCG, one per 16-column group) and the quarter
 // [64 g, 64 g + 64) of every step: per row 32 code bytes and 4 scale bytes,
 // loaded one step ahead.  It decodes them straight into the B operands of
@@ -308,19 +309,23 @@ struct APack {
   uint32_t s[kSkinnySw];
 };
 
-// The body of the decode-shape GEMM for columns [col0, col0 + 16 kCG).
-// `before_a` runs once, after this lane's first W loads are issued and before
-// any A load; it returns false to poison these outputs (NaN) when A never
-// became available.
-template <int kW, int kCG, typename BeforeA>
+// The body of the decode-shape GEMM for columns [col0, col0 + 16 ng), run by
+// one set of kW waves (`wave` = 0 .. kW - 1 within the set) with its own
+// reduction buffer `red`.  With kMasked, only the first ng <= kCG groups are
+// active (uniform: a set of the shorter range skips the last group's loads
+// and work); otherwise all kCG are.  `before_a` runs
+// once, after this lane's first W loads are issued and before any A load; it
+// returns false to poison these outputs (NaN) when A never became available.
+template <int kW, int kCG, bool kMasked, typename BeforeA>
 __device__ __forceinline__ void skinny_body(
-    int64_t col0, const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
-    const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
-    const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
-    int64_t n, int64_t k, float* __restrict__ c, BeforeA before_a) {
-  __shared__ f32x4 red[kW - 1][kCG][64];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    int wave, f32x4 (*red)[kCG][64], int ng, int64_t col0, const uint8_t* __restrict__ a_codes,
+    const uint8_t* __restrict__ a_scales, const float* __restrict__ a_ts,
+    const uint8_t* __restrict__ w_codes, const uint8_t* __restrict__ w_scales,
+    const float* __restrict__ w_ts, int64_t m, int64_t n, int64_t k, float* __restrict__ c,
+    BeforeA before_a) {
+  const int lane = threadIdx.x & 63;
   const int nn = lane & 15, g = lane >> 4;
+  auto active = [&](int cg) { return !kMasked || cg < ng; };
   const int64_t code_pitch = k / 2, scale_pitch = k / kBlock;
   // this wave's K range: steps [S w / kW, S (w + 1) / kW) of the S = k / 256
   // (an equal share when kW divides S; a wave may have none when S < kW)
@@ -344,14 +349,18 @@ __device__ __forceinline__ void skinny_body(
     st = st < steps ? st : steps - 1;
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg)
+      if (active(cg)) {
 #pragma unroll
-      for (int v = 0; v < kSkinnyVec; ++v)
-        p.c[cg][v] = *reinterpret_cast<const uint4*>(wc[cg] + (kSkinnyStep / 2) * st + 16 * v);
+        for (int v = 0; v < kSkinnyVec; ++v)
+          p.c[cg][v] = *reinterpret_cast<const uint4*>(wc[cg] + (kSkinnyStep / 2) * st + 16 * v);
+      }
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg)
+      if (active(cg)) {
 #pragma unroll
-      for (int v = 0; v < kSkinnySw; ++v)
-        p.s[cg][v] = *reinterpret_cast<const uint32_t*>(ws[cg] + (kSkinnyStep / 16) * st + 4 * v);
+        for (int v = 0; v < kSkinnySw; ++v)
+          p.s[cg][v] = *reinterpret_cast<const uint32_t*>(ws[cg] + (kSkinnyStep / 16) * st + 4 * v);
+      }
   };
   auto load_a = [&](APack& p, int64_t st) {
     st = st < steps ? st : steps - 1;
@@ -377,6 +386,7 @@ __device__ __forceinline__ void skinny_body(
       for (int i = 0; i < 4; ++i) fa[i] = __builtin_bit_cast(f16x8, decode8(ca[i], i < 2 ? da0 : da1));
 #pragma unroll
       for (int cg = 0; cg < kCG; ++cg) {
+        if (!active(cg)) continue;
         const uint32_t sw = pw.s[cg][v >> 1] >> (16 * (v & 1));
         const BlockDec d0 = block_dec(sw & 0xFFu), d1 = block_dec((sw >> 8) & 0xFFu);
         const uint32_t cw[4] = {pw.c[cg][v].x, pw.c[cg][v].y, pw.c[cg][v].z, pw.c[cg][v].w};
@@ -423,6 +433,7 @@ __device__ __forceinline__ void skinny_body(
     const float scale = a_ok ? (a_ts ? *a_ts : 1.0f) * (w_ts ? *w_ts : 1.0f) : __builtin_nanf("");
 #pragma unroll
     for (int cg = 0; cg < kCG; ++cg) {
+      if (!active(cg)) continue;
       f32x4 t = acc[cg];
 #pragma unroll
       for (int w = 0; w < kW - 1; ++w) t += red[w][cg][lane];
@@ -439,30 +450,32 @@ __device__ __forceinline__ void skinny_body(
   }
 }
 
-// Columns [16 (kA + kB) b, 16 (kA + kB) (b + 1)) of workgroup b: kA groups,
-// then kB more (kB = 0: one range).  Each column's sum is formed in the same
-// order whatever the split, so C does not depend on it.
+// Columns [16 (kA + kB) b, 16 (kA + kB) (b + 1)) of workgroup b: kA groups
+// (kB = 0: one range, kW waves), or waves 0 .. kW - 1 on kA = 4 groups and
+// waves kW .. 2 kW - 1 on the kB <= 4 groups after them, both with the same
+// body.  Each column's sum is formed in the same order whatever the split, so
+// C does not depend on it.
+template <int kA, int kB>
+constexpr int skinny_sets() { return kB > 0 ? 2 : 1; }
+
 template <int kW, int kA, int kB, typename BeforeA>
 __device__ __forceinline__ void skinny_columns(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
     int64_t n, int64_t k, float* __restrict__ c, BeforeA before_a) {
+  static_assert(kB == 0 || (kA == 4 && kB <= 4), "two ranges are 4 + (1 .. 4) groups");
+  __shared__ f32x4 red[skinny_sets<kA, kB>()][kW - 1][kA][64];
   const int64_t col0 = (int64_t)blockIdx.x * 16 * (kA + kB);
-  bool ok = true;
-  skinny_body<kW, kA>(col0, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, [&]() {
-    ok = before_a();
-    return ok;
-  });
-  if constexpr (kB > 0) {
-    __syncthreads();                                // the reduction buffer is reused
-    skinny_body<kW, kB>(col0 + 16 * kA, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n,
-                        k, c, [&]() { return ok; });
-  }
+  const int wave = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+  const int set = wave / kW;
+  skinny_body<kW, kA, (kB > 0)>(wave - set * kW, red[set], set ? kB : kA, col0 + set * 16 * kA,
+                                a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c,
+                                before_a);
 }
 
 template <int kW, int kA, int kB>
-__global__ __launch_bounds__(64 * kW) void gemm_skinny_kernel(
+__global__ __launch_bounds__(64 * kW * (kB > 0 ? 2 : 1)) void gemm_skinny_kernel(
     const uint8_t* __restrict__ a_codes, const uint8_t* __restrict__ a_scales,
     const float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m,
@@ -582,7 +595,7 @@ __device__ __forceinline__ void produce_a(const uint16_t* __restrict__ x, int64_
 }
 
 template <int kW, int kA, int kB>
-__global__ __launch_bounds__(64 * kW) void decode_step_kernel(
+__global__ __launch_bounds__(64 * kW * (kB > 0 ? 2 : 1)) void decode_step_kernel(
     const uint16_t* __restrict__ x, uint8_t* __restrict__ a_codes, uint8_t* __restrict__ a_scales,
     float* __restrict__ a_ts, const uint8_t* __restrict__ w_codes,
     const uint8_t* __restrict__ w_scales, const float* __restrict__ w_ts, int64_t m, int64_t n,
@@ -643,12 +656,13 @@ hipError_t launch_skinny(const uint8_t* a_codes, const uint8_t* a_scales, const 
                          const uint8_t* w_codes, const uint8_t* w_scales, const float* w_ts,
                          int64_t m, int64_t n, int64_t k, float* c, hipStream_t stream) {
   const unsigned groups = (unsigned)((n + 16 * (kA + kB) - 1) / (16 * (kA + kB)));
+  constexpr int sets = skinny_sets<kA, kB>();
   if (skinny_waves(k) == 4)
-    gemm_skinny_kernel<4, kA, kB><<<groups, 256, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
-                                                              w_scales, w_ts, m, n, k, c);
+    gemm_skinny_kernel<4, kA, kB><<<groups, 256 * sets, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
   else
-    gemm_skinny_kernel<2, kA, kB><<<groups, 128, 0, stream>>>(a_codes, a_scales, a_ts, w_codes,
-                                                              w_scales, w_ts, m, n, k, c);
+    gemm_skinny_kernel<2, kA, kB><<<groups, 128 * sets, 0, stream>>>(
+        a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c);
   return hipGetLastError();
 }
 
@@ -659,24 +673,30 @@ hipError_t launch_step(const uint16_t* x, uint8_t* a_codes, uint8_t* a_scales, f
                        hipStream_t stream) {
   const int64_t groups = (n + 16 * (kA + kB) - 1) / (16 * (kA + kB));
   const int producers = (int)(groups < kStepProducers ? groups : kStepProducers);
+  constexpr int sets = skinny_sets<kA, kB>();
   if (skinny_waves(k) == 4)
-    decode_step_kernel<4, kA, kB><<<(unsigned)groups, 256, 0, stream>>>(
+    decode_step_kernel<4, kA, kB><<<(unsigned)groups, 256 * sets, 0, stream>>>(
         x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, producers);
   else
-    decode_step_kernel<2, kA, kB><<<(unsigned)groups, 128, 0, stream>>>(
+    decode_step_kernel<2, kA, kB><<<(unsigned)groups, 128 * sets, 0, stream>>>(
         x, a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, sync, producers);
   return hipGetLastError();
 }
 
 // Column groups per workgroup of the decode-shape GEMM: the fewest 16-column
 // groups G that cover W with at most one workgroup per CU, run as one range
-// (G <= 4) or as 4 + (G - 4); beyond 8 groups, 4 per workgroup and several
-// workgroups per CU.  Narrow W then still spreads over every CU, and no CU
-// gets two workgroups while others get one.  Measured, m = 16:
-// k = 4096, n = 4096: 5.3 us with G = 1 against 11.7 with 4; n = 8192 7.5
-// against 11.8; n = 11008 9.7 against 11.6; 16 x 28672 x 8192: 33.3 us with
-// 4 + 3 groups on 256 workgroups against 35.4 with 4 groups on 448 (192 CUs
-// with two of them).
+// (G <= 6) or as 4 + (G - 4) on two sets of waves (G = 7, 8); beyond 8
+// groups, 4 per workgroup and several workgroups per CU.  Narrow W then still
+// spreads over every CU, and no CU gets two workgroups while others get one.
+// Measured, m = 16: k = 4096, n = 4096: 5.3 us with G = 1 against 11.7 with
+// 4; n = 8192 7.5 against 11.8; n = 11008 9.7 against 11.6; 16 x 28672 x 8192:
+// 33.3 us with 4 + 3 groups on 256 workgroups against 35.4 with 4 groups on
+// 448 (192 CUs with two of them).  Against 4 + (G - 4) run one after the
+// other by the same 4 waves: one range of 5 (6) groups 23.0 (17.5) us
+// against 26.2 (19.0) on 16 x 20480 x 8192 (16 x 24576 x 4096); concurrent
+// sets 22.0 against 24.3 us on 16 x 32768 x 4096, 31.0 against 33.1 on
+// 1 x 28672 x 8192, 19.5 against 20.9 on 8 x 28672 x 4096, 15.2 against 17.4
+// on 16 x 28672 x 2816, 33.5 against 33.8 on 16 x 28672 x 8192.
 template <typename Launch>
 hipError_t by_column_split(int64_t n, Launch launch) {
   const int64_t cus = compute_units();
@@ -686,8 +706,8 @@ hipError_t by_column_split(int64_t n, Launch launch) {
     case 2: return launch(std::integral_constant<int, 2>{}, std::integral_constant<int, 0>{});
     case 3: return launch(std::integral_constant<int, 3>{}, std::integral_constant<int, 0>{});
     case 4: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 0>{});
-    case 5: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 1>{});
-    case 6: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 2>{});
+    case 5: return launch(std::integral_constant<int, 5>{}, std::integral_constant<int, 0>{});
+    case 6: return launch(std::integral_constant<int, 6>{}, std::integral_constant<int, 0>{});
     case 7: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 3>{});
     case 8: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 4>{});
     default: return launch(std::integral_constant<int, 4>{}, std::integral_constant<int, 0>{});

@@ -68,8 +68,9 @@ def test_shapes(m, n, k):
 @pytest.mark.parametrize("m,n,k", [(16, 22000, 1024), (3, 28000, 512), (16, 31000, 1024),
                                    (8, 40000, 512)])
 def test_wide_w_column_splits(m, n, k):
-    """Wide W: 4 + 2, 4 + 3 and 4 + 4 column groups per workgroup (one
-    workgroup per CU) and 4 groups with several workgroups per CU.  W is
+    """Wide W: one range of 6 column groups per workgroup, 4 + 3 and 4 + 4
+    groups on two sets of waves at once (one workgroup per CU), and 4 groups
+    with several workgroups per CU.  W is
     quantized on the device; A's outputs are checked against the oracle bit
     for bit and C on sampled columns."""
     import paper_2605_31035_amd as M

@@ -226,9 +226,11 @@ def test_workload_full_size(name):
 @pytest.mark.parametrize("m,n,k", [(16, 17000, 512), (5, 22000, 1024), (16, 28672, 512),
                                    (11, 30000, 1024), (16, 40000, 512)])
 def test_decode_shapes_column_splits(m, n, k):
-    """Wide W on the decode-shape kernel: 4 + 1, 4 + 2, 4 + 3 and 4 + 4
-    column groups per workgroup (one workgroup per CU), and 4 groups with
-    several workgroups per CU beyond that.  W is quantized on the device (the
+    """Wide W on the decode-shape kernel: one range of 5 or 6 column groups
+    per workgroup, 4 + 3 and 4 + 4 groups on two sets of waves at once (one
+    workgroup per CU; the second set starts 64 columns into the workgroup's
+    range, a sampled column), and 4 groups with several workgroups per CU
+    beyond that.  W is quantized on the device (the
     quantizer's parity is tested on its own); C is checked on sampled columns,
     both ends of each workgroup's column range included, against the oracle
     quantizing those W rows with W's tensor scale; and column slices cut
