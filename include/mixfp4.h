@@ -401,7 +401,7 @@ const char *mixfp4_status_string(int status);
  * mixfp4_gemm on them bit for bit.
  *   a          A, bf16 bit patterns, row-major [m, k] with row pitch k,
  *              16-byte aligned (device).
- *   m, k       1 <= m <= 16, k > 0, k % 256 == 0 (else MIXFP4_ERR_SHAPE).
+ *   m, k       1 <= m <= 16, k > 0, k % 64 == 0 (else MIXFP4_ERR_SHAPE).
  *   w_codes, w_scales, w_tensor_scale, n
  *              W [n, k] as for mixfp4_gemm (w_scales 4-byte aligned;
  *              w_tensor_scale NULL means 1.0); n >= 1.

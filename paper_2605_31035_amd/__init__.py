@@ -387,8 +387,8 @@ _STEP_SYNC: dict = {}
 
 
 def decode_step_applies(m: int, k: int) -> bool:
-    """Shapes mixfp4_decode_step takes: 1 <= m <= 16 rows, k % 256 == 0."""
-    return 1 <= m <= 16 and k > 0 and k % 256 == 0
+    """Shapes mixfp4_decode_step takes: 1 <= m <= 16 rows, k % 64 == 0."""
+    return 1 <= m <= 16 and k > 0 and k % 64 == 0
 
 
 def mixfp4_decode_step(x: torch.Tensor, w, out: torch.Tensor | None = None, a_out=None,
@@ -407,7 +407,7 @@ def mixfp4_decode_step(x: torch.Tensor, w, out: torch.Tensor | None = None, a_ou
     m, k = x.shape
     n = wc.shape[0] if isinstance(wc, torch.Tensor) and wc.dim() == 2 else -1
     if not decode_step_applies(m, k) or n < 1:
-        raise ValueError(f"decode step needs 1 <= m <= 16, k % 256 == 0, n >= 1 (m={m}, k={k}, n={n})")
+        raise ValueError(f"decode step needs 1 <= m <= 16, k % 64 == 0, n >= 1 (m={m}, k={k}, n={n})")
     if not x.is_contiguous():
         raise ValueError("x must be contiguous")
     _require(wc, "W codes", torch.uint8, (n, k // 2))

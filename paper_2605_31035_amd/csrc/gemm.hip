@@ -278,8 +278,9 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // A workgroup owns 16 G columns of C (G = 1 to 8 MFMA column groups, so that
 // one workgroup per CU covers W): one range of G groups for G <= 6, or for
 // G = 7, 8 two ranges of 4 and G - 4 groups worked on at the same time by two
-// sets of kW waves (two waves per SIMD).  A set splits K (k % 256 == 0) over
-// its kW waves in whole 256-wide steps (skinny_waves: 2 equal shares when
+// sets of kW waves (two waves per SIMD).  A set splits K (k % 64 == 0) over
+// its kW waves in whole 256-wide steps, the last wave also taking the rest of
+// K % 256 as a tail step (skinny_waves: 2 equal shares when
 // k / 256 is 2 mod 4, else 4 shares that differ by at most one step); each
 // wave walks its K range in steps of 256 with no barrier and no LDS until the
 // end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
@@ -296,6 +297,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kSkinnyRows = 16;
 constexpr int kSkinnyStep = 256;                   // K per wave step
+constexpr int kSkinnyK = 64;                       // K multiple the kernel takes (a lane's share of a step)
 constexpr int kSkinnyVec = kSkinnyStep / 128;      // 16-byte code loads per row per lane per step
 constexpr int kSkinnySw = kSkinnyStep / 256;       // scale dwords per row per lane per step
 
@@ -333,6 +335,10 @@ __device__ __forceinline__ void skinny_body(
   const int64_t s_first = total_steps * wave / kW;
   const int64_t steps = total_steps * (wave + 1) / kW - s_first;
   const int64_t kbase = s_first * kSkinnyStep;
+  // K % 256 = 64, 128 or 192: the set's last wave takes one more step after
+  // its range, the tail, in which the lanes past it (64 g >= tail) get zeros
+  const int tail = (int)(k % kSkinnyStep);
+  const bool has_tail = tail != 0 && wave == kW - 1;
   const uint8_t* wc[kCG];
   const uint8_t* ws[kCG];
 #pragma unroll
@@ -423,6 +429,41 @@ __device__ __forceinline__ void skinny_body(
     step(I1{}, s + 1);
   }
   if (s < steps) step(I0{}, s);
+  if (has_tail) {
+    // the tail follows this wave's range (step `steps`); a lane past it
+    // loads its row's first tail piece instead and zeroes it
+    const bool in_tail = kSkinnyVec * 32 * g < tail;
+    const int64_t back = in_tail ? 0 : (kSkinnyStep / 8) * g;     // code bytes back to piece 0
+    const int64_t sback = in_tail ? 0 : (kSkinnyStep / 64) * g;   // scale bytes back
+    const uint4 z4 = make_uint4(0u, 0u, 0u, 0u);
+    WPack<kCG> tw;
+    APack ta;
+#pragma unroll
+    for (int cg = 0; cg < kCG; ++cg)
+      if (active(cg)) {
+#pragma unroll
+        for (int v = 0; v < kSkinnyVec; ++v) {
+          const uint4 x = *reinterpret_cast<const uint4*>(wc[cg] - back + (kSkinnyStep / 2) * steps + 16 * v);
+          tw.c[cg][v] = in_tail ? x : z4;
+        }
+#pragma unroll
+        for (int v = 0; v < kSkinnySw; ++v) {
+          const uint32_t x = *reinterpret_cast<const uint32_t*>(ws[cg] - sback + (kSkinnyStep / 16) * steps + 4 * v);
+          tw.s[cg][v] = in_tail ? x : 0u;
+        }
+      }
+#pragma unroll
+    for (int v = 0; v < kSkinnyVec; ++v) {
+      const uint4 x = *reinterpret_cast<const uint4*>(ac - back + (kSkinnyStep / 2) * steps + 16 * v);
+      ta.c[v] = in_tail ? x : z4;
+    }
+#pragma unroll
+    for (int v = 0; v < kSkinnySw; ++v) {
+      const uint32_t x = *reinterpret_cast<const uint32_t*>(as - sback + (kSkinnyStep / 16) * steps + 4 * v);
+      ta.s[v] = in_tail ? x : 0u;
+    }
+    compute(ta, tw);
+  }
 
   if (wave > 0) {
 #pragma unroll
@@ -648,7 +689,8 @@ hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const fl
 // not a multiple of 4 (equal shares, as measured best), else 4 (equal shares
 // when k % 1024 == 0, otherwise shares differing by one 256-wide step).
 inline int skinny_waves(int64_t k) {
-  return (k % (4 * kSkinnyStep) != 0 && k % (2 * kSkinnyStep) == 0) ? 2 : 4;
+  const int64_t s = k / kSkinnyStep;
+  return (s % 4 != 0 && s % 2 == 0) ? 2 : 4;
 }
 
 template <int kA, int kB>
@@ -717,7 +759,7 @@ hipError_t by_column_split(int64_t n, Launch launch) {
 }  // namespace
 
 bool decode_step_applies(int64_t m, int64_t k) {
-  return m >= 1 && m <= kSkinnyRows && k > 0 && k % kSkinnyStep == 0;
+  return m >= 1 && m <= kSkinnyRows && k > 0 && k % kSkinnyK == 0;
 }
 
 hipError_t launch_decode_step(const uint16_t* x, int64_t m, int64_t k, const uint8_t* w_codes,
@@ -741,11 +783,12 @@ hipError_t launch_gemm(const uint8_t* a_codes, const uint8_t* a_scales, const fl
     fill_zero<<<(int)g, 256, 0, stream>>>(c, m * n);
     return hipGetLastError();
   }
-  // decode shape: the waves split K in whole 256-wide steps (skinny_waves);
+  // decode shape: the waves split K in 256-wide steps and a tail of 64, 128
+  // or 192 (skinny_waves);
   // scale loads are 4-byte words
   const bool skinny_aligned = ((reinterpret_cast<uintptr_t>(w_scales) |
                                 reinterpret_cast<uintptr_t>(a_scales)) & 3u) == 0;
-  if (m <= kSkinnyRows && skinny_aligned && k % kSkinnyStep == 0) {
+  if (m <= kSkinnyRows && skinny_aligned && k % kSkinnyK == 0) {
     return by_column_split(n, [&](auto A, auto B) {
       return launch_skinny<decltype(A)::value, decltype(B)::value>(
           a_codes, a_scales, a_ts, w_codes, w_scales, w_ts, m, n, k, c, stream);

@@ -156,8 +156,8 @@ hipError_t launch_gemm_decoded(const uint8_t* ablk, const float* a_ts, const uin
                                const float* w_ts, int64_t m, int64_t n, int64_t k, float* c,
                                hipStream_t stream);
 // One-launch decode step (A[m, k] bf16 row-major, quantized in the launch,
-// then C = A W^T): applies for 1 <= m <= 16 and k % 256 == 0 (the decode-
-// shape GEMM's K steps); `sync` is 4 zeroed uint32 on the device, returned
+// then C = A W^T): applies for 1 <= m <= 16 and k % 64 == 0 (the decode-
+// shape GEMM's K split); `sync` is 4 zeroed uint32 on the device, returned
 // to zero by the launch.
 bool decode_step_applies(int64_t m, int64_t k);
 hipError_t launch_decode_step(const uint16_t* x, int64_t m, int64_t k, const uint8_t* w_codes,

@@ -300,8 +300,9 @@ def test_decode_step_rejects(lib):
     assert f(*args(c=None)) == 1
     assert f(*args(m=17)) == 2                      # more than 16 rows
     assert f(*args(m=0)) == 2
-    assert f(*args(k=128)) == 2                     # k % 256
+    assert f(*args(k=4096 + 32)) == 2               # k % 64
     assert f(*args(k=4096 + 272)) == 2
+    assert f(*args(k=48)) == 2
     assert f(*args(n=0)) == 2
     assert f(*args(a=P(0x10008))) == 3              # A not 16-byte aligned
     assert f(*args(ac=P(0x10008))) == 3
@@ -313,7 +314,9 @@ def test_decode_step_applies_rule():
     import paper_2605_31035_amd as M
     assert M.decode_step_applies(16, 8192) and M.decode_step_applies(1, 512)
     assert M.decode_step_applies(16, 11008) and M.decode_step_applies(3, 256)
-    assert not M.decode_step_applies(17, 8192) and not M.decode_step_applies(16, 640)
+    assert M.decode_step_applies(16, 640) and M.decode_step_applies(2, 64)   # K tails
+    assert not M.decode_step_applies(17, 8192) and not M.decode_step_applies(16, 4128)
+    assert not M.decode_step_applies(4, 48)
 
 
 def test_quantize_variant_rejects(lib):

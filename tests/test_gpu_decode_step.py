@@ -42,12 +42,14 @@ def _step(a_bits, qw_dev):
 
 @pytest.mark.parametrize("m,n,k", [(16, 300, 4096), (1, 17, 512), (5, 4112, 1024),
                                    (16, 8192, 2048), (11, 12000, 512), (16, 20000, 1024),
-                                   (16, 1100, 11008), (2, 700, 256)])
+                                   (16, 1100, 11008), (2, 700, 256), (16, 900, 4160),
+                                   (3, 2000, 192), (9, 5000, 1344)])
 def test_shapes(m, n, k):
     """Every column-group width (16 .. 64 columns per workgroup), the K
     splits (four equal shares, two, and four shares that differ by one step:
-    k = 11008 is 43 steps of 256, k = 256 one), ragged m and n, and grids
-    smaller than the 32 producer workgroups (n = 17: two workgroups)."""
+    k = 11008 is 43 steps of 256, k = 256 one), K tails of 64, 192 and 64
+    after 16, 0 and 5 whole steps, ragged m and n, and grids smaller than the
+    32 producer workgroups (n = 17: two workgroups)."""
     import paper_2605_31035_amd as M
     a_bits = W.adversarial(m + 3 * n, m, k)
     w_bits = W.adversarial(n + 7, n, k)
@@ -142,7 +144,7 @@ def test_calls_in_a_row_and_sync_reset():
 def test_rejects():
     import paper_2605_31035_amd as M
     w = M.mixfp4_quantize(torch.zeros((8, 512), dtype=torch.bfloat16, device="cuda"))
-    for shape in ((17, 512), (4, 128), (0, 512)):
+    for shape in ((17, 512), (4, 96), (0, 512)):
         with pytest.raises(ValueError):
             M.mixfp4_decode_step(torch.zeros(shape, dtype=torch.bfloat16, device="cuda"), w)
     with pytest.raises(ValueError):

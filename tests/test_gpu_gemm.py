@@ -73,12 +73,16 @@ def test_ragged_shapes(m, n, k):
                                    (16, 256, 8192), (3, 300, 1536), (16, 6150, 1024),
                                    (2, 7000, 1536), (16, 10250, 2048), (7, 10256, 512),
                                    (16, 12300, 1024), (1, 33, 256), (16, 500, 768),
-                                   (4, 1300, 1280), (16, 1100, 11008), (13, 9000, 2816)])
+                                   (4, 1300, 1280), (16, 1100, 11008), (13, 9000, 2816),
+                                   (16, 1000, 64), (5, 3000, 320), (16, 4096, 4160),
+                                   (1, 700, 2880), (13, 2000, 192), (7, 1500, 704)])
 def test_decode_shapes(m, n, k):
-    """m <= 16 with k % 256 == 0 takes the decode-shape kernel: K split over
+    """m <= 16 with k % 64 == 0 takes the decode-shape kernel: K split over
     4 waves in equal shares (k % 1024 == 0) or in shares that differ by one
     256-wide step (k / 256 odd or 1 mod 4 or 3 mod 4: 1, 3, 5, 43, 11 steps;
     fewer steps than waves leave waves idle), over 2 when k / 256 is 2 mod 4;
+    a tail of 64, 128 or 192 after the whole steps (0, 1, 16, 11, 0 and 2 of
+    them) goes to the last wave, its lanes past the tail reading nothing;
     16, 32, 48 or 64 columns per workgroup (n up to 4096, 8192, 12288, above),
     ragged last column groups included."""
     a = W.adversarial(7 * m + k, m, k)
@@ -224,7 +228,8 @@ def test_workload_full_size(name):
 
 
 @pytest.mark.parametrize("m,n,k", [(16, 17000, 512), (5, 22000, 1024), (16, 28672, 512),
-                                   (11, 30000, 1024), (16, 40000, 512)])
+                                   (11, 30000, 1024), (16, 40000, 512), (9, 20000, 1472),
+                                   (16, 30000, 704)])
 def test_decode_shapes_column_splits(m, n, k):
     """Wide W on the decode-shape kernel: one range of 5 or 6 column groups
     per workgroup, 4 + 3 and 4 + 4 groups on two sets of waves at once (one
