@@ -453,6 +453,20 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
     torch.cuda.synchronize()
     spans = [float(np.mean([e[j].elapsed_time(e[j + 1]) for e in ev])) for j in range(8)]
     flops = 2.0 * tok * d_in * d_out
+    # The 2D weight quantizer on its own, back to back, W's tensor scale given:
+    # 2 B read, both layouts' codes and scales written (3.125 B/element).  In
+    # the step it runs right after the GEMMs, at the clock they leave.
+    w_ts = M.mixfp4_quantize_2d(Wt)[0][2].clone()
+    q2d = lambda: M.mixfp4_quantize_2d(Wt, tensor_scale=w_ts)
+    spin_up(torch, q2d, 0.2)
+    b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    b0.record()
+    for _ in range(20):
+        q2d()
+    b1.record()
+    torch.cuda.synchronize()
+    q2d_us = b0.elapsed_time(b1) / 20 * 1e3
+    q2d_gbps = d_out * d_in * 3.125 / (q2d_us * 1e-6) / 1e9
     out = {
         "workload": "train_7b: X[2048,4096] Student-t nu=4 (8 channels x50), W[11008,4096] "
                     "N(0,0.02), dY[2048,11008] 1e-4 Student-t nu=3 (16 channels x20)",
@@ -467,6 +481,10 @@ def measure_train(M, torch, dev, iters: int = 10) -> dict:
                           for n, j, el in (("quantize_2d W (COMPUTE)", 1, d_out * d_in),
                                            ("quantize dY^T (COMPUTE, RHT16, SR)", 5, tok * d_out),
                                            ("quantize X^T (COMPUTE, RHT16)", 6, tok * d_in))},
+        "quantize_2d_standalone": {
+            "what": "mixfp4_quantize_2d of W[11008,4096] (both layouts) back to back, s32 given",
+            "us": round(q2d_us, 2), "GBps": round(q2d_gbps, 1), "bytes_per_elem": 3.125,
+            "hbm_frac": round(q2d_gbps / 8000.0, 4)},
     }
     del X, Wt, dY, t, ws
     torch.cuda.empty_cache()
