@@ -281,7 +281,7 @@ __global__ __launch_bounds__(64 * WM * WN, 1) void gemm_kernel(
 // sets of kW waves (two waves per SIMD).  A set splits K (k % 64 == 0) over
 // its kW waves in whole 256-wide steps, the last wave also taking the rest of
 // K % 256 as a tail step (skinny_waves: 2 equal shares when
-// k / 256 is 2 mod 4, else 4 shares that differ by at most one step); each
+// floor(k / 256) is 2 mod 4, else 4 shares that differ by at most one step); each
 // wave walks its K range in steps of 256 with no barrier and no LDS until the
 // end.  Lane (nn, g) = (lane % 16, lane / 16) owns W rows
 // nn + 16 c (c < kCG, one per 16-column group) and the quarter
@@ -685,9 +685,10 @@ hipError_t launch_tile(const uint8_t* a_codes, const uint8_t* a_scales, const fl
   return hipGetLastError();
 }
 
-// Waves splitting K in the decode-shape kernel: 2 when k / 256 is even but
-// not a multiple of 4 (equal shares, as measured best), else 4 (equal shares
-// when k % 1024 == 0, otherwise shares differing by one 256-wide step).
+// Waves splitting K in the decode-shape kernel, by the S = floor(k / 256)
+// whole steps: 2 when S is even but not a multiple of 4 (equal shares, as
+// measured best), else 4 (equal shares when S % 4 == 0, otherwise shares
+// differing by one step); a K tail goes to the last wave either way.
 inline int skinny_waves(int64_t k) {
   const int64_t s = k / kSkinnyStep;
   return (s % 4 != 0 && s % 2 == 0) ? 2 : 4;
