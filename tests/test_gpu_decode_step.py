@@ -68,7 +68,7 @@ def test_shapes(m, n, k):
 
 
 @pytest.mark.parametrize("m,n,k", [(16, 22000, 1024), (3, 28000, 512), (16, 31000, 1024),
-                                   (8, 40000, 512)])
+                                   (8, 40000, 512), (5, 27940, 512)])
 def test_wide_w_column_splits(m, n, k):
     """Wide W: one range of 6 column groups per workgroup, 4 + 3 and 4 + 4
     groups on two sets of waves at once (one workgroup per CU), and 4 groups

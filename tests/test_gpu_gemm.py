@@ -229,7 +229,7 @@ def test_workload_full_size(name):
 
 @pytest.mark.parametrize("m,n,k", [(16, 17000, 512), (5, 22000, 1024), (16, 28672, 512),
                                    (11, 30000, 1024), (16, 40000, 512), (9, 20000, 1472),
-                                   (16, 30000, 704)])
+                                   (16, 30000, 704), (16, 28600, 512)])
 def test_decode_shapes_column_splits(m, n, k):
     """Wide W on the decode-shape kernel: one range of 5 or 6 column groups
     per workgroup, 4 + 3 and 4 + 4 groups on two sets of waves at once (one
