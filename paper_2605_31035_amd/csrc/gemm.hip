@@ -381,11 +381,16 @@ __device__ __forceinline__ void skinny_body(
 #pragma unroll
   for (int cg = 0; cg < kCG; ++cg) acc[cg] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
   auto compute = [&](const APack& pa, const WPack<kCG>& pw) {
+    BlockDec dA[4];
+    block_dec4(pa.s[0], dA);
+    BlockDec dW[kCG][4];
+#pragma unroll
+    for (int cg = 0; cg < kCG; ++cg)
+      if (active(cg)) block_dec4(pw.s[cg][0], dW[cg]);
 #pragma unroll
     for (int v = 0; v < kSkinnyVec; ++v) {
       // 16-byte word v holds 32 elements = blocks 2v, 2v + 1 (scale bytes 2v, 2v + 1)
-      const uint32_t sa = pa.s[v >> 1] >> (16 * (v & 1));
-      const BlockDec da0 = block_dec(sa & 0xFFu), da1 = block_dec((sa >> 8) & 0xFFu);
+      const BlockDec da0 = dA[2 * v], da1 = dA[2 * v + 1];
       const uint32_t ca[4] = {pa.c[v].x, pa.c[v].y, pa.c[v].z, pa.c[v].w};
       f16x8 fa[4];
 #pragma unroll
@@ -393,8 +398,7 @@ __device__ __forceinline__ void skinny_body(
 #pragma unroll
       for (int cg = 0; cg < kCG; ++cg) {
         if (!active(cg)) continue;
-        const uint32_t sw = pw.s[cg][v >> 1] >> (16 * (v & 1));
-        const BlockDec d0 = block_dec(sw & 0xFFu), d1 = block_dec((sw >> 8) & 0xFFu);
+        const BlockDec d0 = dW[cg][2 * v], d1 = dW[cg][2 * v + 1];
         const uint32_t cw[4] = {pw.c[cg][v].x, pw.c[cg][v].y, pw.c[cg][v].z, pw.c[cg][v].w};
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
