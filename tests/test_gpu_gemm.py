@@ -265,3 +265,36 @@ def test_decode_shapes_column_splits(m, n, k):
     torch.cuda.synchronize()
     assert torch.equal(part, full[:, lo:hi])
     log(f"split ok, worst ratio {worst:.3g}")
+
+
+@pytest.mark.parametrize("m,route", [(16, "decode"), (5, "decode"), (300, "fused"),
+                                     (300, "two-pass")])
+def test_every_scale_byte(m, route):
+    """Hand-built operands whose 16-element blocks cycle through all 254
+    finite scale bytes (every E4M3 code but the NaN one, with T = 0 and with
+    T = 1) and random nibbles of both signs, through the decode-shape kernel
+    (m <= 16, four blocks' scales decoded together), the fused kernel and the
+    two-pass route: every block decode -- T's codebook and the E4M3 scale --
+    against the oracle's dequantization, at tensor scales that are not powers
+    of two."""
+    import paper_2605_31035_amd as M
+    rng = np.random.default_rng(40 + m)
+    n, k = 64, 1024
+    finite = np.array([b for b in range(256) if (b & 0x7F) != 0x7F], np.uint8)
+
+    def operand(rows, s32):
+        nb = rows * (k // 16)
+        sc = np.resize(rng.permutation(finite), nb)
+        rng.shuffle(sc)
+        codes = rng.integers(0, 256, (rows, k // 2), dtype=np.uint8)
+        return Q.Quantized(codes=codes, scales=sc.reshape(rows, k // 16), s32=np.float32(s32),
+                           t=None, sf_code=None, si_code=None, delta=None)
+
+    qa, qw = operand(m, 0.37), operand(n, 1.9)
+    assert set(np.unique(np.concatenate([qa.scales.ravel(), qw.scales.ravel()]))) == set(finite)
+    log(f"gemm every scale byte m={m} route={route}")
+    a = (dev_u8(qa.codes), dev_u8(qa.scales), dev_f32(qa.s32))
+    w = (dev_u8(qw.codes), dev_u8(qw.scales), dev_f32(qw.s32))
+    c = M.mixfp4_gemm(a, w, workspace=True if route == "two-pass" else None)
+    torch.cuda.synchronize()
+    _check(host(c), qa, qw)
